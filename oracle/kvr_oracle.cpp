@@ -1,0 +1,612 @@
+// kvr_oracle.cpp - plain, slow, single-threaded CPU oracle of the batched
+// KV-cache routing/eviction simulation.
+//
+// TEST INFRASTRUCTURE ONLY.  Only tests/, the smoke entry point and the
+// benchmark's CPU-baseline leg may load this library.  It shares no code,
+// header, table or helper with the HIP path.
+//
+// What it computes (one replica, one query at a time, in stream order):
+//   * the online model of Sec. 3.1: per worker i a load and a cache state;
+//     the cache changes only on the worker a query is routed to (Eq. 3);
+//   * cache matching = longest prefix of the query present in the worker's
+//     token-level prefix tree (Sec. 3.2 "Cache Matching");
+//   * LBGR routing (Algorithm 2, Eq. "LBGR-score", Sec. 4.2, App. A
+//     constants): estimated service time + decayed queue load + a per-worker
+//     linear residual model, argmin over workers, load increment on the
+//     routed worker, release of the remaining load and an online update of
+//     the residual model when a query completes, exponential decay every
+//     decay interval;
+//   * RLT insertion/eviction (Algorithm 1, Sec. 4.1): every token of the
+//     path is marked; the marking set is reset to the current token when it
+//     would exceed B; a missing token is loaded after evicting, when the
+//     cache is full, an unmarked leaf token chosen uniformly at random;
+//   * L-LRU (Sec. 3.2): evict the least recently used leaf token.
+//
+// Representation: one trie node per cached token (a token is a position in
+// the prefix tree, i.e. a root path), children kept in an ordered map so a
+// depth-first walk visits leaves in lexicographic order of their root paths.
+//
+// Readings of points the paper leaves open (each one is listed with its
+// reason in the design notes of the repository):
+//   - only the prompt q_j is inserted (responses never recur here);
+//   - the insertion point (the parent of the token being loaded) is never
+//     evicted while its child is loaded, so the tree stays prefix-closed;
+//   - "uniformly at random" = index floor(r * |U| / 2^64) into U sorted by
+//     root path, r = word 0 of Philox4x64-10 with key (seed, replica) and
+//     counter (global query index, worker, draw index, 0);
+//   - if U is empty while the cache is full a new phase is forced
+//     (marking set reset to the current token) and U is recomputed;
+//   - the hit estimate used by the router is the exact per-worker match;
+//   - LBGR quantities are in seconds with the per-1k-token scaling of App. A
+//     (features 0.001*h, 0.001*(|q|-h), load, 1);
+//   - the residual model is updated by normalised LMS (step = the paper's
+//     learning rate) or, optionally, recursive least squares (forgetting
+//     factor = the paper's learning rate); update NONE leaves it at zero;
+//     the error fed to the update is E minus the prediction of the current
+//     model on the features stored at routing time (the squared loss of
+//     Sec. 4.2 is minimised at the current parameters);
+//   - the observed latency comes from a per-worker FIFO fluid queue whose
+//     service time per query is the paper's Cost_ij (Eq. 1) in integer us;
+//   - decay ticks are multiples of the decay interval of simulated time;
+//     pending completions are applied, in FIFO order, at the first arrival
+//     at or after their completion time, before the decay to that arrival.
+//
+// Floating point: IEEE double, every sum left to right, compiled with
+// -ffp-contract=off so no multiply-add is fused.
+#include <cstdint>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <vector>
+
+extern "C" {
+
+// ---------------------------------------------------------------------------
+// public structs (ctypes mirrors them in oracle/oracle.py)
+
+typedef struct orc_config {
+  uint32_t num_workers;       // M in the paper
+  uint32_t cache_tokens;      // B_i (same for every worker)
+  uint64_t seed;              // Philox key word 0
+  int32_t evict;              // 0 = RLT, 1 = L-LRU
+  int32_t update;             // 0 = NLMS, 1 = RLS, 2 = none
+  int32_t u_mode;             // 0 = maintained ordered candidate list, 1 = recompute U at each draw
+  int32_t check;              // 1 = check invariants after every step
+  double alpha_cached;        // s per 1k tokens (App. A: 0 ms per 1k tokens)
+  double alpha_miss;          // s per 1k tokens (App. A: 1000 ms per 1k tokens)
+  double rho;                 // decay factor (App. A: 31/32)
+  int64_t decay_interval_us;  // Delta t (App. A: 20 ms)
+  double lr;                  // App. A: 0.992
+  double nlms_eps;
+  double rls_p0;
+  int64_t true_cached_us;     // observed-latency model, us per cached token
+  int64_t true_miss_us;       // us per missed token
+  int64_t true_out_us;        // us per output token
+} orc_config;
+
+typedef struct orc_worker_stats {
+  uint64_t routed, prompt_tokens, hit_tokens, matched_tokens;
+  uint64_t loads, evictions, phase, cnt, forced_resets, resident;
+  uint64_t digest_sum, digest_xor, marked_count, marked_sum;
+  uint64_t completions, pending_depth, pending_max;
+  uint64_t latency_sum_us, latency_max_us;
+  int64_t backlog_us, last_decay_us;
+  double load_est;
+  double theta[4];
+} orc_worker_stats;
+
+}  // extern "C"
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+// easy as 1, 2, 3", SC'11): ten rounds of two 64x64->128 multiplications,
+// key bumped by the Weyl constants between rounds.
+const uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ULL;
+const uint64_t kPhiloxM1 = 0xCA5A826395121157ULL;
+const uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ULL;
+const uint64_t kPhiloxW1 = 0xBB67AE8584CAA73BULL;
+
+void philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
+  uint64_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+  uint64_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += kPhiloxW0;
+      k1 += kPhiloxW1;
+    }
+    unsigned __int128 p0 = (unsigned __int128)kPhiloxM0 * c[0];
+    unsigned __int128 p1 = (unsigned __int128)kPhiloxM1 * c[2];
+    uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+    uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    uint64_t n0 = hi1 ^ c[1] ^ k0;
+    uint64_t n1 = lo1;
+    uint64_t n2 = hi0 ^ c[3] ^ k1;
+    uint64_t n3 = lo0;
+    c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+  }
+  out[0] = c[0]; out[1] = c[1]; out[2] = c[2]; out[3] = c[3];
+}
+
+// SplitMix64 finaliser, used only for the cache digest.
+uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+// rho^k by square-and-multiply, least significant bit first.
+double pow_int(double rho, uint64_t k) {
+  double res = 1.0, b = rho;
+  while (k) {
+    if (k & 1) res = res * b;
+    b = b * b;
+    k >>= 1;
+  }
+  return res;
+}
+
+struct Node {
+  int32_t tok = 0;
+  int32_t parent = -1;
+  uint32_t mark = 0;      // phase in which the token was last marked (0 = never)
+  uint64_t stamp = 0;     // L-LRU access stamp
+  bool alive = false;
+  std::map<int32_t, int32_t> kids;  // child token -> node id, ordered
+};
+
+struct Pending {
+  int64_t t_route, t_done;
+  double chat;   // estimated service time at routing
+  double base;   // estimated service time + queue load at routing
+  double e_obs;  // observed latency (s)
+  double phi[4];
+};
+
+struct Worker {
+  std::vector<Node> nodes;     // node 0 = root (the empty path)
+  std::vector<int32_t> free_ids;
+  uint64_t size = 0;           // |S_i| in tokens
+  uint32_t phase = 1, cnt = 0; // marking set T = {v : mark(v) == phase}, |T| = cnt
+  std::vector<int32_t> U;      // ordered candidate list (u_mode 0)
+  bool U_valid = false;
+  double P = 0.0;              // estimated queue load
+  double theta[4] = {0, 0, 0, 0};
+  double Pm[16];               // RLS inverse-correlation matrix
+  int64_t tl = 0;              // time of the last decay (us)
+  int64_t Wb = 0;              // observed-latency backlog (us)
+  std::deque<Pending> pend;
+  orc_worker_stats st;
+};
+
+struct Sim {
+  orc_config cfg;
+  uint32_t replica;
+  std::vector<Worker> w;
+  int64_t tprev = 0;
+  int error = 0;
+};
+
+int32_t new_node(Worker& w, int32_t tok, int32_t parent) {
+  int32_t id;
+  if (!w.free_ids.empty()) {
+    id = w.free_ids.back();
+    w.free_ids.pop_back();
+  } else {
+    id = (int32_t)w.nodes.size();
+    w.nodes.emplace_back();
+  }
+  Node& n = w.nodes[id];
+  n.tok = tok;
+  n.parent = parent;
+  n.mark = 0;
+  n.stamp = 0;
+  n.alive = true;
+  n.kids.clear();
+  w.nodes[parent].kids[tok] = id;
+  w.size += 1;
+  return id;
+}
+
+void remove_leaf(Worker& w, int32_t id) {
+  Node& n = w.nodes[id];
+  w.nodes[n.parent].kids.erase(n.tok);
+  n.alive = false;
+  n.kids.clear();
+  w.free_ids.push_back(id);
+  w.size -= 1;
+}
+
+bool is_leaf(const Worker& w, int32_t id) { return id != 0 && w.nodes[id].kids.empty(); }
+
+// U by definition: the leaf tokens of S that are not marked in the current
+// phase, minus the pinned insertion point, in lexicographic order of their
+// root paths (= pre-order of a depth-first walk with ordered children).
+std::vector<int32_t> candidates(const Worker& w, int32_t pinned) {
+  std::vector<int32_t> out, stack;
+  stack.push_back(0);
+  while (!stack.empty()) {
+    int32_t x = stack.back();
+    stack.pop_back();
+    const Node& n = w.nodes[x];
+    if (x != 0 && n.kids.empty()) {
+      if (n.mark != w.phase && x != pinned) out.push_back(x);
+      continue;
+    }
+    for (auto it = n.kids.rbegin(); it != n.kids.rend(); ++it) stack.push_back(it->second);
+  }
+  return out;
+}
+
+int32_t lcp(const Worker& w, const int32_t* q, int32_t L) {
+  int32_t u = 0, h = 0;
+  while (h < L) {
+    auto it = w.nodes[u].kids.find(q[h]);
+    if (it == w.nodes[u].kids.end()) break;
+    u = it->second;
+    h += 1;
+  }
+  return h;
+}
+
+// Mark token v (already in S, or about to be loaded when v < 0), Algorithm 1:
+// add it to T; if |T| reaches B+1 the marking set becomes {v}.
+// Returns true when a new phase started.
+bool mark_token(Worker& w, uint32_t B, int32_t v) {
+  bool newly = (v < 0) || (w.nodes[v].mark != w.phase);
+  bool reset = false;
+  if (newly) {
+    w.cnt += 1;
+    if (w.cnt == B + 1) {
+      w.phase += 1;
+      w.cnt = 1;
+      reset = true;
+    }
+    if (v >= 0) w.nodes[v].mark = w.phase;
+  }
+  return reset;
+}
+
+void erase_value(std::vector<int32_t>& v, int32_t x) {
+  for (size_t k = 0; k < v.size(); ++k)
+    if (v[k] == x) {
+      v.erase(v.begin() + (long)k);
+      return;
+    }
+}
+
+// RLT insertion of path q into worker i (Algorithm 1 for one path).
+void insert_rlt(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
+  Worker& w = s.w[i];
+  const uint32_t B = s.cfg.cache_tokens;
+  uint64_t d = 0;  // draw index within this query
+  int32_t u = 0;   // node of q[0:p)
+  for (int32_t p = 0; p < L; ++p) {
+    auto it = w.nodes[u].kids.find(q[p]);
+    int32_t v = (it == w.nodes[u].kids.end()) ? -1 : it->second;
+    bool was_leaf_cand = (v >= 0) && is_leaf(w, v) && w.nodes[v].mark != w.phase;
+    if (mark_token(w, B, v)) {
+      w.U_valid = false;
+      w.st.phase = w.phase;
+    } else if (was_leaf_cand && w.U_valid) {
+      erase_value(w.U, v);  // a candidate leaf got marked
+    }
+    if (v >= 0) {  // hit: continue along the path
+      u = v;
+      continue;
+    }
+    if (w.size == B) {
+      std::vector<int32_t> Udef;
+      std::vector<int32_t>* Up;
+      if (s.cfg.u_mode == 1) {
+        Udef = candidates(w, u);
+        Up = &Udef;
+      } else {
+        if (!w.U_valid) {
+          w.U = candidates(w, u);
+          w.U_valid = true;
+        }
+        Up = &w.U;
+      }
+      if (Up->empty()) {
+        // no unmarked leaf: start a new phase with T = {t} and recompute U
+        w.phase += 1;
+        w.cnt = 1;
+        w.st.forced_resets += 1;
+        w.st.phase = w.phase;
+        *Up = candidates(w, u);
+        w.U_valid = (s.cfg.u_mode == 0);
+        if (Up->empty()) {
+          s.error |= 4;  // the path alone exceeds the cache (|q| > B)
+          return;
+        }
+      }
+      uint64_t ctr[4] = {jg, (uint64_t)i, d, 0};
+      uint64_t key[2] = {s.cfg.seed, (uint64_t)s.replica};
+      uint64_t r[4];
+      philox4x64_10(ctr, key, r);
+      d += 1;
+      uint64_t k = (uint64_t)(((unsigned __int128)r[0] * (uint64_t)Up->size()) >> 64);
+      int32_t victim = (*Up)[k];
+      int32_t par = w.nodes[victim].parent;
+      remove_leaf(w, victim);
+      w.st.evictions += 1;
+      if (s.cfg.u_mode == 0) {
+        // the parent of the evicted leaf takes its place in the ordered list
+        // if it is now an unmarked, unpinned leaf; otherwise the entry goes.
+        if (par != 0 && w.nodes[par].kids.empty() && w.nodes[par].mark != w.phase && par != u)
+          w.U[k] = par;
+        else
+          w.U.erase(w.U.begin() + (long)k);
+      }
+    }
+    int32_t nv = new_node(w, q[p], u);
+    w.nodes[nv].mark = w.phase;  // marked before it was loaded
+    w.st.loads += 1;
+    u = nv;
+  }
+}
+
+// L-LRU insertion: every access stamps the token; a miss with a full cache
+// evicts the leaf (other than the insertion point) with the oldest stamp.
+void insert_lru(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
+  Worker& w = s.w[i];
+  const uint32_t B = s.cfg.cache_tokens;
+  int32_t u = 0;
+  for (int32_t p = 0; p < L; ++p) {
+    uint64_t stamp = (jg << 32) | (uint64_t)(uint32_t)p;
+    auto it = w.nodes[u].kids.find(q[p]);
+    if (it != w.nodes[u].kids.end()) {
+      u = it->second;
+      w.nodes[u].stamp = stamp;
+      continue;
+    }
+    if (w.size == B) {
+      int32_t best = -1;
+      for (int32_t x = 1; x < (int32_t)w.nodes.size(); ++x) {
+        const Node& n = w.nodes[x];
+        if (!n.alive || !n.kids.empty() || x == u) continue;
+        if (best < 0 || n.stamp < w.nodes[best].stamp) best = x;
+      }
+      if (best < 0) {
+        s.error |= 4;
+        return;
+      }
+      remove_leaf(w, best);
+      w.st.evictions += 1;
+    }
+    int32_t nv = new_node(w, q[p], u);
+    w.nodes[nv].stamp = stamp;
+    w.st.loads += 1;
+    u = nv;
+  }
+}
+
+// Residual-model update with error e = E - E_hat on features phi.
+void online_update(Sim& s, Worker& w, const double phi[4], double e) {
+  const orc_config& c = s.cfg;
+  if (c.update == 0) {  // normalised LMS
+    double ss = phi[0] * phi[0];
+    ss = ss + phi[1] * phi[1];
+    ss = ss + phi[2] * phi[2];
+    ss = ss + phi[3] * phi[3];
+    double g = (c.lr * e) / (c.nlms_eps + ss);
+    for (int a = 0; a < 4; ++a) w.theta[a] = w.theta[a] + g * phi[a];
+  } else if (c.update == 1) {  // recursive least squares, forgetting factor lr
+    double pi[4];
+    for (int a = 0; a < 4; ++a) {
+      double acc = w.Pm[a * 4 + 0] * phi[0];
+      acc = acc + w.Pm[a * 4 + 1] * phi[1];
+      acc = acc + w.Pm[a * 4 + 2] * phi[2];
+      acc = acc + w.Pm[a * 4 + 3] * phi[3];
+      pi[a] = acc;
+    }
+    double den = phi[0] * pi[0];
+    den = den + phi[1] * pi[1];
+    den = den + phi[2] * pi[2];
+    den = den + phi[3] * pi[3];
+    den = c.lr + den;
+    double k[4];
+    for (int a = 0; a < 4; ++a) k[a] = pi[a] / den;
+    for (int a = 0; a < 4; ++a) w.theta[a] = w.theta[a] + k[a] * e;
+    for (int a = 0; a < 4; ++a)
+      for (int b = 0; b < 4; ++b) w.Pm[a * 4 + b] = (w.Pm[a * 4 + b] - k[a] * pi[b]) / c.lr;
+  }
+}
+
+int64_t tick(const orc_config& c, int64_t t) { return t / c.decay_interval_us; }
+
+void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int64_t t, int32_t o,
+          int32_t* route_out, int32_t* hit_out, int32_t* all_hits_row) {
+  const orc_config& c = s.cfg;
+  const uint32_t W = c.num_workers;
+  // 1. completions (update thread) and decay (background thread)
+  for (uint32_t i = 0; i < W; ++i) {
+    Worker& w = s.w[i];
+    while (!w.pend.empty() && w.pend.front().t_done <= t) {
+      Pending pc = w.pend.front();
+      w.pend.pop_front();
+      w.P = w.P * pow_int(c.rho, (uint64_t)(tick(c, pc.t_done) - tick(c, w.tl)));
+      w.tl = pc.t_done;
+      double rem = pc.chat * pow_int(c.rho, (uint64_t)(tick(c, pc.t_done) - tick(c, pc.t_route)));
+      double np = w.P - rem;
+      w.P = np > 0.0 ? np : 0.0;
+      // the squared loss (E - E_hat)^2 is minimised at the current model:
+      // E_hat is re-evaluated with the current theta on the stored features
+      double res = w.theta[0] * pc.phi[0];
+      res = res + w.theta[1] * pc.phi[1];
+      res = res + w.theta[2] * pc.phi[2];
+      res = res + w.theta[3] * pc.phi[3];
+      double ehat_now = pc.base + res;
+      online_update(s, w, pc.phi, pc.e_obs - ehat_now);
+      w.st.completions += 1;
+    }
+    w.P = w.P * pow_int(c.rho, (uint64_t)(tick(c, t) - tick(c, w.tl)));
+    w.tl = t;
+    int64_t nb = w.Wb - (t - s.tprev);
+    w.Wb = nb > 0 ? nb : 0;
+  }
+  s.tprev = t;
+  // 2. match on every worker (no state changes)
+  std::vector<int32_t> h(W);
+  for (uint32_t i = 0; i < W; ++i) {
+    h[i] = lcp(s.w[i], q, L);
+    s.w[i].st.matched_tokens += (uint64_t)h[i];
+    if (all_hits_row) all_hits_row[i] = h[i];
+  }
+  // 3-4. LBGR score and argmin (lowest index on ties)
+  std::vector<double> chat(W), ehat(W), phis(4 * W);
+  uint32_t best = 0;
+  for (uint32_t i = 0; i < W; ++i) {
+    Worker& w = s.w[i];
+    double x1 = (double)h[i] * 0.001;
+    double x2 = (double)(L - h[i]) * 0.001;
+    double x3 = w.P;
+    double x4 = 1.0;
+    double ch = c.alpha_cached * x1 + c.alpha_miss * x2;
+    double res = w.theta[0] * x1;
+    res = res + w.theta[1] * x2;
+    res = res + w.theta[2] * x3;
+    res = res + w.theta[3] * x4;
+    double eh = (ch + w.P) + res;
+    chat[i] = ch;
+    ehat[i] = eh;
+    phis[4 * i + 0] = x1;
+    phis[4 * i + 1] = x2;
+    phis[4 * i + 2] = x3;
+    phis[4 * i + 3] = x4;
+    if (i == 0 || eh < ehat[best]) best = i;
+  }
+  // 5. commit: load increment, observed latency, pending completion
+  Worker& w = s.w[best];
+  double base_route = chat[best] + w.P;
+  w.P = w.P + chat[best];
+  int64_t hb = h[best];
+  int64_t cost_us = c.true_cached_us * hb + c.true_miss_us * ((int64_t)L - hb) + c.true_out_us * (int64_t)o;
+  int64_t e_us = w.Wb + cost_us;
+  w.Wb = w.Wb + cost_us;
+  Pending pc;
+  pc.t_route = t;
+  pc.t_done = t + e_us;
+  pc.chat = chat[best];
+  pc.base = base_route;
+  pc.e_obs = (double)e_us * 1e-6;
+  for (int a = 0; a < 4; ++a) pc.phi[a] = phis[4 * best + a];
+  w.pend.push_back(pc);
+  if (w.pend.size() > w.st.pending_max) w.st.pending_max = w.pend.size();
+  w.st.routed += 1;
+  w.st.prompt_tokens += (uint64_t)L;
+  w.st.hit_tokens += (uint64_t)hb;
+  w.st.latency_sum_us += (uint64_t)e_us;
+  if ((uint64_t)e_us > w.st.latency_max_us) w.st.latency_max_us = (uint64_t)e_us;
+  if (route_out) *route_out = (int32_t)best;
+  if (hit_out) *hit_out = (int32_t)hb;
+  // 6. insert the path into the routed worker's cache
+  if (c.evict == 0)
+    insert_rlt(s, best, q, L, jg);
+  else
+    insert_lru(s, best, q, L, jg);
+}
+
+// Per-token path hash H(v) = mix64(H(parent) + GOLDEN * (tok + 1)), H(root) = 0.
+void digest(const Worker& w, orc_worker_stats& st) {
+  st.digest_sum = st.digest_xor = st.marked_count = st.marked_sum = 0;
+  std::vector<std::pair<int32_t, uint64_t>> stack;
+  stack.push_back({0, 0});
+  uint64_t count = 0;
+  while (!stack.empty()) {
+    auto [x, hx] = stack.back();
+    stack.pop_back();
+    for (auto& kv : w.nodes[x].kids) {
+      uint64_t hv = mix64(hx + 0x9E3779B97F4A7C15ULL * (uint64_t)(int64_t)(kv.first + 1));
+      st.digest_sum += hv;
+      st.digest_xor ^= hv;
+      count += 1;
+      if (w.nodes[kv.second].mark == w.phase) {
+        st.marked_count += 1;
+        st.marked_sum += hv;
+      }
+      stack.push_back({kv.second, hv});
+    }
+  }
+  st.resident = count;
+}
+
+bool check_invariants(const Sim& s) {
+  for (const Worker& w : s.w) {
+    if (w.size > s.cfg.cache_tokens) return false;
+    uint64_t alive = 0, marked = 0;
+    for (size_t x = 1; x < w.nodes.size(); ++x) {
+      const Node& n = w.nodes[x];
+      if (!n.alive) continue;
+      alive += 1;
+      if (!w.nodes[n.parent].alive && n.parent != 0) return false;  // prefix-closed
+      if (n.mark == w.phase) marked += 1;
+    }
+    if (alive != w.size) return false;
+    if (s.cfg.evict == 0 && marked != w.cnt) return false;  // T is a subset of S after an insert
+    if (w.P < 0.0) return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Run replica `replica` over queries [0, n) of the stream from the initial
+// state (empty caches, zero loads, phase 1).  Outputs: route[j], hits[j] and,
+// if all_hits != NULL, all_hits[j*W + i].  wstats[W] receives the final
+// per-worker state.  Returns 0, or a bit set: 1 = bad argument,
+// 2 = invariant violated, 4 = a path longer than the cache.
+int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* tokens,
+            const uint64_t* offsets, const int64_t* arrival_us, const uint16_t* out_len,
+            int32_t* route, int32_t* hits, int32_t* all_hits, orc_worker_stats* wstats) {
+  if (!cfg || cfg->num_workers == 0 || cfg->cache_tokens == 0 || cfg->decay_interval_us <= 0) return 1;
+  Sim s;
+  s.cfg = *cfg;
+  s.replica = replica;
+  s.w.resize(cfg->num_workers);
+  for (Worker& w : s.w) {
+    w.nodes.emplace_back();
+    w.nodes[0].alive = true;
+    std::memset(&w.st, 0, sizeof(w.st));
+    w.st.phase = 1;
+    for (int a = 0; a < 16; ++a) w.Pm[a] = (a % 5 == 0) ? cfg->rls_p0 : 0.0;
+  }
+  for (uint64_t j = 0; j < n; ++j) {
+    const int32_t* q = tokens + offsets[j];
+    int32_t L = (int32_t)(offsets[j + 1] - offsets[j]);
+    int32_t o = out_len ? (int32_t)out_len[j] : 4;
+    step(s, j, q, L, arrival_us[j], o, route ? route + j : nullptr, hits ? hits + j : nullptr,
+         all_hits ? all_hits + j * cfg->num_workers : nullptr);
+    if (s.error) break;
+    if (cfg->check && !check_invariants(s)) {
+      s.error |= 2;
+      break;
+    }
+  }
+  for (uint32_t i = 0; i < cfg->num_workers; ++i) {
+    Worker& w = s.w[i];
+    digest(w, w.st);
+    w.st.phase = w.phase;
+    w.st.cnt = w.cnt;
+    w.st.pending_depth = w.pend.size();
+    w.st.backlog_us = w.Wb;
+    w.st.last_decay_us = w.tl;
+    w.st.load_est = w.P;
+    for (int a = 0; a < 4; ++a) w.st.theta[a] = w.theta[a];
+    if (wstats) wstats[i] = w.st;
+  }
+  return s.error;
+}
+
+// Philox4x64-10 block for (counter, key); exported for the known-answer test.
+void orc_philox4x64_10(const uint64_t* ctr, const uint64_t* key, uint64_t* out) {
+  philox4x64_10(ctr, key, out);
+}
+
+double orc_pow_int(double rho, uint64_t k) { return pow_int(rho, k); }
+
+}  // extern "C"

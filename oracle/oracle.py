@@ -1,0 +1,152 @@
+"""ctypes front end of the CPU oracle (test infrastructure only).
+
+Only ``tests/``, the smoke entry point and the benchmark's CPU-baseline leg
+may use this module.  It never touches the HIP library and the HIP library
+never touches it: the two share only the seeded streams from ``workload``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Any, Dict, Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "kvr_oracle.cpp")
+LIB = os.path.join(HERE, "liboracle.so")
+
+EVICT = {"rlt": 0, "lru": 1}
+UPDATE = {"nlms": 0, "rls": 1, "none": 2}
+
+
+class OrcConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_workers", ctypes.c_uint32),
+        ("cache_tokens", ctypes.c_uint32),
+        ("seed", ctypes.c_uint64),
+        ("evict", ctypes.c_int32),
+        ("update", ctypes.c_int32),
+        ("u_mode", ctypes.c_int32),
+        ("check", ctypes.c_int32),
+        ("alpha_cached", ctypes.c_double),
+        ("alpha_miss", ctypes.c_double),
+        ("rho", ctypes.c_double),
+        ("decay_interval_us", ctypes.c_int64),
+        ("lr", ctypes.c_double),
+        ("nlms_eps", ctypes.c_double),
+        ("rls_p0", ctypes.c_double),
+        ("true_cached_us", ctypes.c_int64),
+        ("true_miss_us", ctypes.c_int64),
+        ("true_out_us", ctypes.c_int64),
+    ]
+
+
+_U64 = ["routed", "prompt_tokens", "hit_tokens", "matched_tokens", "loads", "evictions",
+        "phase", "cnt", "forced_resets", "resident", "digest_sum", "digest_xor",
+        "marked_count", "marked_sum", "completions", "pending_depth", "pending_max",
+        "latency_sum_us", "latency_max_us"]
+
+
+class OrcWorkerStats(ctypes.Structure):
+    _fields_ = ([(n, ctypes.c_uint64) for n in _U64]
+                + [("backlog_us", ctypes.c_int64), ("last_decay_us", ctypes.c_int64),
+                   ("load_est", ctypes.c_double), ("theta", ctypes.c_double * 4)])
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with g++ (plain C++17, no FMA contraction)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(["g++", "-std=c++17", "-O2", "-ffp-contract=off", "-fPIC",
+                               "-shared", "-o", tmp, SRC])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        _lib = ctypes.CDLL(build())
+        _lib.orc_run.restype = ctypes.c_int
+        _lib.orc_run.argtypes = [ctypes.POINTER(OrcConfig), ctypes.c_uint32, ctypes.c_uint64,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.POINTER(OrcWorkerStats)]
+        _lib.orc_philox4x64_10.restype = None
+        _lib.orc_philox4x64_10.argtypes = [ctypes.c_void_p] * 3
+        _lib.orc_pow_int.restype = ctypes.c_double
+        _lib.orc_pow_int.argtypes = [ctypes.c_double, ctypes.c_uint64]
+    return _lib
+
+
+DEFAULTS: Dict[str, Any] = dict(
+    seed=0, evict="rlt", update="nlms", u_mode=0, check=0,
+    alpha_cached=0.0, alpha_miss=1.0, rho=31.0 / 32.0, decay_interval_us=20000,
+    lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
+    true_cached_us=0, true_miss_us=1000, true_out_us=10000)
+
+
+def make_config(W: int, B: int, **kw) -> OrcConfig:
+    p = dict(DEFAULTS)
+    p.update(kw)
+    c = OrcConfig()
+    c.num_workers = W
+    c.cache_tokens = B
+    c.seed = int(p["seed"])
+    c.evict = EVICT[p["evict"]] if isinstance(p["evict"], str) else int(p["evict"])
+    c.update = UPDATE[p["update"]] if isinstance(p["update"], str) else int(p["update"])
+    c.u_mode = int(p["u_mode"])
+    c.check = int(p["check"])
+    for f in ("alpha_cached", "alpha_miss", "rho", "lr", "nlms_eps", "rls_p0"):
+        setattr(c, f, float(p[f]))
+    for f in ("decay_interval_us", "true_cached_us", "true_miss_us", "true_out_us"):
+        setattr(c, f, int(p[f]))
+    return c
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def run(stream, W: int, B: int, replica: int = 0, n: Optional[int] = None,
+        all_hits: bool = False, **kw) -> Dict[str, Any]:
+    """Run one replica of the simulation over the first ``n`` queries."""
+    cfg = make_config(W, B, **kw)
+    n = stream.n if n is None else min(int(n), stream.n)
+    tokens = np.ascontiguousarray(stream.tokens, dtype=np.int32)
+    offsets = np.ascontiguousarray(stream.offsets, dtype=np.uint64)
+    arrival = np.ascontiguousarray(stream.arrival_us, dtype=np.int64)
+    out_len = np.ascontiguousarray(stream.out_len, dtype=np.uint16)
+    route = np.zeros(n, dtype=np.int32)
+    hits = np.zeros(n, dtype=np.int32)
+    ah = np.zeros((n, W), dtype=np.int32) if all_hits else None
+    ws = (OrcWorkerStats * W)()
+    rc = lib().orc_run(ctypes.byref(cfg), replica, n, _ptr(tokens), _ptr(offsets), _ptr(arrival),
+                       _ptr(out_len), _ptr(route), _ptr(hits), _ptr(ah), ws)
+    workers = []
+    for i in range(W):
+        s = ws[i]
+        d = {name: int(getattr(s, name)) for name in _U64}
+        d["backlog_us"] = int(s.backlog_us)
+        d["last_decay_us"] = int(s.last_decay_us)
+        d["load_est"] = float(s.load_est)
+        d["theta"] = [float(x) for x in s.theta]
+        workers.append(d)
+    return {"rc": rc, "route": route, "hits": hits, "all_hits": ah, "workers": workers}
+
+
+def philox4x64_10(counter, key) -> np.ndarray:
+    c = np.asarray(counter, dtype=np.uint64)
+    k = np.asarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib().orc_philox4x64_10(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out
+
+
+def pow_int(rho: float, k: int) -> float:
+    return float(lib().orc_pow_int(rho, k))

@@ -1,0 +1,355 @@
+"""Pins of the CPU oracle against facts it does not compute itself.
+
+* Philox4x64-10 against the generator's published known-answer vector and
+  numpy's independent implementation.
+* rho^k by square-and-multiply against the exact rational power.
+* The whole step against a brute-force model (tests/spec_model.py): caches
+  as sets of token tuples, U recomputed and sorted at every draw, random
+  words from numpy.
+* Cache matching against brute-force LCP over everything routed earlier when
+  nothing is evicted.
+* The lower-bound construction of Theorem 1 (L-LRU misses every query).
+* The uniform-tail construction of Theorem 5 (any policy misses with
+  probability exactly 1/(B-L+2) once full).
+* Exact expected hits of RLT by enumerating every random choice.
+* LBGR closed forms: decayed load, full release on completion, one NLMS
+  step, RLS = exponentially weighted ridge least squares.
+"""
+from fractions import Fraction
+import math
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from workload import generate, small_spec
+from workload.gen import Stream
+import spec_model as SM
+
+
+def _paths_stream(paths, order, gap_us=83333, out_len=4):
+    return generate({"kind": "paths", "paths": paths, "order": order, "gap_us": gap_us,
+                     "out_len": out_len})
+
+
+# ---------------------------------------------------------------------------
+# RNG
+
+def test_philox_known_answer_vector():
+    # Random123 known-answer vector for philox4x64-10, counter 0, key 0
+    out = O.philox4x64_10([0, 0, 0, 0], [0, 0])
+    assert [int(x) for x in out] == [0x16554D9ECA36314C, 0xDB20FE9D672D0FDC,
+                                      0xD7E772CEE186176B, 0x7E68B68AEC7BA23B]
+
+
+def test_philox_matches_numpy():
+    rng = np.random.default_rng(7)
+    for _ in range(200):
+        ctr = [int(x) for x in rng.integers(0, 2**63, size=4)]
+        key = [int(x) for x in rng.integers(0, 2**63, size=2)]
+        ours = O.philox4x64_10(ctr, key)
+        assert int(ours[0]) == SM.philox_word0(key[0], key[1], tuple(ctr))
+
+
+def test_pow_int_exact_within_rounding():
+    rho = 31.0 / 32.0
+    exact_rho = Fraction(31, 32)
+    # (31/32)^k underflows below the smallest subnormal past k ~ 23600
+    assert O.pow_int(rho, 10**7) == 0.0
+    for k in [0, 1, 2, 3, 7, 50, 51, 1000, 4097, 20000]:
+        got = Fraction(O.pow_int(rho, k))
+        if k == 0:
+            assert got == 1
+            continue
+        ex = exact_rho ** k
+        # squaring doubles the relative error of the running base, so the
+        # error of the product is at most about 2k roundings of 2^-53
+        bound = (2 * k + 2 * k.bit_length()) * 2.0 ** -53
+        assert abs(float((got - ex) / ex)) <= bound
+
+
+# ---------------------------------------------------------------------------
+# brute-force model equality on random tiny instances
+
+def _random_tiny_stream(rng, n, vocab, max_len, B):
+    paths = []
+    for _ in range(n):
+        L = int(rng.integers(1, min(max_len, B) + 1))
+        paths.append([int(x) for x in rng.integers(0, vocab, size=L)])
+    gaps = rng.integers(1, 400000, size=n)
+    s = _paths_stream(paths, list(range(n)))
+    s.arrival_us = np.cumsum(gaps).astype(np.int64)
+    s.out_len = rng.integers(0, 6, size=n).astype(np.uint16)
+    return s
+
+
+def _path_hashes(S):
+    """Path hash of every cached path (same definition as the oracle's
+    statistics: H(v) = mix64(H(parent) + G*(tok+1)), H(root) = 0)."""
+    M = (1 << 64) - 1
+
+    def mix(z):
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M
+        return z ^ (z >> 31)
+
+    H = {(): 0}
+    for x in sorted(S, key=len):
+        H[x] = mix((H[x[:-1]] + 0x9E3779B97F4A7C15 * (x[-1] + 1)) & M)
+    return H
+
+
+def _digest_of_set(S, sub=None):
+    H = _path_hashes(S)
+    sub = S if sub is None else sub
+    s = x_ = 0
+    for x in sub:
+        s = (s + H[x]) & ((1 << 64) - 1)
+        x_ ^= H[x]
+    return len(sub), s, x_
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+@pytest.mark.parametrize("update", ["nlms", "rls", "none"])
+def test_oracle_equals_bruteforce_model(evict, update):
+    rng = np.random.default_rng(1000 + 7 * len(evict) + len(update))
+    for case in range(60):
+        W = int(rng.integers(1, 4))
+        B = int(rng.integers(2, 13))
+        vocab = int(rng.integers(2, 5))
+        n = int(rng.integers(5, 30))
+        s = _random_tiny_stream(rng, n, vocab, 6, B)
+        replica = int(rng.integers(0, 1000))
+        kw = dict(evict=evict, update=update, seed=int(rng.integers(0, 2**32)))
+        r = O.run(s, W, B, replica=replica, all_hits=True, check=1, **kw)
+        assert r["rc"] == 0
+        sim, routes, hits, allh = SM.run_spec(s, W, B, replica=replica, **kw)
+        np.testing.assert_array_equal(r["route"], routes)
+        np.testing.assert_array_equal(r["hits"], hits)
+        np.testing.assert_array_equal(r["all_hits"], allh)
+        for i in range(W):
+            ws, sw = r["workers"][i], sim.w[i]
+            assert ws["evictions"] == sw.evictions and ws["loads"] == sw.loads
+            cnt, dsum, dxor = _digest_of_set(sw.S)
+            assert (ws["resident"], ws["digest_sum"], ws["digest_xor"]) == (cnt, dsum, dxor)
+            assert ws["theta"] == sw.theta
+            assert ws["load_est"] == sw.P
+            if evict == "rlt":
+                marked = {x for x in sw.S if sw.mark.get(x, 0) == sw.phase}
+                assert ws["marked_count"] == len(marked) == ws["cnt"] == sw.cnt
+                assert ws["marked_sum"] == _digest_of_set(sw.S, marked)[1]
+                assert ws["phase"] == sw.phase and ws["forced_resets"] == sw.forced
+
+
+def test_candidate_list_equals_definition():
+    """The maintained ordered candidate list gives the same run as
+    recomputing U from its definition at every draw."""
+    rng = np.random.default_rng(5)
+    for case in range(12):
+        sp = small_spec(n=int(rng.integers(100, 250)), groups=int(rng.integers(2, 8)),
+                        prefix_len=(4, 30), suffix_len=(1, 20), vocab=int(rng.integers(3, 40)),
+                        seed=case)
+        s = generate(sp)
+        W = int(rng.integers(1, 4))
+        B = int(max(s.max_len, rng.integers(40, 300)))
+        a = O.run(s, W, B, replica=case, u_mode=0, all_hits=True)
+        b = O.run(s, W, B, replica=case, u_mode=1, all_hits=True)
+        np.testing.assert_array_equal(a["route"], b["route"])
+        np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
+        assert a["workers"] == b["workers"]
+
+
+# ---------------------------------------------------------------------------
+# matching: brute-force LCP when the cache never evicts
+
+def test_match_is_lcp_over_routed_history():
+    s = generate(small_spec(n=300, groups=5, prefix_len=(5, 25), suffix_len=(1, 15), vocab=6))
+    W, B = 3, 10**6
+    r = O.run(s, W, B, all_hits=True)
+    assert sum(w["evictions"] for w in r["workers"]) == 0
+    qs = [tuple(int(x) for x in s.query(j)) for j in range(s.n)]
+    for j in range(s.n):
+        for i in range(W):
+            best = 0
+            for k in range(j):
+                if r["route"][k] == i:
+                    a, b = qs[j], qs[k]
+                    l = 0
+                    while l < min(len(a), len(b)) and a[l] == b[l]:
+                        l += 1
+                    best = max(best, l)
+            assert r["all_hits"][j, i] == best
+
+
+# ---------------------------------------------------------------------------
+# constructions from the proofs
+
+def _tail_paths(B, L, vocab_base=100):
+    n = B - L + 2
+    prefix = list(range(vocab_base, vocab_base + L - 1))
+    return [prefix + [k] for k in range(n)], n
+
+
+def test_lru_worst_case_misses_every_query():
+    """Theorem 1 lower bound: B-L+2 paths share an (L-1)-token prefix and
+    differ in the last token; queried cyclically, L-LRU misses the tail of
+    every query once the cache is full."""
+    for B, L in [(10, 4), (33, 7), (64, 2)]:
+        paths, n = _tail_paths(B, L)
+        order = list(range(n)) * 6
+        s = _paths_stream(paths, order)
+        r = O.run(s, 1, B, evict="lru", check=1)
+        assert r["rc"] == 0
+        assert (r["hits"][n:] == L - 1).all()
+        assert r["workers"][0]["evictions"] == len(order) - n + 1
+
+
+def test_uniform_tail_miss_probability():
+    """Theorem 5 distribution: tails drawn uniformly from n = B-L+2 paths;
+    once full, the cache holds n-1 tails whatever the policy, so each query
+    misses with probability exactly 1/n."""
+    B, L = 16, 4
+    paths, n = _tail_paths(B, L)
+    rng = np.random.default_rng(11)
+    N, skip = 3000, 500
+    for evict, reps in [("lru", 1), ("rlt", 40)]:
+        misses = total = 0
+        for rep in range(reps):
+            order = [int(x) for x in rng.integers(0, n, size=N)]
+            s = _paths_stream(paths, order)
+            r = O.run(s, 1, B, evict=evict, replica=rep, check=1)
+            h = r["hits"][skip:]
+            assert (h >= L - 1).all()
+            misses += int((h == L - 1).sum())
+            total += h.shape[0]
+        p = 1.0 / n
+        sd = math.sqrt(total * p * (1 - p))
+        assert abs(misses - total * p) < 4 * sd, (evict, misses, total * p, sd)
+
+
+EXACT_CASES = [
+    (5, [(0, 1, 2), (0, 1, 3), (0, 2), (1, 2, 3), (0, 1, 2), (1, 2), (0, 1, 3), (0, 2, 1),
+         (1, 2, 3), (0, 1, 2)]),
+    (4, [(0, 1), (0, 2), (1, 0), (0, 1, 2), (1, 1), (0, 2), (2,), (0, 1), (1, 0, 1), (0, 2)]),
+    (6, [(3, 1, 2, 0), (3, 1, 0), (2, 2, 2), (3, 1, 2, 1), (0,), (2, 2, 1), (3, 1, 2, 0),
+         (3, 0), (2, 2, 2)]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(EXACT_CASES)))
+def test_rlt_mean_hits_match_exact_enumeration(case):
+    B, queries = EXACT_CASES[case]
+    exact = SM.expected_hits(queries, B)
+    s = _paths_stream([list(q) for q in queries], list(range(len(queries))))
+    R = 20000
+    tot = np.zeros(R)
+    per = np.zeros((R, len(queries)))
+    for rep in range(R):
+        r = O.run(s, 1, B, replica=rep)
+        per[rep] = r["hits"]
+        tot[rep] = r["hits"].sum()
+    ex_tot = float(sum(exact))
+    sd = tot.std(ddof=1) / math.sqrt(R)
+    assert abs(tot.mean() - ex_tot) < 4 * sd + 1e-12, (tot.mean(), ex_tot, sd)
+    # every query's mean too (4.5 sigma: several comparisons)
+    for j, e in enumerate(exact):
+        sdj = per[:, j].std(ddof=1) / math.sqrt(R)
+        assert abs(per[:, j].mean() - float(e)) < 4.5 * sdj + 1e-12
+
+
+# ---------------------------------------------------------------------------
+# LBGR closed forms
+
+def test_decayed_load_and_routing_away():
+    """A query routed to worker 0 at t1 leaves load C*rho^(ticks) at t2, so
+    an equal query at t2 goes to the idle worker 1."""
+    dt = 20000
+    L1 = 800  # completes at t1 + 1000*L1 + 40000 us, after t2
+    t1, t2 = 30000, 30000 + 37 * dt + 1234
+    s = _paths_stream([list(range(1, L1 + 1)), [7000, 8, 9, 10, 11]], [0, 1])
+    s.arrival_us = np.array([t1, t2], np.int64)
+    r = O.run(s, 2, 1000, update="none")
+    assert list(r["route"]) == [0, 1]
+    c = L1 * 0.001
+    k = t2 // dt - t1 // dt
+    got = Fraction(r["workers"][0]["load_est"])
+    ex = Fraction(c) * Fraction(31, 32) ** k
+    assert abs(float((got - ex) / ex)) < 1e-14
+    assert r["workers"][1]["load_est"] == 5 * 0.001
+
+
+def test_release_returns_load_to_zero():
+    """After its completion a query's remaining share is released, so a
+    lone query leaves no load and the next query ties and goes to worker 0."""
+    L = 20
+    s = _paths_stream([list(range(L)), list(range(100, 100 + L))], [0, 1])
+    done = 1000 * L + 10000 * 4
+    s.arrival_us = np.array([5000, 5000 + done + 7], np.int64)
+    r = O.run(s, 2, 100, update="none")
+    assert list(r["route"]) == [0, 0]
+    # worker 0's load is exactly the second query's estimate
+    assert r["workers"][0]["load_est"] == L * 0.001
+    assert r["workers"][0]["completions"] == 1
+
+
+def test_nlms_single_step_closed_form():
+    L, o = 37, 3
+    s = _paths_stream([list(range(L)), list(range(200, 210))], [0, 1], out_len=o)
+    s.arrival_us = np.array([0, 10**9], np.int64)
+    r = O.run(s, 1, 1000, update="nlms")
+    phi = np.array([0.0, L * 0.001, 0.0, 1.0])
+    E = (1000 * L + 10000 * o) * 1e-6
+    e = E - (L * 0.001 + 0.0)
+    theta = 0.992 * e / (1e-9 + phi @ phi) * phi
+    np.testing.assert_allclose(r["workers"][0]["theta"], theta, rtol=1e-13, atol=1e-18)
+
+
+def test_rls_equals_weighted_ridge_least_squares():
+    """RLS with forgetting factor lam and P0 = p0*I minimises
+    sum_t lam^(n-t) (y_t - theta.phi_t)^2 + lam^n |theta|^2 / p0."""
+    rng = np.random.default_rng(3)
+    sp = small_spec(n=120, groups=4, prefix_len=(10, 60), suffix_len=(5, 40), vocab=30)
+    s = generate(sp)
+    s.arrival_us = (np.arange(1, s.n + 1) * 10**8).astype(np.int64)  # every query completes first
+    s.out_len = rng.integers(0, 9, size=s.n).astype(np.uint16)
+    lam, p0 = 0.992, 100.0
+    r = O.run(s, 1, 10**6, update="rls", lr=lam, rls_p0=p0)
+    L = s.lengths
+    h = r["hits"].astype(np.int64)
+    n_upd = s.n - 1  # the last query has not completed
+    Phi = np.stack([h * 0.001, (L - h) * 0.001, np.zeros_like(h, float), np.ones_like(h, float)], 1)[:n_upd]
+    E = (1000 * (L - h) + 10000 * s.out_len.astype(np.int64)) * 1e-6
+    y = (E - (L - h) * 0.001)[:n_upd]
+    wts = lam ** np.arange(n_upd - 1, -1, -1, dtype=float)
+    A = (Phi * wts[:, None]).T @ Phi + (lam ** n_upd / p0) * np.eye(4)
+    b = (Phi * wts[:, None]).T @ y
+    theta = np.linalg.solve(A, b)
+    np.testing.assert_allclose(r["workers"][0]["theta"], theta, rtol=1e-7, atol=1e-9)
+
+
+def test_ties_route_to_lowest_index():
+    s = _paths_stream([[1, 2], [3, 4], [5, 6]], [0, 1, 2])
+    s.arrival_us = np.array([10**9, 2 * 10**9, 3 * 10**9], np.int64)
+    r = O.run(s, 4, 100, update="none")
+    assert list(r["route"]) == [0, 0, 0]
+
+
+# ---------------------------------------------------------------------------
+# invariants on generated workloads
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_invariants_hold(seed):
+    s = generate(small_spec(n=400, groups=7, prefix_len=(10, 60), suffix_len=(5, 40),
+                            vocab=20, seed=seed))
+    W, B = 3, 250
+    r = O.run(s, W, B, replica=seed, check=1, all_hits=True)
+    assert r["rc"] == 0
+    L = s.lengths
+    assert (r["all_hits"] <= L[:, None]).all() and (r["all_hits"] >= 0).all()
+    assert ((r["route"] >= 0) & (r["route"] < W)).all()
+    assert sum(w["routed"] for w in r["workers"]) == s.n
+    for w in r["workers"]:
+        assert w["resident"] <= B
+        assert w["resident"] == w["loads"] - w["evictions"]
+        assert w["marked_count"] == w["cnt"] <= B
+        assert w["load_est"] >= 0.0
