@@ -1,0 +1,174 @@
+/*
+ * kvr.h - C ABI of the batched KV-cache routing / eviction simulator.
+ *
+ * The library simulates R independent replicas of the online problem of
+ * Sec. 3.1 (Eqs. 1-3, Table 1): M = W workers, each with a prefix-sharing
+ * token cache of B tokens, receive an ordered stream of queries q_j.  For
+ * every query and every replica the library
+ *   1. applies completions and load decay (Algorithm 2, update and decay
+ *      threads; Sec. 4.2 "Queue Load Estimation"),
+ *   2. computes h_ij, the longest prefix of q_j present in worker i's cache
+ *      (Sec. 3.2 "Cache Matching"), for every worker,
+ *   3. routes q_j to argmin_i of the LBGR score (Algorithm 2, routing
+ *      thread; Eq. LBGR-score), lowest index on ties, and adds the estimated
+ *      service time to that worker's load (Eq. 2 with the estimate),
+ *   4. inserts q_j into the routed worker's cache with RLT (Algorithm 1):
+ *      mark every token of the path, reset the marking set when it would
+ *      exceed B, and evict a uniformly random unmarked leaf token before
+ *      loading a missing token into a full cache (Eq. 3: no other cache
+ *      changes).
+ * Replicas see the same stream and differ only in the random key of RLT.
+ *
+ * Conventions
+ *   - Every pointer named d_* is a device pointer (e.g. a torch tensor's
+ *     data_ptr()) on the device current when kvr_init_replicas was called.
+ *     h_* pointers are host memory.  The caller owns every buffer it passes,
+ *     including the workspace; the library owns only the small host context.
+ *   - kvr_route_batch is asynchronous on the context's stream (a hipStream_t
+ *     given at init; NULL = the default stream).  Its outputs are valid after
+ *     that stream has been synchronised; kvr_stats and kvr_check synchronise.
+ *   - A batch is a transport unit only: query k of a batch has global index
+ *     j0 + k, where j0 is the number of queries already routed, so splitting
+ *     a stream into batches differently gives identical results.
+ *   - Errors are status codes; nothing is thrown across the ABI.  Errors the
+ *     host can see (bad configuration, bad arguments, NULL pointers) return
+ *     before any device work.  Errors only the device can see (a query of
+ *     length 0 or above max_query_tokens, a negative token, decreasing
+ *     arrival times, a full completion ring, a full node table or arena) set
+ *     a sticky status word in the workspace: an invalid batch is rejected
+ *     as a whole before any state changes (KVR_EINVAL), a capacity overflow
+ *     stops the replica where it happened (KVR_ECAPACITY; re-initialise).
+ *     kvr_check / kvr_stats report it, and later kvr_route_batch calls
+ *     return KVR_ESTATE once the host has seen it.
+ */
+#ifndef KVR_H
+#define KVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVR_ABI_VERSION 1u
+
+typedef enum kvr_status {
+  KVR_OK = 0,
+  KVR_EINVAL = -1,    /* invalid configuration, argument or batch content */
+  KVR_ENOMEM = -2,    /* workspace too small */
+  KVR_EDEVICE = -3,   /* HIP runtime error (no device, launch failure) */
+  KVR_ECAPACITY = -4, /* a device-side capacity was exceeded */
+  KVR_ESTATE = -5     /* the context is in an error state */
+} kvr_status;
+
+enum { KVR_EVICT_RLT = 0, KVR_EVICT_LRU = 1 }; /* L-LRU on the device: not built yet */
+enum { KVR_ROUTE_LBGR = 0 };
+enum { KVR_UPD_NLMS = 0, KVR_UPD_RLS = 1, KVR_UPD_NONE = 2 };
+
+/* Device status bits (kvr_check reports the first one as a kvr_status). */
+enum {
+  KVR_DEV_BAD_LENGTH = 1u,   /* a query of length 0 or > max_query_tokens  */
+  KVR_DEV_BAD_TOKEN = 2u,    /* a negative token id                        */
+  KVR_DEV_BAD_ARRIVAL = 4u,  /* arrival times decrease                     */
+  KVR_DEV_PENDING_FULL = 8u, /* completion ring of a worker is full        */
+  KVR_DEV_NODES_FULL = 16u,  /* node table of a worker is full             */
+  KVR_DEV_ARENA_FULL = 32u,  /* token/child arena of a worker is full      */
+  KVR_DEV_INTERNAL = 64u     /* an internal consistency check failed       */
+};
+
+typedef struct kvr_config {
+  uint32_t abi_version;      /* KVR_ABI_VERSION                                    */
+  uint32_t struct_size;      /* sizeof(kvr_config)                                 */
+  uint32_t num_replicas;     /* R >= 1                                             */
+  uint32_t num_workers;      /* W = M of Sec. 3.1, 1..64                           */
+  uint32_t cache_tokens;     /* B_i (same for all workers), >= 1                   */
+  uint32_t max_query_tokens; /* bound on |q_j|, 1..cache_tokens (|q_j| <= B_i)      */
+  uint64_t seed;             /* Philox key word 0; key word 1 = replica index      */
+  int32_t evict;             /* KVR_EVICT_*                                        */
+  int32_t router;            /* KVR_ROUTE_*                                        */
+  int32_t update;            /* KVR_UPD_*                                          */
+  uint32_t pending_capacity; /* completion ring per (replica, worker), >= 1        */
+  uint32_t node_capacity;    /* nodes per (replica, worker); 0 = cache_tokens + 3  */
+  uint32_t arena_words;      /* words per semispace per (replica, worker), 0 = default
+                                2*B + 2*max_query_tokens + 4096; else >= B + 2*max_q + 64 */
+  double alpha_cached;       /* s per 1k cached tokens (App. A: 0)                 */
+  double alpha_miss;         /* s per 1k missed tokens (App. A: 1)                 */
+  double rho;                /* load decay factor (App. A: 31/32), in (0, 1]       */
+  int64_t decay_interval_us; /* decay interval (App. A: 20 ms), > 0                */
+  double lr;                 /* NLMS step / RLS forgetting factor (App. A: 0.992)  */
+  double nlms_eps;           /* NLMS regulariser (1e-9)                            */
+  double rls_p0;             /* RLS initial inverse correlation scale (100)        */
+  int64_t true_cached_us;    /* observed-latency model: us per cached token (0)    */
+  int64_t true_miss_us;      /* us per missed token (1000)                         */
+  int64_t true_out_us;       /* us per output token (10000)                        */
+} kvr_config;
+
+/* Final per-(replica, worker) state and counters (kvr_stats). */
+typedef struct kvr_worker_stats {
+  uint64_t routed, prompt_tokens, hit_tokens, matched_tokens;
+  uint64_t loads, evictions, phase, cnt, forced_resets, resident;
+  uint64_t digest_sum, digest_xor, marked_count, marked_sum;
+  uint64_t completions, pending_depth, pending_max;
+  uint64_t latency_sum_us, latency_max_us;
+  int64_t backlog_us, last_decay_us;
+  double load_est;
+  double theta[4];
+  uint64_t nodes, gc_runs; /* layout-dependent, informative only */
+} kvr_worker_stats;
+
+typedef struct kvr_ctx kvr_ctx;
+
+/* Fill *cfg with the paper's constants (App. A) and the defaults above for
+ * the given sizes.  Pure host function. */
+void kvr_config_default(kvr_config* cfg, uint32_t num_replicas, uint32_t num_workers,
+                        uint32_t cache_tokens, uint32_t max_query_tokens);
+
+/* Bytes of device workspace kvr_init_replicas needs for *cfg.  Pure host
+ * function, no device call.  KVR_EINVAL for an invalid configuration. */
+kvr_status kvr_workspace_size(const kvr_config* cfg, size_t* bytes);
+
+/* Lay the replicas out in d_workspace (>= kvr_workspace_size bytes, caller
+ * owned, any content) and initialise them on hip_stream (a hipStream_t, or
+ * NULL): empty caches, phase 1, zero loads and models.  On success *out is a
+ * new context (free with kvr_destroy).  Asynchronous. */
+kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t bytes,
+                             void* hip_stream, kvr_ctx** out);
+
+/* Route n queries for every replica (Algorithm 2 routing + Algorithm 1
+ * insertion).  d_tokens: concatenated token ids (int32, >= 0); d_offsets:
+ * n+1 uint64 offsets into d_tokens (d_offsets[0] may be non-zero);
+ * d_arrival_us: n arrival times in us, non-decreasing, also across calls;
+ * d_out_len: n output lengths, or NULL for 4 (the paper's default).
+ * Outputs (each optional, NULL to skip): d_route[r*n + k] = routed worker
+ * of query k for replica r; d_hits[r*n + k] = h of the routed worker;
+ * d_all_hits[(r*n + k)*W + i] = h_ik for every worker.  n = 0 is a no-op.
+ * Asynchronous on the context's stream. */
+kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens,
+                           const uint64_t* d_offsets, const int64_t* d_arrival_us,
+                           const uint16_t* d_out_len, int32_t* d_route, int32_t* d_hits,
+                           int32_t* d_all_hits);
+
+/* Synchronise the stream and copy the state of every (replica, worker) into
+ * h_out[r*W + i] (R*W entries, host memory).  Returns the device status as
+ * kvr_check does. */
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out);
+
+/* Synchronise the stream and return the sticky device status as a
+ * kvr_status; *h_bits (optional) receives the raw KVR_DEV_* bits. */
+kvr_status kvr_check(kvr_ctx* ctx, uint32_t* h_bits);
+
+/* Number of queries routed so far (the global index of the next query). */
+uint64_t kvr_queries_done(const kvr_ctx* ctx);
+
+/* Free the host context.  Does not free or touch the caller's workspace. */
+void kvr_destroy(kvr_ctx* ctx);
+
+/* Message for the last failure on this thread ("" if none). */
+const char* kvr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVR_H */

@@ -1,0 +1,273 @@
+// kvr_api.cpp - host side of the C ABI declared in include/kvr.h.
+//
+// Validates configurations and arguments, computes the workspace layout,
+// keeps the small host context (stream, layout, constants, number of
+// queries routed) and launches the kernels of kvr_device.hip.  Every device
+// buffer belongs to the caller.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "kvr_layout.h"
+
+namespace kvr {
+hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st);
+hipError_t launch_step(const StepArgs& a, hipStream_t st);
+hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st);
+hipError_t set_step_lds_limit(size_t bytes);
+}  // namespace kvr
+
+struct kvr_ctx {
+  kvr::Layout L;
+  kvr::Consts C;
+  char* ws;
+  hipStream_t stream;
+  int device;
+  uint64_t queries_done;
+  uint32_t seen_bits;  // device status bits already reported to the host
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+kvr_status fail(kvr_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+kvr_status fail_hip(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return KVR_EDEVICE;
+}
+
+bool finite(double x) { return std::isfinite(x); }
+
+kvr_status validate(const kvr_config* c) {
+  if (!c) return fail(KVR_EINVAL, "config is NULL");
+  if (c->abi_version != KVR_ABI_VERSION) return fail(KVR_EINVAL, "abi_version mismatch");
+  if (c->struct_size != sizeof(kvr_config)) return fail(KVR_EINVAL, "struct_size mismatch");
+  if (c->num_replicas < 1) return fail(KVR_EINVAL, "num_replicas must be >= 1");
+  if (c->num_workers < 1 || c->num_workers > kvr::kMaxWorkers)
+    return fail(KVR_EINVAL, "num_workers must be in 1..64");
+  if (c->cache_tokens < 1 || c->cache_tokens > (1u << 30))
+    return fail(KVR_EINVAL, "cache_tokens must be in 1..2^30");
+  if (c->max_query_tokens < 1 || c->max_query_tokens > c->cache_tokens)
+    return fail(KVR_EINVAL, "max_query_tokens must be in 1..cache_tokens");
+  if (c->max_query_tokens > 32768)
+    return fail(KVR_EINVAL, "max_query_tokens above 32768 does not fit the LDS staging buffer");
+  if (c->evict == KVR_EVICT_LRU)
+    return fail(KVR_EINVAL, "L-LRU eviction is not built on the device (RLT only)");
+  if (c->evict != KVR_EVICT_RLT) return fail(KVR_EINVAL, "unknown evict policy");
+  if (c->router != KVR_ROUTE_LBGR) return fail(KVR_EINVAL, "unknown router");
+  if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
+    return fail(KVR_EINVAL, "unknown update rule");
+  if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
+    return fail(KVR_EINVAL, "pending_capacity must be in 1..2^28");
+  if (c->node_capacity != 0 && (c->node_capacity < 2 || c->node_capacity > (1u << 30)))
+    return fail(KVR_EINVAL, "node_capacity must be 0 or in 2..2^30");
+  const uint64_t min_arena = (uint64_t)c->cache_tokens + 2ull * c->max_query_tokens + 64ull;
+  if (c->arena_words != 0 && c->arena_words < min_arena)
+    return fail(KVR_EINVAL, "arena_words must be 0 or >= cache_tokens + 2*max_query_tokens + 64");
+  const uint64_t dflt_arena = 2ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
+  if (c->arena_words == 0 && dflt_arena >= (1ull << 32))
+    return fail(KVR_EINVAL, "cache too large for 32-bit arena offsets");
+  if (!finite(c->alpha_cached) || !finite(c->alpha_miss))
+    return fail(KVR_EINVAL, "alpha_cached/alpha_miss must be finite");
+  if (!finite(c->rho) || !(c->rho > 0.0) || c->rho > 1.0) return fail(KVR_EINVAL, "rho must be in (0, 1]");
+  if (c->decay_interval_us <= 0) return fail(KVR_EINVAL, "decay_interval_us must be > 0");
+  if (!finite(c->lr) || !(c->lr > 0.0)) return fail(KVR_EINVAL, "lr must be finite and > 0");
+  if (!finite(c->nlms_eps) || c->nlms_eps < 0.0) return fail(KVR_EINVAL, "nlms_eps must be >= 0");
+  if (!finite(c->rls_p0) || !(c->rls_p0 > 0.0)) return fail(KVR_EINVAL, "rls_p0 must be > 0");
+  if (c->true_cached_us < 0 || c->true_miss_us < 0 || c->true_out_us < 0)
+    return fail(KVR_EINVAL, "true_*_us must be >= 0");
+  if (c->true_cached_us > (1ll << 32) || c->true_miss_us > (1ll << 32) || c->true_out_us > (1ll << 32))
+    return fail(KVR_EINVAL, "true_*_us too large");
+  return KVR_OK;
+}
+
+kvr_status status_from_bits(uint32_t bits) {
+  if (bits & (KVR_DEV_BAD_LENGTH | KVR_DEV_BAD_TOKEN | KVR_DEV_BAD_ARRIVAL)) return KVR_EINVAL;
+  if (bits & (KVR_DEV_PENDING_FULL | KVR_DEV_NODES_FULL | KVR_DEV_ARENA_FULL)) return KVR_ECAPACITY;
+  if (bits) return KVR_ESTATE;
+  return KVR_OK;
+}
+
+std::string describe_bits(uint32_t bits) {
+  std::string s;
+  const char* names[] = {"query length out of range", "negative token id", "arrival times decrease",
+                         "completion ring full", "node table full", "arena full",
+                         "internal consistency check failed"};
+  for (int b = 0; b < 7; ++b)
+    if (bits & (1u << b)) {
+      if (!s.empty()) s += "; ";
+      s += names[b];
+    }
+  return s;
+}
+
+}  // namespace
+
+extern "C" {
+
+void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint32_t maxL) {
+  if (!c) return;
+  std::memset(c, 0, sizeof(*c));
+  c->abi_version = KVR_ABI_VERSION;
+  c->struct_size = sizeof(kvr_config);
+  c->num_replicas = R;
+  c->num_workers = W;
+  c->cache_tokens = B;
+  c->max_query_tokens = maxL;
+  c->seed = 0;
+  c->evict = KVR_EVICT_RLT;
+  c->router = KVR_ROUTE_LBGR;
+  c->update = KVR_UPD_NLMS;
+  c->pending_capacity = 4096;
+  c->node_capacity = 0;
+  c->arena_words = 0;
+  c->alpha_cached = 0.0;  // App. A: 0 ms per 1k cached tokens
+  c->alpha_miss = 1.0;    // App. A: 1000 ms per 1k missed tokens
+  c->rho = 31.0 / 32.0;   // App. A
+  c->decay_interval_us = 20000;  // App. A: 20 ms
+  c->lr = 0.992;                 // App. A
+  c->nlms_eps = 1e-9;
+  c->rls_p0 = 100.0;
+  c->true_cached_us = 0;
+  c->true_miss_us = 1000;
+  c->true_out_us = 10000;
+}
+
+kvr_status kvr_workspace_size(const kvr_config* cfg, size_t* bytes) {
+  kvr_status st = validate(cfg);
+  if (st != KVR_OK) return st;
+  if (!bytes) return fail(KVR_EINVAL, "bytes is NULL");
+  *bytes = (size_t)kvr::make_layout(*cfg).total;
+  return KVR_OK;
+}
+
+kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t bytes, void* hip_stream,
+                             kvr_ctx** out) {
+  kvr_status st = validate(cfg);
+  if (st != KVR_OK) return st;
+  if (!out) return fail(KVR_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!d_workspace) return fail(KVR_EINVAL, "workspace is NULL");
+  if (((uintptr_t)d_workspace) % 256 != 0) return fail(KVR_EINVAL, "workspace must be 256-byte aligned");
+  kvr::Layout L = kvr::make_layout(*cfg);
+  if (bytes < L.total)
+    return fail(KVR_ENOMEM, "workspace too small: need " + std::to_string(L.total) + " bytes");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  const size_t lds = (size_t)L.maxL * sizeof(int32_t);
+  if (lds > 65536) {
+    e = kvr::set_step_lds_limit(lds);
+    if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
+  }
+  kvr_ctx* c = new (std::nothrow) kvr_ctx;
+  if (!c) return fail(KVR_ENOMEM, "host allocation failed");
+  c->L = L;
+  c->C.seed = cfg->seed;
+  c->C.alpha_cached = cfg->alpha_cached;
+  c->C.alpha_miss = cfg->alpha_miss;
+  c->C.rho = cfg->rho;
+  c->C.lr = cfg->lr;
+  c->C.nlms_eps = cfg->nlms_eps;
+  c->C.rls_p0 = cfg->rls_p0;
+  c->C.dt_us = cfg->decay_interval_us;
+  c->C.true_cached_us = cfg->true_cached_us;
+  c->C.true_miss_us = cfg->true_miss_us;
+  c->C.true_out_us = cfg->true_out_us;
+  c->C.update = cfg->update;
+  c->C.evict = cfg->evict;
+  c->ws = static_cast<char*>(d_workspace);
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->device = dev;
+  c->queries_done = 0;
+  c->seen_bits = 0;
+  e = kvr::launch_init(c->ws, L, cfg->rls_p0, c->stream);
+  if (e != hipSuccess) {
+    delete c;
+    return fail_hip(e, "init kernel launch");
+  }
+  *out = c;
+  return KVR_OK;
+}
+
+kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens, const uint64_t* d_offsets,
+                           const int64_t* d_arrival_us, const uint16_t* d_out_len, int32_t* d_route,
+                           int32_t* d_hits, int32_t* d_all_hits) {
+  if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
+  if (ctx->seen_bits) return fail(KVR_ESTATE, "context is in an error state: " + describe_bits(ctx->seen_bits));
+  if (n == 0) return KVR_OK;
+  if (!d_tokens || !d_offsets || !d_arrival_us) return fail(KVR_EINVAL, "tokens, offsets and arrival_us are required");
+  if (n > (1u << 30)) return fail(KVR_EINVAL, "batch too large");
+  kvr::StepArgs a;
+  a.ws = ctx->ws;
+  a.L = ctx->L;
+  a.C = ctx->C;
+  a.tokens = d_tokens;
+  a.offsets = d_offsets;
+  a.arrival = d_arrival_us;
+  a.out_len = d_out_len;
+  a.route = d_route;
+  a.hits = d_hits;
+  a.all_hits = d_all_hits;
+  a.n = n;
+  a.j0 = ctx->queries_done;
+  hipError_t e = kvr::launch_step(a, ctx->stream);
+  if (e != hipSuccess) return fail_hip(e, "step kernel launch");
+  ctx->queries_done += n;
+  return KVR_OK;
+}
+
+kvr_status kvr_check(kvr_ctx* ctx, uint32_t* h_bits) {
+  if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  kvr::GlobalHdr g;
+  e = hipMemcpy(&g, ctx->ws + ctx->L.off_global, sizeof(g), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpy(status)");
+  const uint32_t bits = g.status;
+  ctx->seen_bits |= bits;
+  if (h_bits) *h_bits = bits;
+  kvr_status st = status_from_bits(bits);
+  if (st != KVR_OK) {
+    std::string msg = describe_bits(bits);
+    if (g.err_taken)
+      msg += " (first: check " + std::to_string(g.err_check) + ", replica " + std::to_string(g.err_replica) +
+             ", query " + std::to_string(g.err_query) + ", values " + std::to_string(g.err_val[0]) + " " +
+             std::to_string(g.err_val[1]) + " " + std::to_string(g.err_val[2]) + ")";
+    return fail(st, msg);
+  }
+  return KVR_OK;
+}
+
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out) {
+  if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
+  if (!h_out) return fail(KVR_EINVAL, "h_out is NULL");
+  uint32_t bits = 0;
+  kvr_status st = kvr_check(ctx, &bits);
+  hipError_t e = kvr::launch_stats(ctx->ws, ctx->L, ctx->stream);
+  if (e != hipSuccess) return fail_hip(e, "stats kernel launch");
+  e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  const size_t n = (size_t)ctx->L.R * ctx->L.W;
+  e = hipMemcpy(h_out, ctx->ws + ctx->L.off_stats, n * sizeof(kvr_worker_stats), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpy(stats)");
+  if (st != KVR_OK) return fail(st, describe_bits(bits));
+  return KVR_OK;
+}
+
+uint64_t kvr_queries_done(const kvr_ctx* ctx) { return ctx ? ctx->queries_done : 0; }
+
+void kvr_destroy(kvr_ctx* ctx) { delete ctx; }
+
+const char* kvr_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

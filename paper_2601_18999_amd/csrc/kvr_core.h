@@ -1,0 +1,1106 @@
+// kvr_core.h - per-wave logic of the simulator (included by kvr_device.hip).
+//
+// Every function here is executed by one whole wavefront with wave-uniform
+// control flow; lane-parallel loops step by KVR_WAVE lanes (64 on gfx950).
+// Writes of shared scalars are done by lane 0.
+#ifndef KVR_CORE_H
+#define KVR_CORE_H
+
+#include <stdint.h>
+
+#include "kvr_layout.h"
+
+#ifndef KVR_WAVE
+#define KVR_WAVE 64
+#endif
+
+namespace kvr {
+
+
+// ---------------------------------------------------------------- wave tools
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (KVR_WAVE - 1u)); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  return (1ull << (uint32_t)lane_id()) - 1ull;
+}
+
+#ifndef KVR_SYNC_SCOPE
+#define KVR_SYNC_SCOPE "workgroup"
+#endif
+// Global stores of one lane are read back by the other lanes of the same
+// wave (the tree, leaf and candidate arrays are shared by the whole wave):
+// complete them before any later load.
+__device__ __forceinline__ void wave_mem_sync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, KVR_SYNC_SCOPE); }
+
+__device__ __forceinline__ int first_lane(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+  uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, KVR_WAVE);
+  uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, KVR_WAVE);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
+    uint64_t w = shfl_xor_u64(v, o);
+    v = w < v ? w : v;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
+    uint64_t w = shfl_xor_u64(v, o);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------- Philox4x64-10
+// Salmon et al., SC'11: ten rounds, two 64x64->128 products per round, key
+// bumped by the Weyl increments between rounds.  Only word 0 is used.
+__device__ __forceinline__ uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                                 uint64_t k0, uint64_t k1) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+#pragma unroll
+  for (int rnd = 0; rnd < 10; ++rnd) {
+    if (rnd) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+    uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    uint64_t n0 = hi1 ^ c1 ^ k0;
+    uint64_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return c0;
+}
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// rho^k, square-and-multiply from the least significant bit
+__device__ double pow_int(double rho, uint64_t k) {
+  double res = 1.0, b = rho;
+  while (k) {
+    if (k & 1) res = res * b;
+    b = b * b;
+    k >>= 1;
+  }
+  return res;
+}
+
+// ---------------------------------------------------------------- worker view
+
+struct Ptrs {
+  WorkerHdr* hdr;
+  NodeRec* nodes;
+  int32_t* arena0;  // semispace 0; semispace 1 follows at arena0 + A
+  int32_t* leaf;
+  int32_t* U;
+  PendRec* pend;
+  uint64_t* scratch;
+  uint32_t A, NC, PC;
+};
+
+__device__ __forceinline__ Ptrs worker_ptrs(char* ws, const Layout& L, uint32_t r, uint32_t i) {
+  const uint64_t w = (uint64_t)r * L.W + i;
+  Ptrs P;
+  P.hdr = reinterpret_cast<WorkerHdr*>(ws + L.off_whdr) + w;
+  P.nodes = reinterpret_cast<NodeRec*>(ws + L.off_nodes + w * L.node_stride);
+  P.arena0 = reinterpret_cast<int32_t*>(ws + L.off_arena + w * L.arena_stride);
+  P.leaf = reinterpret_cast<int32_t*>(ws + L.off_leaf + w * L.leaf_stride);
+  P.U = reinterpret_cast<int32_t*>(ws + L.off_U + w * L.leaf_stride);
+  P.pend = reinterpret_cast<PendRec*>(ws + L.off_pend + w * L.pend_stride);
+  P.scratch = reinterpret_cast<uint64_t*>(ws + L.off_scratch + w * L.scratch_stride);
+  P.A = L.A;
+  P.NC = L.NC;
+  P.PC = L.PC;
+  return P;
+}
+
+// Wave-uniform copy of the cache part of a worker header.
+struct St {
+  uint32_t phase, cnt, size, hwm;
+  int32_t free_head;
+  uint32_t nleaves, nU, U_valid;
+  int32_t rnode, rlo, rhi;
+  uint32_t rphase;
+  uint32_t arena_sel, arena_top, nnodes;
+  uint64_t loads, evictions, forced, gc_runs;
+  uint32_t err;
+  // first failing internal check (diagnostics only)
+  int32_t dbg_check;
+  int64_t dbg_val[3];
+};
+
+#define KVR_FAIL_CHECK(s, id, a, b, c) \
+  do {                                 \
+    (s).err |= KVR_DEV_INTERNAL;       \
+    if ((s).dbg_check == 0) {          \
+      (s).dbg_check = (id);            \
+      (s).dbg_val[0] = (int64_t)(a);   \
+      (s).dbg_val[1] = (int64_t)(b);   \
+      (s).dbg_val[2] = (int64_t)(c);   \
+    }                                  \
+  } while (0)
+
+__device__ __forceinline__ St load_st(const WorkerHdr* h) {
+  St s;
+  s.phase = h->phase;
+  s.cnt = h->cnt;
+  s.size = h->size;
+  s.hwm = h->hwm;
+  s.free_head = h->free_head;
+  s.nleaves = h->nleaves;
+  s.nU = h->nU;
+  s.U_valid = h->U_valid;
+  s.rnode = h->rnode;
+  s.rlo = h->rlo;
+  s.rhi = h->rhi;
+  s.rphase = h->rphase;
+  s.arena_sel = h->arena_sel;
+  s.arena_top = h->arena_top;
+  s.nnodes = h->nnodes;
+  s.loads = h->loads;
+  s.evictions = h->evictions;
+  s.forced = h->forced_resets;
+  s.gc_runs = h->gc_runs;
+  s.err = 0;
+  s.dbg_check = 0;
+  s.dbg_val[0] = s.dbg_val[1] = s.dbg_val[2] = 0;
+  return s;
+}
+
+__device__ __forceinline__ void store_st(WorkerHdr* h, const St& s) {
+  if (lane_id() != 0) return;
+  h->phase = s.phase;
+  h->cnt = s.cnt;
+  h->size = s.size;
+  h->hwm = s.hwm;
+  h->free_head = s.free_head;
+  h->nleaves = s.nleaves;
+  h->nU = s.nU;
+  h->U_valid = s.U_valid;
+  h->rnode = s.rnode;
+  h->rlo = s.rlo;
+  h->rhi = s.rhi;
+  h->rphase = s.rphase;
+  h->arena_sel = s.arena_sel;
+  h->arena_top = s.arena_top;
+  h->nnodes = s.nnodes;
+  h->loads = s.loads;
+  h->evictions = s.evictions;
+  h->forced_resets = s.forced;
+  h->gc_runs = s.gc_runs;
+}
+
+__device__ __forceinline__ int32_t* arena_of(const Ptrs& P, uint32_t sel) {
+  return P.arena0 + (size_t)sel * P.A;
+}
+
+__device__ __forceinline__ void node_put(const Ptrs& P, int32_t id, const NodeRec& n) {
+  if (lane_id() == 0) P.nodes[id] = n;
+  wave_mem_sync();
+}
+
+// Is edge position `pos` of node `id` in the marking set of the current phase?
+__device__ __forceinline__ bool is_marked(const St& s, const NodeRec& nd, int32_t id, int32_t pos) {
+  if (nd.mphase == s.phase && pos < nd.ma) return true;
+  if (s.rphase == s.phase && s.rnode == id && pos >= s.rlo && pos < s.rhi) return true;
+  return false;
+}
+
+// ---------------------------------------------------------------- array tools (wave)
+
+__device__ int32_t arr_find(const int32_t* a, uint32_t n, int32_t v) {
+  for (uint32_t b = 0; b < n; b += KVR_WAVE) {
+    uint32_t k = b + (uint32_t)lane_id();
+    bool hit = (k < n) && (a[k] == v);
+    uint64_t m = __ballot(hit);
+    if (m) return (int32_t)(b + (uint32_t)first_lane(m));
+  }
+  return -1;
+}
+
+// a[pos+1 .. n+1) = a[pos .. n); a[pos] = v
+__device__ void arr_insert(int32_t* a, uint32_t n, uint32_t pos, int32_t v) {
+  for (int64_t hi = (int64_t)n; hi > (int64_t)pos; hi -= KVR_WAVE) {
+    int64_t lo = hi - KVR_WAVE > (int64_t)pos ? hi - KVR_WAVE : (int64_t)pos;
+    int64_t k = lo + lane_id();
+    int32_t x = 0;
+    if (k < hi) x = a[k];
+    __builtin_amdgcn_wave_barrier();
+    if (k < hi) a[k + 1] = x;
+    wave_mem_sync();
+  }
+  if (lane_id() == 0) a[pos] = v;
+  wave_mem_sync();
+}
+
+// a[pos .. n-1) = a[pos+1 .. n)
+__device__ void arr_erase(int32_t* a, uint32_t n, uint32_t pos) {
+  for (uint32_t lo = pos; lo + 1 < n; lo += KVR_WAVE) {
+    uint32_t k = lo + (uint32_t)lane_id();
+    int32_t x = 0;
+    if (k + 1 < n) x = a[k + 1];
+    __builtin_amdgcn_wave_barrier();
+    if (k + 1 < n) a[k] = x;
+    wave_mem_sync();
+  }
+}
+
+// ---------------------------------------------------------------- child arrays
+
+// Child of a node whose edge starts with `tok`, or -1.
+__device__ int32_t child_find(const int32_t* ar, const NodeRec& nd, int32_t tok) {
+  for (int32_t b = 0; b < nd.nchild; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    bool hit = false;
+    int32_t id = -1;
+    if (k < nd.nchild) {
+      int2 e = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+      hit = (e.x == tok);
+      id = e.y;
+    }
+    uint64_t m = __ballot(hit);
+    if (m) return __shfl(id, first_lane(m), KVR_WAVE);
+  }
+  return -1;
+}
+
+// Child with the largest first token < tok (below) or the smallest > tok.
+__device__ int32_t child_neighbor(const int32_t* ar, const NodeRec& nd, int64_t tok, bool below) {
+  uint64_t best = below ? 0ull : ~0ull;
+  for (int32_t b = 0; b < nd.nchild; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    if (k < nd.nchild) {
+      int2 e = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+      uint64_t key = ((uint64_t)(uint32_t)e.x << 32) | (uint32_t)e.y;
+      if (below && (int64_t)e.x < tok && key > best) best = key;
+      if (!below && (int64_t)e.x > tok && key < best) best = key;
+    }
+  }
+  best = below ? wave_max_u64(best) : wave_min_u64(best);
+  if (below ? best == 0ull : best == ~0ull) return -1;
+  return (int32_t)(uint32_t)(best & 0xffffffffull);
+}
+
+// First (last=false) or last leaf of the subtree of x in lexicographic order
+// (-1 on an inconsistency).
+__device__ int32_t extreme_leaf(const Ptrs& P, const int32_t* ar, int32_t x, bool last, uint32_t hwm) {
+  for (uint32_t steps = 0; steps < hwm; ++steps) {
+    if (x <= 0 || (uint32_t)x >= hwm) return -1;
+    NodeRec nx = P.nodes[x];
+    if (nx.nchild == 0) return x;
+    x = last ? child_neighbor(ar, nx, (int64_t)1 << 32, true) : child_neighbor(ar, nx, -1, false);
+  }
+  return -1;
+}
+
+// Index of the first (after=false) or one past the last (after=true) leaf of
+// the subtree of x in the leaf list, or -1.
+__device__ int32_t leaf_rank(const Ptrs& P, const St& s, const int32_t* ar, int32_t x, bool after) {
+  int32_t lf = extreme_leaf(P, ar, x, after, s.hwm);
+  if (lf < 0) return -1;
+  int32_t pos = arr_find(P.leaf, s.nleaves, lf);
+  if (pos < 0) return -1;
+  return after ? pos + 1 : pos;
+}
+
+// ---------------------------------------------------------------- allocation
+
+// Copying collector: move every live edge and child array of the active
+// semispace to the other one, compacted, and switch semispaces.  False (and
+// nothing switched) when the live data does not fit a semispace.
+__device__ bool collect(const Ptrs& P, St& s) {
+  uint64_t need = 0;
+  for (uint32_t x = 0; x < s.hwm; ++x) {
+    NodeRec nd = P.nodes[x];
+    if (nd.parent == -2) continue;
+    need += (uint64_t)nd.len;
+    if (nd.ccap > 0) need = ((need + 1u) & ~1ull) + 2ull * (uint64_t)nd.ccap;
+  }
+  if (need > P.A) return false;
+  const int32_t* src = arena_of(P, s.arena_sel);
+  int32_t* dst = arena_of(P, s.arena_sel ^ 1u);
+  uint32_t top = 0;
+  for (uint32_t x = 0; x < s.hwm; ++x) {
+    NodeRec nd = P.nodes[x];
+    if (nd.parent == -2) continue;
+    uint32_t noff = top;
+    for (int32_t k = lane_id(); k < nd.len; k += KVR_WAVE) dst[noff + k] = src[nd.off + k];
+    top += (uint32_t)nd.len;
+    uint32_t ncoff = 0;
+    if (nd.ccap > 0) {
+      top = (top + 1u) & ~1u;
+      ncoff = top;
+      for (int32_t k = lane_id(); k < 2 * nd.nchild; k += KVR_WAVE) dst[ncoff + k] = src[nd.coff + k];
+      top += 2u * (uint32_t)nd.ccap;
+    }
+    if (lane_id() == 0) {
+      P.nodes[x].off = noff;
+      P.nodes[x].coff = ncoff;
+    }
+  }
+  wave_mem_sync();
+  s.arena_sel ^= 1u;
+  s.arena_top = top;
+  s.gc_runs += 1;
+  return true;
+}
+
+__device__ bool arena_alloc(const Ptrs& P, St& s, uint32_t words, bool even, uint32_t& off) {
+  uint64_t top = s.arena_top;
+  if (even) top = (top + 1u) & ~1ull;
+  if (top + words > P.A) {
+    if (!collect(P, s)) {
+      s.err |= KVR_DEV_ARENA_FULL;
+      return false;
+    }
+    top = s.arena_top;
+    if (even) top = (top + 1u) & ~1ull;
+    if (top + words > P.A) {
+      s.err |= KVR_DEV_ARENA_FULL;
+      return false;
+    }
+  }
+  off = (uint32_t)top;
+  s.arena_top = (uint32_t)(top + words);
+  return true;
+}
+
+__device__ int32_t node_alloc(const Ptrs& P, St& s) {
+  int32_t id;
+  if (s.free_head >= 0) {
+    id = s.free_head;
+    s.free_head = (int32_t)P.nodes[id].off;
+  } else if (s.hwm < P.NC) {
+    id = (int32_t)s.hwm;
+    s.hwm += 1;
+  } else {
+    s.err |= KVR_DEV_NODES_FULL;
+    return -1;
+  }
+  s.nnodes += 1;
+  return id;
+}
+
+__device__ void node_free(const Ptrs& P, St& s, int32_t id) {
+  if (lane_id() == 0) {
+    P.nodes[id].parent = -2;
+    P.nodes[id].off = (uint32_t)s.free_head;
+  }
+  wave_mem_sync();
+  s.free_head = id;
+  s.nnodes -= 1;
+}
+
+__device__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c) {
+  NodeRec na = P.nodes[a];
+  if (na.nchild == na.ccap) {
+    int32_t ncap = na.ccap ? 2 * na.ccap : 2;
+    uint32_t off;
+    if (!arena_alloc(P, s, 2u * (uint32_t)ncap, true, off)) return false;
+    na = P.nodes[a];  // the collector may have moved the old array
+    int32_t* ar = arena_of(P, s.arena_sel);
+    for (int32_t k = lane_id(); k < 2 * na.nchild; k += KVR_WAVE) ar[off + k] = ar[na.coff + k];
+    wave_mem_sync();
+    na.coff = off;
+    na.ccap = ncap;
+  }
+  int32_t* ar = arena_of(P, s.arena_sel);
+  if (lane_id() == 0) {
+    ar[na.coff + 2 * na.nchild] = tok;
+    ar[na.coff + 2 * na.nchild + 1] = c;
+    P.nodes[a].coff = na.coff;
+    P.nodes[a].ccap = na.ccap;
+    P.nodes[a].nchild = na.nchild + 1;
+  }
+  wave_mem_sync();
+  return true;
+}
+
+__device__ int32_t child_slot(const int32_t* ar, const NodeRec& na, int32_t c) {
+  for (int32_t b = 0; b < na.nchild; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    bool hit = (k < na.nchild) && (ar[na.coff + 2 * k + 1] == c);
+    uint64_t m = __ballot(hit);
+    if (m) return b + first_lane(m);
+  }
+  return -1;
+}
+
+__device__ bool child_remove(const Ptrs& P, const St& s, int32_t a, int32_t c) {
+  NodeRec na = P.nodes[a];
+  int32_t* ar = arena_of(P, s.arena_sel);
+  int32_t pos = child_slot(ar, na, c);
+  if (pos < 0) return false;
+  int32_t last = na.nchild - 1;
+  if (lane_id() == 0) {
+    if (pos != last) {
+      ar[na.coff + 2 * pos] = ar[na.coff + 2 * last];
+      ar[na.coff + 2 * pos + 1] = ar[na.coff + 2 * last + 1];
+    }
+    P.nodes[a].nchild = last;
+  }
+  wave_mem_sync();
+  return true;
+}
+
+__device__ bool child_replace(const Ptrs& P, const St& s, int32_t a, int32_t oldc, int32_t newc) {
+  NodeRec na = P.nodes[a];
+  int32_t* ar = arena_of(P, s.arena_sel);
+  int32_t pos = child_slot(ar, na, oldc);
+  if (pos < 0) return false;
+  if (lane_id() == 0) ar[na.coff + 2 * pos + 1] = newc;
+  wave_mem_sync();
+  return true;
+}
+
+// Split node x at edge offset k (0 < k < len): a new head node takes
+// positions [0, k) and x keeps [k, len) below it, so every leaf keeps its id.
+__device__ int32_t split_node(const Ptrs& P, St& s, int32_t x, int32_t k) {
+  uint32_t coff;
+  if (!arena_alloc(P, s, 4u, true, coff)) return -1;
+  int32_t hd = node_alloc(P, s);
+  if (hd < 0) return -1;
+  NodeRec nx = P.nodes[x];
+  int32_t* ar = arena_of(P, s.arena_sel);
+  int32_t tail_tok = ar[nx.off + (uint32_t)k];
+  NodeRec nh;
+  nh.parent = nx.parent;
+  nh.off = nx.off;
+  nh.len = k;
+  nh.nchild = 1;
+  nh.coff = coff;
+  nh.ccap = 2;
+  nh.mphase = nx.mphase;
+  nh.ma = nx.ma < k ? nx.ma : k;
+  NodeRec nt = nx;
+  nt.parent = hd;
+  nt.off = nx.off + (uint32_t)k;
+  nt.len = nx.len - k;
+  nt.ma = nx.ma - k > 0 ? nx.ma - k : 0;
+  if (s.rnode == x) {
+    if (s.rphase != s.phase) {
+      s.rphase = 0;
+    } else if (s.rhi <= k) {
+      s.rnode = hd;
+    } else if (s.rlo >= k) {
+      s.rlo -= k;
+      s.rhi -= k;
+    } else {
+      int32_t t = s.rhi - k;
+      s.rnode = hd;
+      s.rhi = k;
+      if (nt.mphase == s.phase) {
+        nt.ma = nt.ma > t ? nt.ma : t;
+      } else {
+        nt.mphase = s.phase;
+        nt.ma = t;
+      }
+    }
+  }
+  if (lane_id() == 0) {
+    ar[coff] = tail_tok;
+    ar[coff + 1] = x;
+  }
+  node_put(P, hd, nh);
+  node_put(P, x, nt);
+  if (!child_replace(P, s, nx.parent, x, hd)) {
+    KVR_FAIL_CHECK(s, 3, x, nx.parent, hd);
+    return -1;
+  }
+  return hd;
+}
+
+// ---------------------------------------------------------------- RLT pieces
+
+// U := the leaves (other than `excl`) whose leaf token is unmarked, in the
+// order of the leaf list (lexicographic order of root paths).
+__device__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
+  uint32_t n = 0;
+  for (uint32_t b = 0; b < s.nleaves; b += KVR_WAVE) {
+    uint32_t k = b + (uint32_t)lane_id();
+    bool cand = false;
+    int32_t id = -1;
+    if (k < s.nleaves) {
+      id = P.leaf[k];
+      if (id != excl) {
+        NodeRec nd = P.nodes[id];
+        cand = !is_marked(s, nd, id, nd.len - 1);
+      }
+    }
+    uint64_t m = __ballot(cand);
+    if (cand) P.U[n + (uint32_t)__popcll(m & lanemask_lt())] = id;
+    n += (uint32_t)__popcll(m);
+  }
+  wave_mem_sync();
+  s.nU = n;
+  s.U_valid = 1;
+}
+
+// Evict the leaf token of candidate U[kk].  False on an inconsistency.
+__device__ bool evict_one(const Ptrs& P, St& s, uint32_t kk) {
+  int32_t n = P.U[kk];
+  if (n <= 0 || (uint32_t)n >= s.hwm) {
+    KVR_FAIL_CHECK(s, 10, kk, n, s.nU);
+    return false;
+  }
+  NodeRec nd = P.nodes[n];
+  if (nd.len <= 0 || nd.nchild != 0 || nd.parent < 0) {
+    KVR_FAIL_CHECK(s, 11, n, nd.len, nd.nchild);
+    return false;
+  }
+  int32_t nl = nd.len - 1;
+  if (nl > 0) {
+    if (lane_id() == 0) P.nodes[n].len = nl;
+    wave_mem_sync();
+    if (is_marked(s, nd, n, nl - 1)) {
+      arr_erase(P.U, s.nU, kk);
+      s.nU -= 1;
+    }
+    return true;
+  }
+  int32_t p = nd.parent;
+  int32_t li = arr_find(P.leaf, s.nleaves, n);
+  if (li < 0) {
+    KVR_FAIL_CHECK(s, 12, n, s.nleaves, kk);
+    return false;
+  }
+  if (!child_remove(P, s, p, n)) {
+    KVR_FAIL_CHECK(s, 13, n, p, 0);
+    return false;
+  }
+  node_free(P, s, n);
+  NodeRec np = P.nodes[p];
+  if (p != 0 && np.nchild == 0) {
+    // the parent's last token is a new leaf token, at the rank of n
+    if (lane_id() == 0) P.leaf[li] = p;
+    wave_mem_sync();
+    if (!is_marked(s, np, p, np.len - 1)) {
+      if (lane_id() == 0) P.U[kk] = p;
+      wave_mem_sync();
+    } else {
+      arr_erase(P.U, s.nU, kk);
+      s.nU -= 1;
+    }
+  } else {
+    arr_erase(P.leaf, s.nleaves, (uint32_t)li);
+    s.nleaves -= 1;
+    arr_erase(P.U, s.nU, kk);
+    s.nU -= 1;
+  }
+  return true;
+}
+
+struct InsertArgs {
+  uint64_t seed;
+  uint64_t jg;        // global query index
+  uint32_t worker;    // routed worker
+  uint32_t replica;
+  uint32_t B;
+};
+
+// RLT insertion of q[0, L) into the worker's cache; h = LCP(q, cache).
+// Returns the KVR_DEV_* error bits (0 on success).
+__device__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
+                               int32_t h, int64_t* dbg) {
+  St s = load_st(P.hdr);
+  const uint32_t B = ia.B;
+  int32_t* ar = arena_of(P, s.arena_sel);
+
+  // ---- walk the cached part of the path and mark it
+  int32_t x = 0, d = 0, last = 0, lastcov = 0;
+  while (d < h) {
+    NodeRec nx = P.nodes[x];
+    int32_t c = child_find(ar, nx, qs[d]);
+    if (c <= 0 || (uint32_t)c >= s.hwm) {
+      KVR_FAIL_CHECK(s, 1, x, d, h);
+      goto fail;
+    }
+    NodeRec nc = P.nodes[c];
+    int32_t cov = nc.len < h - d ? nc.len : h - d;
+    if (cov <= 0) {
+      KVR_FAIL_CHECK(s, 2, c, nc.len, d);
+      goto fail;
+    }
+    bool was_cand = (nc.nchild == 0) && !is_marked(s, nc, c, nc.len - 1);
+    int32_t ma = (nc.mphase == s.phase) ? nc.ma : 0;
+    bool rv = (s.rphase == s.phase) && (s.rnode == c);
+    int32_t rlo = s.rlo, rhi = s.rhi;
+    if (rv && rlo <= ma) {  // the reset interval touches the prefix: merge
+      ma = ma > rhi ? ma : rhi;
+      rv = false;
+      s.rphase = 0;
+    }
+    int32_t m1 = ma < cov ? ma : cov;
+    int32_t m2 = 0;
+    if (rv) {
+      int32_t e = rhi < cov ? rhi : cov;
+      m2 = e - rlo > 0 ? e - rlo : 0;
+    }
+    int32_t newly = cov - m1 - m2;
+    if (s.cnt + (uint32_t)newly <= B) {
+      s.cnt += (uint32_t)newly;
+      int32_t nma = ma > cov ? ma : cov;
+      if (rv && rlo <= nma) {
+        nma = nma > rhi ? nma : rhi;
+        s.rphase = 0;
+      }
+      if (lane_id() == 0) {
+        P.nodes[c].mphase = s.phase;
+        P.nodes[c].ma = nma;
+      }
+      wave_mem_sync();
+    } else {
+      // |T| reaches B+1 at the `need`-th newly marked position of this edge
+      int32_t need = (int32_t)(B + 1u - s.cnt);
+      int32_t pr;
+      if (!rv) {
+        pr = ma + need - 1;
+      } else {
+        int32_t e1 = rlo < cov ? rlo : cov;
+        int32_t s1 = e1 - ma > 0 ? e1 - ma : 0;
+        pr = need <= s1 ? ma + need - 1 : rhi + (need - s1) - 1;
+      }
+      s.phase += 1;
+      s.U_valid = 0;
+      s.cnt = (uint32_t)(cov - pr);
+      if (pr == 0) {
+        if (lane_id() == 0) {
+          P.nodes[c].mphase = s.phase;
+          P.nodes[c].ma = cov;
+        }
+        wave_mem_sync();
+      } else {
+        s.rnode = c;
+        s.rlo = pr;
+        s.rhi = cov;
+        s.rphase = s.phase;
+      }
+    }
+    if (was_cand && s.U_valid && cov == nc.len) {
+      // a candidate's leaf token was marked
+      int32_t pos = arr_find(P.U, s.nU, c);
+      if (pos >= 0) {
+        arr_erase(P.U, s.nU, (uint32_t)pos);
+        s.nU -= 1;
+      }
+    }
+    d += cov;
+    last = c;
+    lastcov = cov;
+    x = c;
+  }
+
+  if (h < L) {
+    const int32_t nload = L - h;
+    // ---- attachment point: end of `last`, splitting it if needed
+    int32_t a = last;
+    bool split = false;
+    if (h > 0) {
+      NodeRec nl = P.nodes[last];
+      if (lastcov < nl.len) {
+        a = split_node(P, s, last, lastcov);
+        if (a < 0) goto fail;
+        split = true;
+        ar = arena_of(P, s.arena_sel);
+      }
+    }
+    // ---- rank of the new leaf in the leaf list
+    int32_t pos;
+    bool replace = false;
+    {
+      NodeRec na = P.nodes[a];
+      if (a != 0 && na.nchild == 0) {
+        pos = arr_find(P.leaf, s.nleaves, a);
+        replace = true;
+      } else if (split) {
+        NodeRec nt = P.nodes[last];
+        int32_t tail_tok = ar[nt.off];
+        pos = leaf_rank(P, s, ar, last, !(qs[h] < tail_tok));
+      } else if (na.nchild == 0) {
+        pos = 0;
+      } else {
+        int32_t cb = child_neighbor(ar, na, qs[h], true);
+        if (cb >= 0) {
+          pos = leaf_rank(P, s, ar, cb, true);
+        } else {
+          int32_t ca = child_neighbor(ar, na, qs[h], false);
+          pos = leaf_rank(P, s, ar, ca, false);
+        }
+      }
+    }
+    if (pos < 0 || (uint32_t)pos > s.nleaves) {
+      KVR_FAIL_CHECK(s, 4, pos, s.nleaves, a);
+      goto fail;
+    }
+    // ---- the new leaf node holding q[h, L)
+    uint32_t eoff;
+    if (!arena_alloc(P, s, (uint32_t)nload, false, eoff)) goto fail;
+    ar = arena_of(P, s.arena_sel);
+    for (int32_t k = lane_id(); k < nload; k += KVR_WAVE) ar[eoff + (uint32_t)k] = qs[h + k];
+    wave_mem_sync();
+    int32_t l = node_alloc(P, s);
+    if (l < 0) goto fail;
+    {
+      NodeRec nl;
+      nl.parent = a;
+      nl.off = eoff;
+      nl.len = nload;
+      nl.nchild = 0;
+      nl.coff = 0;
+      nl.ccap = 0;
+      nl.mphase = 0;
+      nl.ma = 0;
+      node_put(P, l, nl);
+    }
+    if (!child_add(P, s, a, qs[h], l)) goto fail;
+    ar = arena_of(P, s.arena_sel);
+    if (replace) {
+      if (lane_id() == 0) P.leaf[pos] = l;
+      wave_mem_sync();
+    } else {
+      arr_insert(P.leaf, s.nleaves, (uint32_t)pos, l);
+      s.nleaves += 1;
+    }
+
+    // ---- loads, evictions and the phase reset of the missed part
+    const uint32_t nfree = B - s.size;
+    const uint32_t nev = (uint32_t)nload > nfree ? (uint32_t)nload - nfree : 0u;
+    const uint32_t c0 = s.cnt;
+    int32_t reset_at = (c0 + (uint32_t)nload >= B + 1u) ? h + (int32_t)(B - c0) : -1;
+    bool applied = false;
+    uint64_t dctr = 0;
+    for (uint32_t k = 0; k < nev; ++k) {
+      const int32_t p = h + (int32_t)nfree + (int32_t)k;
+      if (reset_at >= 0 && !applied && p >= reset_at) {
+        s.phase += 1;
+        s.U_valid = 0;
+        applied = true;
+      }
+      if (!s.U_valid) rebuild_U(P, s, l);
+      if (s.nU == 0) {
+        // no unmarked leaf: a new phase starts with the current token
+        s.phase += 1;
+        s.forced += 1;
+        rebuild_U(P, s, l);
+        reset_at = p;
+        applied = true;
+        if (s.nU == 0) {  // only possible for a path longer than the cache
+          KVR_FAIL_CHECK(s, 6, p, s.nleaves, L);
+          goto fail;
+        }
+      }
+      uint64_t r64 = philox_word0(ia.jg, ia.worker, dctr, 0ull, ia.seed, ia.replica);
+      dctr += 1;
+      uint32_t kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
+      if (!evict_one(P, s, kk)) goto fail;
+    }
+    if (reset_at >= 0 && !applied) {
+      s.phase += 1;
+      s.U_valid = 0;
+      applied = true;
+    }
+    if (applied) {
+      const int32_t lo = reset_at - h;
+      s.cnt = (uint32_t)(L - reset_at);
+      if (lo == 0) {
+        if (lane_id() == 0) {
+          P.nodes[l].mphase = s.phase;
+          P.nodes[l].ma = nload;
+        }
+      } else {
+        s.rnode = l;
+        s.rlo = lo;
+        s.rhi = nload;
+        s.rphase = s.phase;
+      }
+    } else {
+      s.cnt = c0 + (uint32_t)nload;
+      if (lane_id() == 0) {
+        P.nodes[l].mphase = s.phase;
+        P.nodes[l].ma = nload;
+      }
+    }
+    s.size = s.size + (uint32_t)nload - nev;
+    s.loads += (uint64_t)nload;
+    s.evictions += nev;
+  }
+  store_st(P.hdr, s);
+  wave_mem_sync();
+  return 0;
+fail:
+  store_st(P.hdr, s);
+  if (dbg) {
+    dbg[0] = s.dbg_check;
+    dbg[1] = s.dbg_val[0];
+    dbg[2] = s.dbg_val[1];
+    dbg[3] = s.dbg_val[2];
+  }
+  return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
+
+// ---------------------------------------------------------------- matching
+
+__device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n) {
+  for (int32_t b = 0; b < n; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    bool mis = (k < n) && (e[k] != q[k]);
+    uint64_t m = __ballot(mis);
+    if (m) return b + first_lane(m);
+  }
+  return n;
+}
+
+// h = length of the longest prefix of q[0, L) cached in the worker's tree.
+__device__ int32_t match_lcp(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L) {
+  const int32_t* ar = arena_of(P, sel);
+  int32_t x = 0, h = 0;
+  while (h < L) {
+    NodeRec nx = P.nodes[x];
+    int32_t c = child_find(ar, nx, qs[h]);
+    if (c < 0) break;
+    NodeRec nc = P.nodes[c];
+    if (nc.len <= 0) break;  // never true for a consistent tree
+    int32_t n = nc.len < L - h ? nc.len : L - h;
+    int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + h + 1, n - 1);
+    h += k;
+    if (k < nc.len) break;
+    x = c;
+  }
+  return h;
+}
+
+// ---------------------------------------------------------------- LBGR (one lane per worker)
+
+__device__ void online_update(const Consts& C, WorkerHdr* w, const double phi[4], double e) {
+  if (C.update == KVR_UPD_NLMS) {
+    double ss = phi[0] * phi[0];
+    ss = ss + phi[1] * phi[1];
+    ss = ss + phi[2] * phi[2];
+    ss = ss + phi[3] * phi[3];
+    double g = (C.lr * e) / (C.nlms_eps + ss);
+    for (int a = 0; a < 4; ++a) w->theta[a] = w->theta[a] + g * phi[a];
+  } else if (C.update == KVR_UPD_RLS) {
+    double pi[4];
+    for (int a = 0; a < 4; ++a) {
+      double acc = w->Pm[a * 4 + 0] * phi[0];
+      acc = acc + w->Pm[a * 4 + 1] * phi[1];
+      acc = acc + w->Pm[a * 4 + 2] * phi[2];
+      acc = acc + w->Pm[a * 4 + 3] * phi[3];
+      pi[a] = acc;
+    }
+    double den = phi[0] * pi[0];
+    den = den + phi[1] * pi[1];
+    den = den + phi[2] * pi[2];
+    den = den + phi[3] * pi[3];
+    den = C.lr + den;
+    double k[4];
+    for (int a = 0; a < 4; ++a) k[a] = pi[a] / den;
+    for (int a = 0; a < 4; ++a) w->theta[a] = w->theta[a] + k[a] * e;
+    for (int a = 0; a < 4; ++a)
+      for (int b = 0; b < 4; ++b) w->Pm[a * 4 + b] = (w->Pm[a * 4 + b] - k[a] * pi[b]) / C.lr;
+  }
+}
+
+// Completions with t_done <= t (FIFO), then decay to t and drain the
+// observed-latency backlog.
+__device__ void complete_and_decay(const Consts& C, const Ptrs& P, int64_t t, int64_t tprev) {
+  WorkerHdr* w = P.hdr;
+  const int64_t dt = C.dt_us;
+  double Pl = w->P;
+  int64_t tl = w->tl;
+  uint32_t head = w->pend_head, cnt = w->pend_count;
+  uint64_t done = 0;
+  while (cnt > 0) {
+    PendRec pr = P.pend[head];
+    if (pr.t_done > t) break;
+    head = head + 1 == P.PC ? 0u : head + 1;
+    cnt -= 1;
+    Pl = Pl * pow_int(C.rho, (uint64_t)(pr.t_done / dt - tl / dt));
+    tl = pr.t_done;
+    double rem = pr.chat * pow_int(C.rho, (uint64_t)(pr.t_done / dt - pr.t_route / dt));
+    double np = Pl - rem;
+    Pl = np > 0.0 ? np : 0.0;
+    double phi[4];
+    phi[0] = (double)pr.h * 0.001;
+    phi[1] = (double)(pr.L - pr.h) * 0.001;
+    phi[2] = pr.x3;
+    phi[3] = 1.0;
+    double res = w->theta[0] * phi[0];
+    res = res + w->theta[1] * phi[1];
+    res = res + w->theta[2] * phi[2];
+    res = res + w->theta[3] * phi[3];
+    double ehat_now = pr.base + res;
+    double e_obs = (double)(pr.t_done - pr.t_route) * 1e-6;
+    online_update(C, w, phi, e_obs - ehat_now);
+    done += 1;
+  }
+  Pl = Pl * pow_int(C.rho, (uint64_t)(t / dt - tl / dt));
+  w->P = Pl;
+  w->tl = t;
+  w->pend_head = head;
+  w->pend_count = cnt;
+  w->completions += done;
+  int64_t nb = w->Wb - (t - tprev);
+  w->Wb = nb > 0 ? nb : 0;
+}
+
+
+// ---------------------------------------------------------------- routing (one thread per worker)
+
+// LBGR score of one worker (Eq. LBGR-score with the features of Sec. 4.2
+// and the per-1k-token scaling of App. A).  *chat = estimated service time.
+__device__ double lbgr_score(const Consts& C, const WorkerHdr* w, int32_t h, int32_t L, double* chat) {
+  double x1 = (double)h * 0.001;
+  double x2 = (double)(L - h) * 0.001;
+  double x3 = w->P;
+  double x4 = 1.0;
+  double ch = C.alpha_cached * x1 + C.alpha_miss * x2;
+  double res = w->theta[0] * x1;
+  res = res + w->theta[1] * x2;
+  res = res + w->theta[2] * x3;
+  res = res + w->theta[3] * x4;
+  *chat = ch;
+  return (ch + w->P) + res;
+}
+
+// Commit a query on its routed worker: add the estimated service time to the
+// load estimate (Algorithm 2), advance the observed-latency queue and queue
+// the completion record.  Returns KVR_DEV_* bits.
+__device__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t L,
+                                 int64_t t, int32_t olen) {
+  WorkerHdr* w = P.hdr;
+  const double base = chat + w->P;
+  const double x3 = w->P;
+  w->P = w->P + chat;
+  const int64_t cost = C.true_cached_us * hb + C.true_miss_us * (int64_t)(L - hb) + C.true_out_us * (int64_t)olen;
+  const int64_t e_us = w->Wb + cost;
+  w->Wb = w->Wb + cost;
+  uint32_t err = 0;
+  if (w->pend_count >= P.PC) {
+    err |= KVR_DEV_PENDING_FULL;
+  } else {
+    uint32_t slot = w->pend_head + w->pend_count;
+    if (slot >= P.PC) slot -= P.PC;
+    PendRec pr;
+    pr.t_route = t;
+    pr.t_done = t + e_us;
+    pr.chat = chat;
+    pr.base = base;
+    pr.x3 = x3;
+    pr.h = hb;
+    pr.L = L;
+    P.pend[slot] = pr;
+    w->pend_count += 1;
+    if (w->pend_count > w->pending_max) w->pending_max = w->pend_count;
+  }
+  w->routed += 1;
+  w->prompt_tokens += (uint64_t)L;
+  w->hit_tokens += (uint64_t)hb;
+  w->lat_sum_us += (uint64_t)e_us;
+  if ((uint64_t)e_us > w->lat_max_us) w->lat_max_us = (uint64_t)e_us;
+  return err;
+}
+
+// Empty cache, phase 1, zero load and model (one thread per worker).
+__device__ void init_worker(const Ptrs& P, double rls_p0) {
+  WorkerHdr h;
+  uint8_t* hb = reinterpret_cast<uint8_t*>(&h);
+  for (size_t b = 0; b < sizeof(WorkerHdr); ++b) hb[b] = 0;
+  h.phase = 1;
+  h.hwm = 1;
+  h.free_head = -1;
+  h.rnode = -1;
+  for (int k = 0; k < 16; ++k) h.Pm[k] = (k % 5 == 0) ? rls_p0 : 0.0;
+  *P.hdr = h;
+  NodeRec root;
+  root.parent = -1;
+  root.off = 0;
+  root.len = 0;
+  root.nchild = 0;
+  root.coff = 0;
+  root.ccap = 0;
+  root.mphase = 0;
+  root.ma = 0;
+  P.nodes[0] = root;
+}
+
+// Final state of one worker with the path-hash digest of the cached tokens
+// H(v) = mix64(H(parent) + G*(tok+1)), H(root) = 0, over a depth-first walk
+// (one thread; P.scratch holds the stack of (node, start hash) pairs).
+__device__ void worker_stats(const Ptrs& P, kvr_worker_stats* out) {
+  const WorkerHdr* h = P.hdr;
+  St s = load_st(h);
+  const int32_t* ar = arena_of(P, s.arena_sel);
+  uint64_t count = 0, dsum = 0, dxor = 0, mcount = 0, msum = 0;
+  uint64_t* stack = P.scratch;
+  uint64_t sp = 1;
+  stack[0] = 0;
+  stack[1] = 0;
+  for (uint64_t pops = 0; sp > 0 && pops <= s.hwm; ++pops) {
+    sp -= 1;
+    const int32_t x = (int32_t)stack[2 * sp];
+    if (x < 0 || (uint32_t)x >= s.hwm) break;
+    uint64_t hx = stack[2 * sp + 1];
+    const NodeRec nd = P.nodes[x];
+    for (int32_t k = 0; k < nd.len; ++k) {
+      const int32_t tok = ar[nd.off + (uint32_t)k];
+      hx = mix64(hx + 0x9E3779B97F4A7C15ull * (uint64_t)(int64_t)(tok + 1));
+      count += 1;
+      dsum += hx;
+      dxor ^= hx;
+      if (is_marked(s, nd, x, k)) {
+        mcount += 1;
+        msum += hx;
+      }
+    }
+    for (int32_t c = 0; c < nd.nchild && sp < P.NC; ++c) {
+      stack[2 * sp] = (uint64_t)(uint32_t)ar[nd.coff + 2 * c + 1];
+      stack[2 * sp + 1] = hx;
+      sp += 1;
+    }
+  }
+  kvr_worker_stats o;
+  o.routed = h->routed;
+  o.prompt_tokens = h->prompt_tokens;
+  o.hit_tokens = h->hit_tokens;
+  o.matched_tokens = h->matched_tokens;
+  o.loads = h->loads;
+  o.evictions = h->evictions;
+  o.phase = h->phase;
+  o.cnt = h->cnt;
+  o.forced_resets = h->forced_resets;
+  o.resident = count;
+  o.digest_sum = dsum;
+  o.digest_xor = dxor;
+  o.marked_count = mcount;
+  o.marked_sum = msum;
+  o.completions = h->completions;
+  o.pending_depth = h->pend_count;
+  o.pending_max = h->pending_max;
+  o.latency_sum_us = h->lat_sum_us;
+  o.latency_max_us = h->lat_max_us;
+  o.backlog_us = h->Wb;
+  o.last_decay_us = h->tl;
+  o.load_est = h->P;
+  for (int a = 0; a < 4; ++a) o.theta[a] = h->theta[a];
+  o.nodes = h->nnodes;
+  o.gc_runs = h->gc_runs;
+  *out = o;
+}
+
+}  // namespace kvr
+
+#endif  // KVR_CORE_H

@@ -1,0 +1,230 @@
+// kvr_device.hip - gfx950 kernels of the batched KV-cache routing / eviction
+// simulator.
+//
+// One workgroup owns one replica for a whole batch and walks the batch's
+// queries in order (the simulation is sequential within a replica, Sec. 3.1:
+// the state after query j-1 decides query j).  Per query:
+//   * all waves: stage the query tokens in LDS;
+//   * wave 0: completions and load decay for every worker, one lane per
+//     worker (Algorithm 2, update and decay threads; Sec. 4.2);
+//   * every wave takes workers in turn and computes h_ij, the longest
+//     cached prefix of the query, walking the worker's compressed radix tree
+//     and comparing 64 tokens per wave instruction (Sec. 3.2 "Cache
+//     Matching");
+//   * wave 0: the LBGR score of every worker, the argmin (lowest index on
+//     ties) and the commit on the routed worker (Algorithm 2 routing thread,
+//     Eq. LBGR-score, Eq. 2 with the estimate);
+//   * wave 0: RLT insertion into the routed worker's cache (Algorithm 1):
+//     marks along the path, phase resets, a uniform draw over the unmarked
+//     leaf tokens U for every token loaded into a full cache (Eq. 3: no other
+//     cache changes).
+//
+// The cache of a worker is a compressed radix tree: a node holds an edge of
+// `len` tokens; its leaf token (when it has no children) is the last one.
+// U is kept as an ordered list of candidate leaf nodes in lexicographic
+// order of their root paths: rebuilt from the ordered list of all leaves
+// when a phase starts, shortened when a candidate's leaf token is marked,
+// and updated in place when an eviction exposes the parent as a new leaf
+// (the parent inherits the rank of the leaf it replaces).  A draw takes
+// index floor(r * |U| / 2^64), r = word 0 of Philox4x64-10 with key
+// (seed, replica) and counter (query index, worker, draw index, 0).
+//
+// Floating point: double, left-to-right sums, built with -ffp-contract=off so
+// no multiply-add is fused; the same expressions in the same order as the
+// definition, so results are bit-identical to any IEEE implementation that
+// evaluates them in that order.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvr_core.h"
+
+namespace kvr {
+
+// ---------------------------------------------------------------- kernels
+
+__global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
+  extern __shared__ int32_t qs[];  // the current query, max_query_tokens entries
+  __shared__ int32_t h_sh[kMaxWorkers];
+  __shared__ double eh_sh[kMaxWorkers];
+  __shared__ double ch_sh[kMaxWorkers];
+  __shared__ int32_t best_sh;
+  __shared__ uint32_t abort_sh;
+
+  const uint32_t r = blockIdx.x;
+  const uint32_t W = a.L.W;
+  const int lane = lane_id();
+  const uint32_t wave = threadIdx.x / KVR_WAVE;
+  const uint32_t nwaves = blockDim.x / KVR_WAVE;
+  GlobalHdr* g = reinterpret_cast<GlobalHdr*>(a.ws + a.L.off_global);
+  ReplicaHdr* rh = reinterpret_cast<ReplicaHdr*>(a.ws + a.L.off_rhdr) + r;
+
+  if (threadIdx.x == 0) abort_sh = __atomic_load_n(&g->status, __ATOMIC_RELAXED);
+  __syncthreads();
+  if (abort_sh) return;
+
+  for (uint32_t k = 0; k < a.n; ++k) {
+    const uint64_t o0 = a.offsets[k];
+    const int32_t Lq = (int32_t)(a.offsets[k + 1] - o0);
+    const int64_t t = a.arrival[k];
+    const int32_t olen = a.out_len ? (int32_t)a.out_len[k] : 4;
+    for (int32_t x = (int32_t)threadIdx.x; x < Lq; x += (int32_t)blockDim.x) qs[x] = a.tokens[o0 + x];
+    __syncthreads();
+
+    // completions and decay (one lane per worker), then the match (one wave per worker)
+    if (wave == 0 && (uint32_t)lane < W) {
+      const int64_t tprev = rh->tprev;
+      complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), t, tprev);
+    }
+    for (uint32_t i = wave; i < W; i += nwaves) {
+      Ptrs P = worker_ptrs(a.ws, a.L, r, i);
+      const uint32_t sel = P.hdr->arena_sel;
+      int32_t h = match_lcp(P, sel, qs, Lq);
+      if (lane == 0) {
+        h_sh[i] = h;
+        P.hdr->matched_tokens += (uint64_t)h;
+      }
+    }
+    __syncthreads();
+
+    if (wave == 0) {
+      if ((uint32_t)lane < W) {
+        double ch;
+        eh_sh[lane] = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[lane], Lq, &ch);
+        ch_sh[lane] = ch;
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (lane == 0) {
+        uint32_t best = 0;  // argmin, lowest index on ties
+        for (uint32_t i = 1; i < W; ++i)
+          if (eh_sh[i] < eh_sh[best]) best = i;
+        best_sh = (int32_t)best;
+        rh->tprev = t;
+      }
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t best = (uint32_t)best_sh;
+      Ptrs P = worker_ptrs(a.ws, a.L, r, best);
+      const int32_t hb = h_sh[best];
+      uint32_t err = 0;
+      if (lane == 0) {
+        err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
+        const uint64_t orow = (uint64_t)r * a.n + k;
+        if (a.route) a.route[orow] = (int32_t)best;
+        if (a.hits) a.hits[orow] = hb;
+      }
+      if (a.all_hits && (uint32_t)lane < W)
+        a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[lane];
+      err = (uint32_t)__shfl((int)err, 0, KVR_WAVE);
+      if (!err) {
+        InsertArgs ia;
+        ia.seed = a.C.seed;
+        ia.jg = a.j0 + k;
+        ia.worker = best;
+        ia.replica = r;
+        ia.B = a.L.B;
+        int64_t dbg[4] = {0, 0, 0, 0};
+        err = rlt_insert(P, ia, qs, Lq, hb, dbg);
+        if (lane == 0 && err && atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
+          g->err_check = (uint32_t)dbg[0];
+          g->err_replica = r;
+          g->err_query = a.j0 + k;
+          g->err_val[0] = dbg[1];
+          g->err_val[1] = dbg[2];
+          g->err_val[2] = dbg[3];
+        }
+      }
+      if (lane == 0 && err) {
+        atomicOr(&g->status, err);
+        abort_sh = 1;
+      }
+    }
+    __syncthreads();
+    if (abort_sh) break;
+  }
+  if (threadIdx.x == 0 && r == 0 && !abort_sh && a.n > 0) g->last_arrival = a.arrival[a.n - 1];
+}
+
+__global__ void init_kernel(char* ws, Layout L, double rls_p0) {
+  const uint64_t RW = (uint64_t)L.R * L.W;
+  const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid == 0) {
+    GlobalHdr* g = reinterpret_cast<GlobalHdr*>(ws + L.off_global);
+    g->status = 0;
+    g->err_taken = 0;
+    g->last_arrival = 0;
+    g->err_check = 0;
+    g->err_replica = 0;
+    g->err_query = 0;
+    g->err_val[0] = g->err_val[1] = g->err_val[2] = 0;
+  }
+  if (tid < L.R) reinterpret_cast<ReplicaHdr*>(ws + L.off_rhdr)[tid].tprev = 0;
+  if (tid < RW) init_worker(worker_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
+}
+
+// Batch checks before any state changes: lengths and arrival order.
+__global__ void validate_kernel(char* ws, Layout L, const uint64_t* offsets, const int64_t* arrival,
+                                uint32_t n) {
+  GlobalHdr* g = reinterpret_cast<GlobalHdr*>(ws + L.off_global);
+  uint32_t bits = 0;
+  for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n;
+       j += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t o0 = offsets[j], o1 = offsets[j + 1];
+    if (o1 <= o0 || o1 - o0 > L.maxL) bits |= KVR_DEV_BAD_LENGTH;
+    const int64_t prev = j == 0 ? g->last_arrival : arrival[j - 1];
+    if (arrival[j] < prev) bits |= KVR_DEV_BAD_ARRIVAL;
+  }
+  if (bits) atomicOr(&g->status, bits);
+}
+
+// Token ids must be >= 0 (checked only when the offsets passed).
+__global__ void validate_tokens_kernel(char* ws, Layout L, const int32_t* tokens,
+                                       const uint64_t* offsets, uint32_t n) {
+  GlobalHdr* g = reinterpret_cast<GlobalHdr*>(ws + L.off_global);
+  if (__atomic_load_n(&g->status, __ATOMIC_RELAXED)) return;
+  const uint64_t b = offsets[0], e = offsets[n];
+  uint32_t bad = 0;
+  for (uint64_t x = b + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; x < e;
+       x += (uint64_t)gridDim.x * blockDim.x)
+    if (tokens[x] < 0) bad = 1;
+  if (__ballot(bad != 0) && lane_id() == 0) atomicOr(&g->status, (uint32_t)KVR_DEV_BAD_TOKEN);
+}
+
+// Final state of every (replica, worker).
+__global__ void stats_kernel(char* ws, Layout L) {
+  const uint64_t widx = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  Ptrs P = worker_ptrs(ws, L, (uint32_t)(widx / L.W), (uint32_t)(widx % L.W));
+  worker_stats(P, reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats) + widx);
+}
+
+// ---------------------------------------------------------------- launchers (host)
+
+hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st) {
+  const uint64_t work = (uint64_t)L.R * L.W > L.R ? (uint64_t)L.R * L.W : L.R;
+  const uint32_t blocks = (uint32_t)((work + 255) / 256);
+  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, st, ws, L, rls_p0);
+  return hipGetLastError();
+}
+
+hipError_t launch_step(const StepArgs& a, hipStream_t st) {
+  const uint32_t blocks_v = (a.n + 255) / 256 < 1024 ? (a.n + 255) / 256 : 1024;
+  hipLaunchKernelGGL(validate_kernel, dim3(blocks_v ? blocks_v : 1), dim3(256), 0, st, a.ws, a.L,
+                     a.offsets, a.arrival, a.n);
+  hipLaunchKernelGGL(validate_tokens_kernel, dim3(1024), dim3(256), 0, st, a.ws, a.L, a.tokens,
+                     a.offsets, a.n);
+  const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
+  const size_t lds = (size_t)a.L.maxL * sizeof(int32_t);
+  hipLaunchKernelGGL(step_kernel, dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st) {
+  hipLaunchKernelGGL(stats_kernel, dim3(L.R * L.W), dim3(64), 0, st, ws, L);
+  return hipGetLastError();
+}
+
+hipError_t set_step_lds_limit(size_t bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(step_kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+}  // namespace kvr

@@ -1,0 +1,188 @@
+// kvr_layout.h - workspace layout of the HIP simulator (internal).
+//
+// One workspace holds every replica.  Per (replica r, worker i) there is a
+// fixed-size block of each region below, addressed by (r * W + i) * stride,
+// so the replicas stay independent and one workgroup owns one replica.
+//
+//   global header   status word, last arrival, queries routed
+//   replica headers previous arrival time per replica
+//   worker headers  cache counters, marking state, LBGR state, counters
+//   node tables     compressed radix-tree nodes (32 B each), node 0 = root
+//   arenas          two semispaces of int32 words holding edge tokens and
+//                   child arrays; a copying collector compacts live data
+//                   into the other semispace when the active one fills
+//   leaf arrays     every leaf node, in lexicographic order of root paths
+//   U arrays        the RLT candidates: leaves whose leaf token is not
+//                   marked, in the same order
+//   pending rings   completion records (FIFO per worker)
+//   scratch         stack for the digest walk of kvr_stats
+//   stats out       kvr_worker_stats staging for kvr_stats
+#ifndef KVR_LAYOUT_H
+#define KVR_LAYOUT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/kvr.h"
+
+namespace kvr {
+
+constexpr uint32_t kMaxWorkers = 64;
+constexpr uint32_t kWave = 64;
+#ifndef KVR_MAX_WAVES
+#define KVR_MAX_WAVES 16
+#endif
+constexpr uint32_t kMaxWavesPerBlock = KVR_MAX_WAVES;
+
+// A compressed radix-tree node.  Its edge is `len` tokens at arena[off].
+// Tokens of the edge are positions off..off+len-1; the last one is the
+// node's leaf token when the node has no children.
+// Marks: positions [0, ma) are marked when mphase equals the worker phase;
+// one further interval per worker (WorkerHdr::rnode/rlo/rhi/rphase) holds
+// the marks left by a phase reset in the middle of an edge.
+struct NodeRec {
+  int32_t parent;   // -1 for the root, -2 for a free slot
+  uint32_t off;     // edge offset in the active arena; free slot: next free id
+  int32_t len;      // edge length in tokens
+  int32_t nchild;   // number of children
+  uint32_t coff;    // child array offset in the active arena (even)
+  int32_t ccap;     // child array capacity in entries (token, node) pairs
+  uint32_t mphase;  // phase of the prefix marks
+  int32_t ma;       // prefix marks [0, ma)
+};
+static_assert(sizeof(NodeRec) == 32, "node record is 32 bytes");
+
+struct PendRec {      // completion record, 48 B
+  int64_t t_route;    // arrival time of the query (us)
+  int64_t t_done;     // completion time (us)
+  double chat;        // estimated service time (s)
+  double base;        // estimated service time + queue load at routing (s)
+  double x3;          // queue load at routing (feature 3)
+  int32_t h;          // hit tokens on this worker
+  int32_t L;          // query length
+};
+static_assert(sizeof(PendRec) == 48, "pending record is 48 bytes");
+
+struct WorkerHdr {
+  // cache
+  uint32_t phase, cnt, size, hwm;
+  int32_t free_head;
+  uint32_t nleaves, nU, U_valid;
+  int32_t rnode, rlo, rhi;
+  uint32_t rphase;
+  uint32_t arena_sel, arena_top, nnodes, pad0;
+  // LBGR
+  double P;
+  double theta[4];
+  double Pm[16];
+  int64_t tl, Wb;
+  uint32_t pend_head, pend_count;
+  // counters
+  uint64_t routed, prompt_tokens, hit_tokens, matched_tokens;
+  uint64_t loads, evictions, forced_resets, completions, pending_max;
+  uint64_t lat_sum_us, lat_max_us, gc_runs;
+  uint8_t pad[512 - 352];
+};
+static_assert(sizeof(WorkerHdr) == 512, "worker header is 512 bytes");
+
+struct ReplicaHdr {
+  int64_t tprev;
+  int64_t pad[7];
+};
+
+struct GlobalHdr {
+  uint32_t status;       // KVR_DEV_* bits, sticky
+  uint32_t err_taken;    // 1 once the first error below was recorded
+  int64_t last_arrival;  // arrival time of the last routed query
+  // first device-side error: check id, replica, global query index, and
+  // three values of the failing check
+  uint32_t err_check, err_replica;
+  uint64_t err_query;
+  int64_t err_val[3];
+  uint64_t pad[1];
+};
+static_assert(sizeof(GlobalHdr) == 64, "global header is 64 bytes");
+
+struct Layout {
+  uint32_t R, W, B, maxL, NC, A, PC;
+  uint32_t pad0;
+  uint64_t off_global, off_rhdr, off_whdr, off_nodes, off_arena, off_leaf, off_U, off_pend,
+      off_scratch, off_stats, total;
+  uint64_t node_stride, arena_stride, leaf_stride, pend_stride, scratch_stride;
+};
+
+// Constants of one run, passed by value to the kernels.
+struct Consts {
+  uint64_t seed;
+  double alpha_cached, alpha_miss, rho, lr, nlms_eps, rls_p0;
+  int64_t dt_us, true_cached_us, true_miss_us, true_out_us;
+  int32_t update;
+  int32_t evict;
+};
+
+// Arguments of one batch for the step kernel (device pointers).
+struct StepArgs {
+  char* ws;
+  Layout L;
+  Consts C;
+  const int32_t* tokens;
+  const uint64_t* offsets;
+  const int64_t* arrival;
+  const uint16_t* out_len;
+  int32_t* route;
+  int32_t* hits;
+  int32_t* all_hits;
+  uint32_t n;
+  uint64_t j0;
+};
+
+inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Compute the layout for a validated configuration.
+inline Layout make_layout(const kvr_config& c) {
+  Layout L{};
+  L.R = c.num_replicas;
+  L.W = c.num_workers;
+  L.B = c.cache_tokens;
+  L.maxL = c.max_query_tokens;
+  // every non-root node holds >= 1 token, and an insertion adds at most a split
+  // head and the new leaf before its evictions free space: B + 3 always fits
+  L.NC = c.node_capacity ? c.node_capacity : c.cache_tokens + 3u;
+  uint64_t dflt_arena = 2ull * c.cache_tokens + 2ull * c.max_query_tokens + 4096ull;
+  L.A = c.arena_words ? c.arena_words : (uint32_t)dflt_arena;
+  L.A &= ~1u;  // even, so child arrays stay 8-byte aligned in both semispaces
+  L.PC = c.pending_capacity;
+  const uint64_t RW = (uint64_t)L.R * L.W;
+  uint64_t o = 0;
+  L.off_global = o;
+  o = align_up(o + sizeof(GlobalHdr), 256);
+  L.off_rhdr = o;
+  o = align_up(o + (uint64_t)L.R * sizeof(ReplicaHdr), 256);
+  L.off_whdr = o;
+  o = align_up(o + RW * sizeof(WorkerHdr), 256);
+  L.node_stride = align_up((uint64_t)L.NC * sizeof(NodeRec), 256);
+  L.off_nodes = o;
+  o += RW * L.node_stride;
+  L.arena_stride = align_up(2ull * L.A * 4ull, 256);
+  L.off_arena = o;
+  o += RW * L.arena_stride;
+  L.leaf_stride = align_up((uint64_t)L.NC * 4ull, 256);
+  L.off_leaf = o;
+  o += RW * L.leaf_stride;
+  L.off_U = o;
+  o += RW * L.leaf_stride;
+  L.pend_stride = align_up((uint64_t)L.PC * sizeof(PendRec), 256);
+  L.off_pend = o;
+  o += RW * L.pend_stride;
+  L.scratch_stride = align_up((uint64_t)L.NC * 16ull, 256);
+  L.off_scratch = o;
+  o += RW * L.scratch_stride;
+  L.off_stats = o;
+  o = align_up(o + RW * sizeof(kvr_worker_stats), 256);
+  L.total = o;
+  return L;
+}
+
+}  // namespace kvr
+
+#endif  // KVR_LAYOUT_H

@@ -1,0 +1,26 @@
+// emul_wave.h - single-lane host stand-ins for the wave intrinsics used by
+// paper_2601_18999_amd/csrc/kvr_core.h, so its logic can be compiled with g++
+// and replayed on the CPU in tests (KVR_WAVE = 1: every lane-parallel loop
+// becomes a sequential loop, every ballot has one lane).  Test-only.
+#pragma once
+#include <cstdint>
+#include <cstddef>
+
+#define KVR_WAVE 1
+#define __device__
+#define __forceinline__ inline
+#define __builtin_amdgcn_wave_barrier() ((void)0)
+#define __builtin_amdgcn_fence(order, scope) ((void)0)
+
+struct kvr_emul_dim3 { unsigned x, y, z; };
+static const kvr_emul_dim3 threadIdx = {0, 0, 0};
+struct int2 { int x, y; };
+
+inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
+inline int __shfl(int v, int, int) { return v; }
+inline int __shfl_xor(int v, int, int) { return v; }
+inline int __ffsll(unsigned long long m) { return __builtin_ffsll((long long)m); }
+inline int __popcll(unsigned long long m) { return __builtin_popcountll(m); }
+inline uint64_t __umul64hi(uint64_t a, uint64_t b) {
+  return (uint64_t)(((unsigned __int128)a * b) >> 64);
+}

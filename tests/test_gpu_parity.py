@@ -1,0 +1,198 @@
+"""HIP path vs the CPU oracle, through the C ABI, on an MI355X.
+
+Bit-exact on routes, every h_ij, hit counts, cache digests (path hashes of
+every cached token), marking state and counters; the load estimate and the
+residual model to 1e-9 relative.  Sizes are ones the oracle finishes in
+seconds but that still cover many 64-token tiles, ragged tails, phase
+resets, forced resets and collector runs.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import paper_2601_18999_amd as K
+from oracle import oracle as O
+from workload import PRESETS, generate, small_spec
+from gpu_helpers import assert_parity, gpu_run, note
+import spec_model as SM
+
+pytestmark = pytest.mark.gpu
+
+
+def test_device_present():
+    import torch
+    assert torch.cuda.is_available()
+    note(f"device: {torch.cuda.get_device_name(0)}")
+    K.load_library()
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_small_random_parity(case):
+    rng = np.random.default_rng(100 + case)
+    vocab = int(rng.integers(2, 40))
+    sp = small_spec(n=int(rng.integers(60, 400)), groups=int(rng.integers(1, 9)),
+                    prefix_len=(1, int(rng.integers(3, 90))), suffix_len=(1, int(rng.integers(2, 70))),
+                    vocab=vocab, seed=case)
+    s = generate(sp)
+    W = int(rng.integers(1, 7))
+    B = int(max(s.max_len, rng.integers(2, 600)))
+    R = 3
+    upd = ["nlms", "rls", "none"][case % 3]
+    note(f"case {case}: R={R} W={W} B={B} n={s.n} vocab={vocab} update={upd}")
+    res, stats = gpu_run(s, R, W, B, update=upd, seed=case)
+    assert_parity(s, res, stats, W, B, range(R), update=upd, seed=case)
+
+
+def test_collector_under_small_arena():
+    s = generate(small_spec(n=500, groups=6, prefix_len=(10, 70), suffix_len=(5, 50), vocab=30))
+    W, B, R = 3, 320, 4
+    note("collector stress")
+    res, stats = gpu_run(s, R, W, B, arena_words=B + 2 * s.max_len + 100)
+    assert sum(w["gc_runs"] for rr in stats for w in rr) > 50
+    assert_parity(s, res, stats, W, B, range(R))
+
+
+def test_many_waves_per_replica():
+    """W = 24 workers: 16 waves per workgroup, several workers per wave."""
+    s = generate(small_spec(n=300, groups=12, prefix_len=(20, 120), suffix_len=(5, 40), vocab=200))
+    W, B, R = 24, 500, 3
+    res, stats = gpu_run(s, R, W, B)
+    assert_parity(s, res, stats, W, B, range(R))
+
+
+def test_config1_full_all_replicas_ragged_batches():
+    p = PRESETS[1]
+    s = generate(p["stream"])
+    R = 8
+    note("config 1, R=8, batches of 333")
+    res, stats = gpu_run(s, R, p["W"], p["B"], batch=333)
+    assert_parity(s, res, stats, p["W"], p["B"], range(R))
+
+
+def test_config2_full_sampled_replicas():
+    p = PRESETS[2]
+    s = generate(p["stream"])
+    import time
+    t0 = time.time()
+    res, stats = gpu_run(s, p["R"], p["W"], p["B"], batch=2500)
+    t1 = time.time()
+    assert_parity(s, res, stats, p["W"], p["B"], [0, 21, 42, 63])
+    note(f"config 2, R=64, n={s.n}: gpu {t1 - t0:.2f}s, oracle x4 {time.time() - t1:.2f}s, "
+         f"evictions {sum(w['evictions'] for rr in stats for w in rr)}")
+
+
+def test_batch_split_invariance_and_determinism():
+    s = generate(small_spec(n=400, groups=5, prefix_len=(5, 50), suffix_len=(3, 30), vocab=12))
+    W, B, R = 3, 200, 4
+    a, sa = gpu_run(s, R, W, B, batch=0)
+    b, sb = gpu_run(s, R, W, B, batch=37)
+    c, sc = gpu_run(s, R, W, B, batch=1)
+    d, sd = gpu_run(s, R, W, B, batch=0)
+    for x, sx in ((b, sb), (c, sc), (d, sd)):
+        np.testing.assert_array_equal(a["route"], x["route"])
+        np.testing.assert_array_equal(a["all_hits"], x["all_hits"])
+        assert sa == sx
+
+
+def test_replicas_differ_only_by_random_key():
+    """All replicas see the same stream; with no eviction they are identical."""
+    s = generate(small_spec(n=200, groups=4, prefix_len=(5, 30), suffix_len=(3, 20), vocab=9))
+    W, R = 3, 5
+    res, stats = gpu_run(s, R, W, 10**5)
+    for r in range(1, R):
+        np.testing.assert_array_equal(res["route"][0], res["route"][r])
+        assert stats[0] == stats[r]
+    assert sum(w["evictions"] for w in stats[0]) == 0
+
+
+# ---------------------------------------------------------------- randomised semantics
+
+EXACT_CASES = [
+    (5, [(0, 1, 2), (0, 1, 3), (0, 2), (1, 2, 3), (0, 1, 2), (1, 2), (0, 1, 3), (0, 2, 1),
+         (1, 2, 3), (0, 1, 2)]),
+    (4, [(0, 1), (0, 2), (1, 0), (0, 1, 2), (1, 1), (0, 2), (2,), (0, 1), (1, 0, 1), (0, 2)]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(EXACT_CASES)))
+def test_mean_hits_match_exact_enumeration(case):
+    B, queries = EXACT_CASES[case]
+    exact = SM.expected_hits(queries, B)
+    s = generate({"kind": "paths", "paths": [list(q) for q in queries],
+                  "order": list(range(len(queries)))})
+    R = 20000
+    res, _ = gpu_run(s, R, 1, B, all_hits=False)
+    assert res["status"] == K.KVR_OK, (res["status"], res["bits"])
+    tot = res["hits"].sum(1).astype(float)
+    sd = tot.std(ddof=1) / math.sqrt(R)
+    assert abs(tot.mean() - float(sum(exact))) < 4 * sd, (tot.mean(), float(sum(exact)), sd)
+
+
+def test_uniform_tail_miss_probability():
+    B, L = 16, 4
+    n_t = B - L + 2
+    prefix = list(range(100, 100 + L - 1))
+    paths = [prefix + [k] for k in range(n_t)]
+    rng = np.random.default_rng(4)
+    order = [int(x) for x in rng.integers(0, n_t, size=2000)]
+    s = generate({"kind": "paths", "paths": paths, "order": order})
+    R = 64
+    res, _ = gpu_run(s, R, 1, B, all_hits=False)
+    assert res["status"] == K.KVR_OK, (res["status"], res["bits"])
+    h = res["hits"][:, 500:]
+    assert (h >= L - 1).all()
+    misses, total = int((h == L - 1).sum()), h.size
+    p = 1.0 / n_t
+    assert abs(misses - total * p) < 4 * math.sqrt(total * p * (1 - p))
+
+
+# ---------------------------------------------------------------- error paths
+
+def _sim_for(s, **cfg):
+    return K.Simulator(2, 2, 100, max(1, s.max_len), **cfg)
+
+
+def test_invalid_batches_are_rejected_before_any_state_change():
+    import torch
+    s = generate(small_spec(n=50, groups=3, prefix_len=(3, 10), suffix_len=(2, 8), vocab=7))
+    for kind in ("empty_query", "negative_token", "decreasing_arrival"):
+        sim = _sim_for(s)
+        ds = sim.upload(s)
+        sim.route(ds, 0, 20)
+        before = sim.stats()
+        bad = generate(small_spec(n=10, groups=2, prefix_len=(3, 10), suffix_len=(2, 8), vocab=7, seed=9))
+        if kind == "empty_query":
+            bad.offsets = bad.offsets.copy()
+            bad.offsets[3] = bad.offsets[2]
+        elif kind == "negative_token":
+            bad.tokens = bad.tokens.copy()
+            bad.tokens[5] = -3
+        else:
+            bad.arrival_us = np.zeros(bad.n, np.int64)
+        dbad = sim.upload(bad)
+        sim.route(dbad, 0, bad.n)
+        st, bits = sim.check()
+        assert st == K.KVR_EINVAL, (kind, st, bits)
+        after = sim.stats(check=False)
+        assert before == after, kind
+        with pytest.raises(K.KvrError) as ei:
+            sim.route(ds, 20, 5)
+        assert ei.value.status == K.KVR_ESTATE
+        sim.close()
+        torch.cuda.synchronize()
+
+
+def test_capacity_errors_are_reported():
+    s = generate(small_spec(n=200, groups=3, prefix_len=(3, 20), suffix_len=(2, 15), vocab=50))
+    s.arrival_us = np.arange(s.n, dtype=np.int64)  # arrivals 1 us apart: completions pile up
+    sim = K.Simulator(2, 1, 400, s.max_len, pending_capacity=2)
+    sim.run(s)
+    st, bits = sim.check()
+    assert st == K.KVR_ECAPACITY and bits & 8
+    sim.close()
+    sim = K.Simulator(2, 2, 400, s.max_len, node_capacity=4)
+    sim.run(s)
+    st, bits = sim.check()
+    assert st == K.KVR_ECAPACITY and bits & 16
+    sim.close()

@@ -1,0 +1,63 @@
+"""The step kernel's per-wave logic (paper_2601_18999_amd/csrc/kvr_core.h),
+compiled for one lane with g++ and replayed on the CPU, against the oracle:
+compressed tree, interval marks, ordered candidate list and the copying
+collector must reproduce the per-token definition exactly."""
+import numpy as np
+import pytest
+
+import emul_kernel as E
+from oracle import oracle as O
+from workload import PRESETS, generate, small_spec
+
+
+def _compare(s, R, W, B, update="nlms", seed=0, **cfg):
+    e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, **cfg)
+    assert e["rc"] == 0
+    for r in range(R):
+        o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed)
+        np.testing.assert_array_equal(e["route"][r], o["route"])
+        np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
+        for i in range(W):
+            g, c = e["workers"][r][i], o["workers"][i]
+            assert {k: g[k] for k in c} == c, (r, i)
+    return e
+
+
+@pytest.mark.parametrize("block", range(4))
+def test_random_instances(block):
+    rng = np.random.default_rng(77 + block)
+    for case in range(40):
+        vocab = int(rng.integers(2, 12))
+        sp = small_spec(n=int(rng.integers(20, 160)), groups=int(rng.integers(1, 8)),
+                        prefix_len=(1, int(rng.integers(2, 30))), suffix_len=(1, int(rng.integers(2, 20))),
+                        vocab=vocab, seed=1000 * block + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 5))
+        B = int(max(s.max_len, rng.integers(2, 150)))
+        _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case)
+
+
+def test_collector_stress():
+    s = generate(small_spec(n=400, groups=6, prefix_len=(10, 60), suffix_len=(5, 40), vocab=30))
+    B = 300
+    e = _compare(s, 2, 3, B, arena_words=B + 2 * s.max_len + 64)
+    assert sum(w["gc_runs"] for rr in e["workers"] for w in rr) > 50
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_presets(cfg):
+    p = PRESETS[cfg]
+    s = generate(p["stream"])
+    if cfg == 2:
+        s = s.head(4000)
+    _compare(s, 2, p["W"], p["B"])
+
+
+def test_tiny_caches_from_the_exact_enumeration_cases():
+    """Caches of 4-6 tokens: the node table must hold the transient split
+    head and new leaf of an insertion into a full cache."""
+    from test_oracle_pins import EXACT_CASES
+    for B, queries in EXACT_CASES:
+        s = generate({"kind": "paths", "paths": [list(q) for q in queries],
+                      "order": list(range(len(queries)))})
+        _compare(s, 64, 1, B)
