@@ -1,0 +1,189 @@
+#!/usr/bin/env python3
+"""Benchmark: batched KV-cache routing (LBGR) + RLT eviction on one MI355X.
+
+A step is one kvr_route_batch call: one batch of `--batch` queries of the
+synthetic stream, routed for every replica (completions and decay, the match
+on every worker, LBGR score/argmin/commit, RLT insertion).  The first
+`--warmup` batches fill the caches untimed; the next `--steps` batches are
+timed with events on the library's stream, with the stream and workspace
+already resident in HBM.  Prints one JSON line.
+
+Default workload: the largest configuration (32 replicas x 32 workers,
+262,144-token caches, prompts of 2,176-9,216 tokens from 256 Zipf groups in
+on/off bursts).  Other configurations: --config 1..5.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2601_18999_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2601_18999_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per step-kernel launch measured by rocprofv3 counters, if
+    they were taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t
+
+
+def totals(stats):
+    keys = ("matched_tokens", "prompt_tokens", "hit_tokens", "loads", "evictions", "routed")
+    return {k: sum(w[k] for rr in stats for w in rr) for k in keys}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(stream, W, B, budget_s: float):
+    """The CPU oracle, single-threaded, on replica 0 of the same stream: the
+    first n queries, n doubled until one run takes at least budget_s / 2."""
+    from oracle import oracle as O
+    n = min(1000, stream.n)
+    while True:
+        t0 = time.perf_counter()
+        O.run(stream, W, B, replica=0, n=n)
+        dt = time.perf_counter() - t0
+        log(f"cpu oracle: {n} queries in {dt:.1f} s")
+        if dt >= budget_s / 2 or n >= stream.n:
+            break
+        n = min(stream.n, 2 * n)
+    return {"value": n / dt, "unit": "queries/s", "cores": 1, "kind": "oracle",
+            "sample": f"replica 0, queries 0..{n} of the same stream, one thread, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=6)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--batch", type=int, default=2000)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print("bench.py runs on one GPU only: replicas are independent, and this build measures "
+              "one GPU's share; multi-GPU sharding over replicas is not built. Use --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2601_18999_amd as K
+    from workload import PRESETS, generate
+
+    p = PRESETS[args.config]
+    R, W, B = p["R"], p["W"], p["B"]
+    t0 = time.perf_counter()
+    stream = generate(p["stream"])
+    log(f"{p['name']}: {stream.n} queries, {stream.tokens.size} tokens ({time.perf_counter() - t0:.1f} s)")
+    need = (args.warmup + args.steps) * args.batch
+    if need > stream.n:
+        print(f"warmup+steps need {need} queries, the stream has {stream.n}", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0")
+    ds = sim.upload(stream)
+    out = sim.alloc_outputs(args.batch)
+    torch.cuda.synchronize()
+
+    log(f"workspace {sim.nbytes / 1e9:.1f} GB, stream resident")
+    q = 0
+    for k in range(args.warmup):
+        sim.route(ds, q, args.batch, out=out)
+        torch.cuda.synchronize()
+        q += args.batch
+        log(f"warmup batch {k + 1}/{args.warmup} done")
+    before = totals(sim.stats())
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    q0 = q
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(sim.stream)
+        sim.route(ds, q, args.batch, out=out)
+        ev[k][1].record(sim.stream)
+        q += args.batch
+        ev[k][1].synchronize()
+        log(f"timed batch {k + 1}/{args.steps}: {ev[k][0].elapsed_time(ev[k][1]):.1f} ms")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st, bits = sim.check()
+    if st != K.KVR_OK:
+        print(f"device status {st} bits {bits}: {K.kvr_last_error()}", file=sys.stderr)
+        return 1
+    after = totals(sim.stats())
+    d = {k: after[k] - before[k] for k in after}
+    kernel_ms = sum(a.elapsed_time(b) for a, b in ev)
+    nq = R * (q - q0)
+    lens = stream.lengths[q0:q].astype("int64")
+    prompt = int(lens.sum()) * R
+    assert prompt == d["prompt_tokens"]
+    # algorithmic bytes of the timed launches: query staging, edge tokens
+    # compared on every worker, edge tokens written for loaded tokens, one
+    # candidate/node read-modify-write per eviction, LBGR + completion record
+    alg_bytes = (4 * prompt + 4 * d["matched_tokens"] + 4 * d["loads"] + 32 * d["evictions"]
+                 + 96 * nq)
+    achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
+    workload = p["name"]
+    traffic = load_traffic(workload)
+    line = {
+        "metric": "routed queries/sec",
+        "value": nq / (kernel_ms * 1e-3),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": kernel_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i32+f64",
+        "data": "synthetic",
+        "config": {"workload": workload, "replicas": R, "workers": W, "cache_tokens": B,
+                   "batch_queries": args.batch, "timed_queries": q - q0,
+                   "first_timed_query": q0, "stream_queries": stream.n},
+        "prefix_matched_tokens_per_s": d["matched_tokens"] / (kernel_ms * 1e-3),
+        "routed_hit_tokens_per_s": d["hit_tokens"] / (kernel_ms * 1e-3),
+        "evictions_per_s": d["evictions"] / (kernel_ms * 1e-3),
+        "wall_s": wall,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic["bytes_per_launch"] if traffic else None,
+                     "alg_bytes_per_launch": alg_bytes / args.steps},
+    }
+    sim.close()
+    del ds, out
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

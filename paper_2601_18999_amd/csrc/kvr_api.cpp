@@ -19,6 +19,7 @@ hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st)
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st);
 hipError_t set_step_lds_limit(size_t bytes);
+size_t step_lds_bytes(uint32_t maxL, uint32_t ucap, uint32_t rcap);
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -29,6 +30,8 @@ struct kvr_ctx {
   int device;
   uint64_t queries_done;
   uint32_t seen_bits;  // device status bits already reported to the host
+  uint32_t ucap;       // candidate entries the step kernel stages in LDS
+  uint32_t rcap;       // draw words the step kernel precomputes in LDS
 };
 
 namespace {
@@ -164,7 +167,24 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
-  const size_t lds = (size_t)L.maxL * sizeof(int32_t);
+  // LDS per workgroup: the query buffer plus as much of the candidate list as
+  // fits (16 B per entry, at most 8192 entries)
+  int lds_max = 0;
+  e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return fail_hip(e, "hipDeviceGetAttribute(max LDS per block)");
+  const size_t static_lds = 2048;
+  const size_t qbytes = kvr::step_lds_bytes(L.maxL, 0, 0);
+  if (qbytes + static_lds > (size_t)lds_max)
+    return fail(KVR_EINVAL, "max_query_tokens does not fit in LDS (" + std::to_string(lds_max) + " bytes)");
+  size_t room = (size_t)lds_max - static_lds - qbytes;
+  // precomputed draw words first (8 B each, up to 4096), then candidates
+  size_t rcap = room / 2 / 8u;
+  if (rcap > 4096) rcap = 4096;
+  room -= rcap * 8u;
+  size_t ucap = room / 16u;
+  if (ucap > 8192) ucap = 8192;
+  if (ucap < 64) ucap = 0;
+  const size_t lds = kvr::step_lds_bytes(L.maxL, (uint32_t)ucap, (uint32_t)rcap);
   if (lds > 65536) {
     e = kvr::set_step_lds_limit(lds);
     if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
@@ -190,6 +210,8 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   c->device = dev;
   c->queries_done = 0;
   c->seen_bits = 0;
+  c->ucap = (uint32_t)ucap;
+  c->rcap = (uint32_t)rcap;
   e = kvr::launch_init(c->ws, L, cfg->rls_p0, c->stream);
   if (e != hipSuccess) {
     delete c;
@@ -219,6 +241,8 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens, co
   a.hits = d_hits;
   a.all_hits = d_all_hits;
   a.n = n;
+  a.ucap = ctx->ucap;
+  a.rcap = ctx->rcap;
   a.j0 = ctx->queries_done;
   hipError_t e = kvr::launch_step(a, ctx->stream);
   if (e != hipSuccess) return fail_hip(e, "step kernel launch");

@@ -25,6 +25,10 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return (1ull << (uint32_t)lane_id()) - 1ull;
 }
 
+__device__ __forceinline__ uint64_t lanemask_le() {
+  return (2ull << (uint32_t)lane_id()) - 1ull;
+}
+
 #ifndef KVR_SYNC_SCOPE
 #define KVR_SYNC_SCOPE "workgroup"
 #endif
@@ -217,6 +221,15 @@ __device__ __forceinline__ bool is_marked(const St& s, const NodeRec& nd, int32_
   if (nd.mphase == s.phase && pos < nd.ma) return true;
   if (s.rphase == s.phase && s.rnode == id && pos >= s.rlo && pos < s.rhi) return true;
   return false;
+}
+
+// First edge position from which the tail of a leaf is unmarked: every
+// position >= mark_top is evictable (the marked positions form [0, ma) and,
+// on one node per phase, [rlo, rhi)).
+__device__ __forceinline__ int32_t mark_top(const St& s, const NodeRec& nd, int32_t id) {
+  int32_t top = (nd.mphase == s.phase) ? nd.ma : 0;
+  if (s.rphase == s.phase && s.rnode == id && s.rhi > top) top = s.rhi;
+  return top;
 }
 
 // ---------------------------------------------------------------- array tools (wave)
@@ -549,29 +562,10 @@ __device__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
   s.U_valid = 1;
 }
 
-// Evict the leaf token of candidate U[kk].  False on an inconsistency.
-__device__ bool evict_one(const Ptrs& P, St& s, uint32_t kk) {
-  int32_t n = P.U[kk];
-  if (n <= 0 || (uint32_t)n >= s.hwm) {
-    KVR_FAIL_CHECK(s, 10, kk, n, s.nU);
-    return false;
-  }
-  NodeRec nd = P.nodes[n];
-  if (nd.len <= 0 || nd.nchild != 0 || nd.parent < 0) {
-    KVR_FAIL_CHECK(s, 11, n, nd.len, nd.nchild);
-    return false;
-  }
-  int32_t nl = nd.len - 1;
-  if (nl > 0) {
-    if (lane_id() == 0) P.nodes[n].len = nl;
-    wave_mem_sync();
-    if (is_marked(s, nd, n, nl - 1)) {
-      arr_erase(P.U, s.nU, kk);
-      s.nU -= 1;
-    }
-    return true;
-  }
-  int32_t p = nd.parent;
+// The candidate at U[kk], node n with parent p, has just lost its last
+// token: drop it from the tree and the leaf list; its parent, if that became
+// an unmarked leaf, takes its place (and rank) in U, else the entry goes.
+__device__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk, int32_t n, int32_t p) {
   int32_t li = arr_find(P.leaf, s.nleaves, n);
   if (li < 0) {
     KVR_FAIL_CHECK(s, 12, n, s.nleaves, kk);
@@ -584,7 +578,6 @@ __device__ bool evict_one(const Ptrs& P, St& s, uint32_t kk) {
   node_free(P, s, n);
   NodeRec np = P.nodes[p];
   if (p != 0 && np.nchild == 0) {
-    // the parent's last token is a new leaf token, at the rank of n
     if (lane_id() == 0) P.leaf[li] = p;
     wave_mem_sync();
     if (!is_marked(s, np, p, np.len - 1)) {
@@ -609,12 +602,254 @@ struct InsertArgs {
   uint32_t worker;    // routed worker
   uint32_t replica;
   uint32_t B;
+  uint32_t rn;        // draw words 0..rn-1 are precomputed in rw
+  const uint64_t* rw;
 };
+
+// Word 0 of Philox4x64-10 for draw d of this insertion: key (seed, replica),
+// counter (query index, worker, d, 0).
+__device__ __forceinline__ uint64_t draw_word(const InsertArgs& ia, uint64_t d) {
+  if (d < ia.rn) return ia.rw[d];
+  return philox_word0(ia.jg, ia.worker, d, 0ull, ia.seed, ia.replica);
+}
+
+// Evict with draws dctr .. dctr+cnt-1 (cnt <= wave width), one lane per
+// draw, all taken against the current U: a draw only trims the leaf token of
+// its candidate, so draws commute until one takes a candidate's last
+// evictable token (the next token is marked, or the node empties), which is
+// the only event that changes U.  Commits the draws up to and including the
+// first such one, applies it, and returns the number of draws consumed in
+// `done`.  Identical to taking the draws one at a time.
+__device__ bool evict_block(const Ptrs& P, St& s, const InsertArgs& ia, uint64_t dctr, uint32_t cnt,
+                            uint32_t& done) {
+  const int lane = lane_id();
+  const bool act = (uint32_t)lane < cnt;
+  uint32_t kk = 0;
+  int32_t n = 0;
+  if (act) {
+    const uint64_t r64 = draw_word(ia, dctr + (uint64_t)lane);
+    kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
+    n = P.U[kk];
+  }
+  if (__ballot(act && (n <= 0 || (uint32_t)n >= s.hwm))) {
+    KVR_FAIL_CHECK(s, 10, kk, n, s.nU);
+    return false;
+  }
+  NodeRec nd = P.nodes[act ? n : 0];
+  int32_t top = (nd.mphase == s.phase) ? nd.ma : 0;
+  if (s.rphase == s.phase && s.rnode == n && s.rhi > top) top = s.rhi;
+  const int32_t e = nd.len - top;  // evictable tail tokens of my candidate
+  if (__ballot(act && (e <= 0 || nd.nchild != 0 || nd.parent < 0))) {
+    KVR_FAIL_CHECK(s, 11, n, nd.len, nd.nchild);
+    return false;
+  }
+  // c = draws on my candidate up to and including mine; grp = their lanes
+  uint64_t todo = __ballot(act);
+  uint64_t grp = 0;
+  int32_t c = 0;
+  while (todo) {
+    const int ld = first_lane(todo);
+    const uint32_t v = (uint32_t)__shfl((int)kk, ld, KVR_WAVE);
+    const bool same = act && kk == v;
+    const uint64_t m = __ballot(same);
+    if (same) {
+      grp = m;
+      c = __popcll(m & lanemask_le());
+    }
+    todo &= ~m;
+  }
+  const uint64_t exm = __ballot(act && c == e);
+  const int f = exm ? first_lane(exm) : (int)cnt - 1;  // last committed draw
+  const uint64_t commit = (2ull << (uint32_t)f) - 1ull;
+  const uint64_t mine = grp & commit;
+  // the last committed draw on each candidate writes its new length
+  if (act && lane <= f && mine && 63 - __clzll((long long)mine) == lane)
+    P.nodes[n].len = nd.len - __popcll(mine);
+  wave_mem_sync();
+  done = (uint32_t)f + 1u;
+  if (exm) {
+    const uint32_t kkf = (uint32_t)__shfl((int)kk, f, KVR_WAVE);
+    const int32_t nf = __shfl(n, f, KVR_WAVE);
+    const int32_t pf = __shfl(nd.parent, f, KVR_WAVE);
+    const int32_t left = __shfl(top, f, KVR_WAVE);
+    if (left > 0) {  // the next token is marked: no longer a candidate
+      arr_erase(P.U, s.nU, kkf);
+      s.nU -= 1;
+    } else if (!remove_emptied(P, s, kkf, nf, pf)) {
+      return false;
+    }
+  }
+  return true;
+}
+
+// The candidate list staged in LDS for the eviction phase of an insertion:
+// entry k = (node, length, mark_top, parent) of U[k].  While staged, the LDS
+// copy is authoritative for U and for the lengths of the staged nodes; the
+// tree, leaf list and child arrays stay in global memory.
+struct UStage {
+  int32_t* node;
+  int32_t* len;
+  int32_t* top;
+  int32_t* par;
+  uint32_t cap;
+};
+
+__device__ __forceinline__ bool stage_in(const Ptrs& P, St& s, const UStage& u) {
+  bool bad = false;
+  for (uint32_t b = 0; b < s.nU; b += KVR_WAVE) {
+    const uint32_t k = b + (uint32_t)lane_id();
+    if (k < s.nU) {
+      const int32_t n = P.U[k];
+      if (n <= 0 || (uint32_t)n >= s.hwm) {
+        bad = true;
+      } else {
+        const NodeRec nd = P.nodes[n];
+        u.node[k] = n;
+        u.len[k] = nd.len;
+        u.top[k] = mark_top(s, nd, n);
+        u.par[k] = nd.parent;
+      }
+    }
+  }
+  wave_mem_sync();
+  if (__ballot(bad)) {
+    KVR_FAIL_CHECK(s, 14, s.nU, s.hwm, 0);
+    return false;
+  }
+  return true;
+}
+
+__device__ __forceinline__ void stage_out(const Ptrs& P, const St& s, const UStage& u) {
+  for (uint32_t b = 0; b < s.nU; b += KVR_WAVE) {
+    const uint32_t k = b + (uint32_t)lane_id();
+    if (k < s.nU) {
+      const int32_t n = u.node[k];
+      P.U[k] = n;
+      P.nodes[n].len = u.len[k];
+    }
+  }
+  wave_mem_sync();
+}
+
+// remove entry pos of the staged list (n entries); LDS only, so the wave's
+// in-order LDS accesses need no fence
+__device__ __forceinline__ void stage_erase(const UStage& u, uint32_t n, uint32_t pos) {
+  for (uint32_t lo = pos; lo + 1 < n; lo += KVR_WAVE) {
+    const uint32_t k = lo + (uint32_t)lane_id();
+    int32_t a = 0, b = 0, c = 0, d = 0;
+    if (k + 1 < n) {
+      a = u.node[k + 1];
+      b = u.len[k + 1];
+      c = u.top[k + 1];
+      d = u.par[k + 1];
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (k + 1 < n) {
+      u.node[k] = a;
+      u.len[k] = b;
+      u.top[k] = c;
+      u.par[k] = d;
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// evict_block with U staged in LDS (same draws, same result).  A draw whose
+// candidate has more than `cnt` evictable tokens cannot exhaust it within
+// the block, so only the lanes drawing nearly exhausted candidates need
+// their rank among equal draws; the committed trims are LDS decrements.
+__device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const InsertArgs& ia, const UStage& u,
+                                                   uint64_t dctr, uint32_t cnt, uint32_t& done) {
+  const int lane = lane_id();
+  const bool act = (uint32_t)lane < cnt;
+  uint32_t kk = 0;
+  int32_t n = 0, len = 0, top = 0, par = 0;
+  if (act) {
+    const uint64_t r64 = draw_word(ia, dctr + (uint64_t)lane);
+    kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
+    n = u.node[kk];
+    len = u.len[kk];
+    top = u.top[kk];
+    par = u.par[kk];
+  }
+  const int32_t e = len - top;
+  if (__ballot(act && (e <= 0 || par < 0))) {
+    KVR_FAIL_CHECK(s, 11, n, len, top);
+    return false;
+  }
+  int f = (int)cnt - 1;  // last committed draw
+  uint64_t exm = 0;
+  const uint64_t risky = __ballot(act && e <= (int32_t)cnt);
+  if (risky) {
+    // rank of each risky draw among the draws on its candidate, in order
+    uint64_t todo = risky;
+    int32_t c = 0;
+    while (todo) {
+      const int j = first_lane(todo);
+      const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk, j);
+      const bool same = act && kk == v;
+      const uint64_t m = __ballot(same);
+      if (same) c = __popcll(m & lanemask_le());
+      todo &= ~m;
+    }
+    exm = __ballot(((risky >> lane) & 1ull) && c == e);
+    if (exm) f = first_lane(exm);
+  }
+  if (act && lane <= f) atomicSub(&u.len[kk], 1);
+  done = (uint32_t)f + 1u;
+  if (exm) {
+    const uint32_t kkf = (uint32_t)__builtin_amdgcn_readlane((int)kk, f);
+    const int32_t nf = __builtin_amdgcn_readlane(n, f);
+    const int32_t pf = __builtin_amdgcn_readlane(par, f);
+    const int32_t left = __builtin_amdgcn_readlane(top, f);
+    if (left > 0) {  // the next token is marked: no longer a candidate
+      if (lane == 0) P.nodes[nf].len = left;
+      wave_mem_sync();
+      stage_erase(u, s.nU, kkf);
+      s.nU -= 1;
+      return true;
+    }
+    // the node is empty: drop it; its parent may take its place
+    const int32_t li = arr_find(P.leaf, s.nleaves, nf);
+    if (li < 0) {
+      KVR_FAIL_CHECK(s, 12, nf, s.nleaves, kkf);
+      return false;
+    }
+    if (!child_remove(P, s, pf, nf)) {
+      KVR_FAIL_CHECK(s, 13, nf, pf, 0);
+      return false;
+    }
+    node_free(P, s, nf);
+    const NodeRec np = P.nodes[pf];
+    if (pf != 0 && np.nchild == 0) {
+      if (lane == 0) P.leaf[li] = pf;
+      wave_mem_sync();
+      const int32_t ptop = mark_top(s, np, pf);
+      if (ptop < np.len) {
+        if (lane == 0) {
+          u.node[kkf] = pf;
+          u.len[kkf] = np.len;
+          u.top[kkf] = ptop;
+          u.par[kkf] = np.parent;
+        }
+      } else {
+        stage_erase(u, s.nU, kkf);
+        s.nU -= 1;
+      }
+    } else {
+      arr_erase(P.leaf, s.nleaves, (uint32_t)li);
+      s.nleaves -= 1;
+      stage_erase(u, s.nU, kkf);
+      s.nU -= 1;
+    }
+  }
+  return true;
+}
 
 // RLT insertion of q[0, L) into the worker's cache; h = LCP(q, cache).
 // Returns the KVR_DEV_* error bits (0 on success).
-__device__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
-                               int32_t h, int64_t* dbg) {
+__device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
+                               int32_t h, const UStage& ustage, int64_t* dbg) {
   St s = load_st(P.hdr);
   const uint32_t B = ia.B;
   int32_t* ar = arena_of(P, s.arena_sel);
@@ -782,9 +1017,15 @@ __device__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_
     int32_t reset_at = (c0 + (uint32_t)nload >= B + 1u) ? h + (int32_t)(B - c0) : -1;
     bool applied = false;
     uint64_t dctr = 0;
-    for (uint32_t k = 0; k < nev; ++k) {
+    uint32_t k = 0;
+    bool staged = false;
+    while (k < nev) {
       const int32_t p = h + (int32_t)nfree + (int32_t)k;
       if (reset_at >= 0 && !applied && p >= reset_at) {
+        if (staged) {
+          stage_out(P, s, ustage);
+          staged = false;
+        }
         s.phase += 1;
         s.U_valid = 0;
         applied = true;
@@ -792,6 +1033,10 @@ __device__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_
       if (!s.U_valid) rebuild_U(P, s, l);
       if (s.nU == 0) {
         // no unmarked leaf: a new phase starts with the current token
+        if (staged) {
+          stage_out(P, s, ustage);
+          staged = false;
+        }
         s.phase += 1;
         s.forced += 1;
         rebuild_U(P, s, l);
@@ -802,11 +1047,23 @@ __device__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_
           goto fail;
         }
       }
-      uint64_t r64 = philox_word0(ia.jg, ia.worker, dctr, 0ull, ia.seed, ia.replica);
-      dctr += 1;
-      uint32_t kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
-      if (!evict_one(P, s, kk)) goto fail;
+      if (!staged && s.nU <= ustage.cap) {
+        if (!stage_in(P, s, ustage)) goto fail;
+        staged = true;
+      }
+      // draws for positions p, p+1, ...: never across a pending phase reset
+      uint32_t cnt = nev - k < (uint32_t)KVR_WAVE ? nev - k : (uint32_t)KVR_WAVE;
+      if (reset_at >= 0 && !applied && (uint32_t)(reset_at - p) < cnt) cnt = (uint32_t)(reset_at - p);
+      uint32_t done = 0;
+      if (staged) {
+        if (!evict_block_staged(P, s, ia, ustage, dctr, cnt, done)) goto fail;
+      } else {
+        if (!evict_block(P, s, ia, dctr, cnt, done)) goto fail;
+      }
+      dctr += done;
+      k += done;
     }
+    if (staged) stage_out(P, s, ustage);
     if (reset_at >= 0 && !applied) {
       s.phase += 1;
       s.U_valid = 0;
@@ -853,12 +1110,24 @@ fail:
 
 // ---------------------------------------------------------------- matching
 
+// First index k < n with e[k] != q[k], or n.  Eight wave-wide loads are in
+// flight per iteration (512 tokens on a 64-lane wave).
 __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n) {
-  for (int32_t b = 0; b < n; b += KVR_WAVE) {
-    int32_t k = b + lane_id();
-    bool mis = (k < n) && (e[k] != q[k]);
-    uint64_t m = __ballot(mis);
-    if (m) return b + first_lane(m);
+  constexpr int kUnroll = 8;
+  for (int32_t b = 0; b < n; b += kUnroll * KVR_WAVE) {
+    int32_t ev[kUnroll], qv[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int32_t k = b + u * KVR_WAVE + lane_id();
+      ev[u] = k < n ? e[k] : 0;
+      qv[u] = k < n ? q[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int32_t k = b + u * KVR_WAVE + lane_id();
+      const uint64_t m = __ballot(k < n && ev[u] != qv[u]);
+      if (m) return b + u * KVR_WAVE + first_lane(m);
+    }
   }
   return n;
 }

@@ -43,12 +43,27 @@ namespace kvr {
 // ---------------------------------------------------------------- kernels
 
 __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
-  extern __shared__ int32_t qs[];  // the current query, max_query_tokens entries
+  // dynamic LDS: the current query (max_query_tokens entries), then the
+  // staged candidate list (ucap entries of node, length, mark_top, parent)
+  extern __shared__ int32_t smem[];
+  int32_t* qs = smem;
+  // draw words precomputed by every wave before the insertion (8-byte aligned)
+  uint64_t* rw = reinterpret_cast<uint64_t*>(smem + ((a.L.maxL + 3u) & ~3u));
+  UStage ustage;
+  {
+    int32_t* ub = reinterpret_cast<int32_t*>(rw + a.rcap);
+    ustage.node = ub;
+    ustage.len = ub + a.ucap;
+    ustage.top = ub + 2 * a.ucap;
+    ustage.par = ub + 3 * a.ucap;
+    ustage.cap = a.ucap;
+  }
   __shared__ int32_t h_sh[kMaxWorkers];
   __shared__ double eh_sh[kMaxWorkers];
   __shared__ double ch_sh[kMaxWorkers];
   __shared__ int32_t best_sh;
   __shared__ uint32_t abort_sh;
+  __shared__ uint32_t nev_sh;
 
   const uint32_t r = blockIdx.x;
   const uint32_t W = a.L.W;
@@ -114,15 +129,40 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
       if (a.all_hits && (uint32_t)lane < W)
         a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[lane];
       err = (uint32_t)__shfl((int)err, 0, KVR_WAVE);
-      if (!err) {
+      if (lane == 0) {
+        // draws this insertion will take: one per token loaded into a full cache
+        const uint32_t size = P.hdr->size;
+        const uint32_t nload = (uint32_t)(Lq - hb);
+        const uint32_t nfree = a.L.B - size;
+        nev_sh = err ? 0u : (nload > nfree ? nload - nfree : 0u);
+        if (err) {
+          atomicOr(&g->status, err);
+          abort_sh = 1;
+        }
+      }
+    }
+    __syncthreads();
+    if (abort_sh) break;
+    const uint32_t best = (uint32_t)best_sh;
+    const uint32_t nev = nev_sh;
+    const uint32_t rn = nev < a.rcap ? nev : a.rcap;
+    for (uint32_t d = threadIdx.x; d < rn; d += blockDim.x)
+      rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
+    if (rn) __syncthreads();
+    if (wave == 0) {
+      Ptrs P = worker_ptrs(a.ws, a.L, r, best);
+      uint32_t err = 0;
+      {
         InsertArgs ia;
         ia.seed = a.C.seed;
         ia.jg = a.j0 + k;
         ia.worker = best;
         ia.replica = r;
         ia.B = a.L.B;
+        ia.rn = rn;
+        ia.rw = rw;
         int64_t dbg[4] = {0, 0, 0, 0};
-        err = rlt_insert(P, ia, qs, Lq, hb, dbg);
+        err = rlt_insert(P, ia, qs, Lq, h_sh[best], ustage, dbg);
         if (lane == 0 && err && atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];
           g->err_replica = r;
@@ -198,6 +238,12 @@ __global__ void stats_kernel(char* ws, Layout L) {
 
 // ---------------------------------------------------------------- launchers (host)
 
+size_t step_lds_bytes(uint32_t maxL, uint32_t ucap, uint32_t rcap) {
+  return (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint64_t) +
+         (size_t)ucap * 4u * sizeof(int32_t);
+}
+
+
 hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st) {
   const uint64_t work = (uint64_t)L.R * L.W > L.R ? (uint64_t)L.R * L.W : L.R;
   const uint32_t blocks = (uint32_t)((work + 255) / 256);
@@ -212,7 +258,7 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(validate_tokens_kernel, dim3(1024), dim3(256), 0, st, a.ws, a.L, a.tokens,
                      a.offsets, a.n);
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
-  const size_t lds = (size_t)a.L.maxL * sizeof(int32_t);
+  const size_t lds = step_lds_bytes(a.L.maxL, a.ucap, a.rcap);
   hipLaunchKernelGGL(step_kernel, dim3(a.L.R), dim3(64 * waves), lds, st, a);
   return hipGetLastError();
 }

@@ -133,6 +133,8 @@ struct StepArgs {
   int32_t* hits;
   int32_t* all_hits;
   uint32_t n;
+  uint32_t ucap;  // candidate entries staged in LDS (0: U stays in global memory)
+  uint32_t rcap;  // draw words precomputed in LDS per insertion
   uint64_t j0;
 };
 

@@ -18,9 +18,12 @@ struct int2 { int x, y; };
 
 inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
 inline int __shfl(int v, int, int) { return v; }
+inline int __builtin_amdgcn_readlane(int v, int) { return v; }
+inline int atomicSub(int* p, int v) { int o = *p; *p -= v; return o; }
 inline int __shfl_xor(int v, int, int) { return v; }
 inline int __ffsll(unsigned long long m) { return __builtin_ffsll((long long)m); }
 inline int __popcll(unsigned long long m) { return __builtin_popcountll(m); }
+inline int __clzll(long long m) { return m ? __builtin_clzll((unsigned long long)m) : 64; }
 inline uint64_t __umul64hi(uint64_t a, uint64_t b) {
   return (uint64_t)(((unsigned __int128)a * b) >> 64);
 }

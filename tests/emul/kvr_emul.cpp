@@ -11,7 +11,7 @@ using namespace kvr;
 
 extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens, const uint64_t* offsets,
                         const int64_t* arrival, const uint16_t* out_len, int32_t* route, int32_t* hits,
-                        int32_t* all_hits, kvr_worker_stats* out, char* ws_out) {
+                        int32_t* all_hits, kvr_worker_stats* out, char* ws_out, uint32_t ucap_in) {
   Layout L = make_layout(*cfg);
   std::vector<uint64_t> mem(ws_out ? 0 : (L.total + 7) / 8);
   char* ws = ws_out ? ws_out : reinterpret_cast<char*>(mem.data());
@@ -30,6 +30,15 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   C.update = cfg->update;
   C.evict = cfg->evict;
   const uint32_t W = L.W;
+  // candidate list staging buffer (LDS on the device)
+  const uint32_t ucap = ucap_in;
+  std::vector<int32_t> ubuf(4 * (size_t)(ucap ? ucap : 1));
+  UStage ustage;
+  ustage.node = ubuf.data();
+  ustage.len = ubuf.data() + ucap;
+  ustage.top = ubuf.data() + 2 * ucap;
+  ustage.par = ubuf.data() + 3 * ucap;
+  ustage.cap = ucap;
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
   for (uint32_t r = 0; r < L.R; ++r) {
@@ -65,7 +74,9 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.worker = best;
         ia.replica = r;
         ia.B = L.B;
-        err = rlt_insert(P, ia, qs, Lq, h[best], nullptr);
+        ia.rn = 0;
+        ia.rw = nullptr;
+        err = rlt_insert(P, ia, qs, Lq, h[best], ustage, nullptr);
       }
       if (err) return (int)err;
     }

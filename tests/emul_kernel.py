@@ -39,11 +39,11 @@ def lib():
     if _lib is None:
         _lib = ctypes.CDLL(build())
         _lib.emul_run.restype = ctypes.c_int
-        _lib.emul_run.argtypes = [ctypes.POINTER(K.KvrConfig), ctypes.c_uint64] + [ctypes.c_void_p] * 9
+        _lib.emul_run.argtypes = [ctypes.POINTER(K.KvrConfig), ctypes.c_uint64] + [ctypes.c_void_p] * 9 + [ctypes.c_uint32]
     return _lib
 
 
-def run(stream, R, W, B, all_hits=True, ws=None, **cfg):
+def run(stream, R, W, B, all_hits=True, ws=None, ucap=8192, **cfg):
     c = K.kvr_config_default(R, W, B, max(1, stream.max_len), **cfg)
     n = stream.n
     tok = np.ascontiguousarray(stream.tokens, np.int32)
@@ -56,7 +56,7 @@ def run(stream, R, W, B, all_hits=True, ws=None, **cfg):
     st = (K.KvrWorkerStats * (R * W))()
     rc = lib().emul_run(ctypes.byref(c), n, tok.ctypes.data, off.ctypes.data, arr.ctypes.data, ol.ctypes.data,
                         route.ctypes.data, hits.ctypes.data, ah.ctypes.data if ah is not None else None, st,
-                        ws.ctypes.data if ws is not None else None)
+                        ws.ctypes.data if ws is not None else None, ucap)
     flat = K._stats_dicts(st, R * W)
     return {"rc": rc, "route": route, "hits": hits, "all_hits": ah,
             "workers": [flat[r * W:(r + 1) * W] for r in range(R)]}

@@ -10,8 +10,8 @@ from oracle import oracle as O
 from workload import PRESETS, generate, small_spec
 
 
-def _compare(s, R, W, B, update="nlms", seed=0, **cfg):
-    e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, **cfg)
+def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, **cfg):
+    e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, ucap=ucap, **cfg)
     assert e["rc"] == 0
     for r in range(R):
         o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed)
@@ -61,3 +61,17 @@ def test_tiny_caches_from_the_exact_enumeration_cases():
         s = generate({"kind": "paths", "paths": [list(q) for q in queries],
                       "order": list(range(len(queries)))})
         _compare(s, 64, 1, B)
+
+
+@pytest.mark.parametrize("ucap", [0, 3, 8])
+def test_candidate_staging_capacity(ucap):
+    """U staged in LDS, in global memory, or switching between the two as it
+    grows past the staging capacity: the same run every time."""
+    rng = np.random.default_rng(900 + ucap)
+    for case in range(25):
+        sp = small_spec(n=int(rng.integers(40, 160)), groups=int(rng.integers(2, 9)),
+                        prefix_len=(1, 25), suffix_len=(1, 15), vocab=int(rng.integers(2, 9)), seed=case)
+        s = generate(sp)
+        W = int(rng.integers(1, 4))
+        B = int(max(s.max_len, rng.integers(10, 120)))
+        _compare(s, 2, W, B, ucap=ucap, seed=case)
