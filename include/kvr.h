@@ -83,7 +83,7 @@ typedef struct kvr_config {
   uint32_t num_replicas;     /* R >= 1                                             */
   uint32_t num_workers;      /* W = M of Sec. 3.1, 1..64                           */
   uint32_t cache_tokens;     /* B_i (same for all workers), >= 1                   */
-  uint32_t max_query_tokens; /* bound on |q_j|, 1..cache_tokens (|q_j| <= B_i)      */
+  uint32_t max_query_tokens; /* bound on |q_j|: 1..min(cache_tokens, 16384)        */
   uint64_t seed;             /* Philox key word 0; key word 1 = replica index      */
   int32_t evict;             /* KVR_EVICT_*                                        */
   int32_t router;            /* KVR_ROUTE_*                                        */
@@ -91,7 +91,7 @@ typedef struct kvr_config {
   uint32_t pending_capacity; /* completion ring per (replica, worker), >= 1        */
   uint32_t node_capacity;    /* nodes per (replica, worker); 0 = cache_tokens + 3  */
   uint32_t arena_words;      /* words per semispace per (replica, worker), 0 = default
-                                2*B + 2*max_query_tokens + 4096; else >= B + 2*max_q + 64 */
+                                4*B + 2*max_query_tokens + 4096; else >= B + 2*max_q + 64 */
   double alpha_cached;       /* s per 1k cached tokens (App. A: 0)                 */
   double alpha_miss;         /* s per 1k missed tokens (App. A: 1)                 */
   double rho;                /* load decay factor (App. A: 31/32), in (0, 1]       */

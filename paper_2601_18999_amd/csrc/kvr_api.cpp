@@ -61,8 +61,8 @@ kvr_status validate(const kvr_config* c) {
     return fail(KVR_EINVAL, "cache_tokens must be in 1..2^30");
   if (c->max_query_tokens < 1 || c->max_query_tokens > c->cache_tokens)
     return fail(KVR_EINVAL, "max_query_tokens must be in 1..cache_tokens");
-  if (c->max_query_tokens > 32768)
-    return fail(KVR_EINVAL, "max_query_tokens above 32768 does not fit the LDS staging buffer");
+  if (c->max_query_tokens > 16384)
+    return fail(KVR_EINVAL, "max_query_tokens above 16384 does not fit the LDS query buffers");
   if (c->evict == KVR_EVICT_LRU)
     return fail(KVR_EINVAL, "L-LRU eviction is not built on the device (RLT only)");
   if (c->evict != KVR_EVICT_RLT) return fail(KVR_EINVAL, "unknown evict policy");
@@ -76,7 +76,7 @@ kvr_status validate(const kvr_config* c) {
   const uint64_t min_arena = (uint64_t)c->cache_tokens + 2ull * c->max_query_tokens + 64ull;
   if (c->arena_words != 0 && c->arena_words < min_arena)
     return fail(KVR_EINVAL, "arena_words must be 0 or >= cache_tokens + 2*max_query_tokens + 64");
-  const uint64_t dflt_arena = 2ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
+  const uint64_t dflt_arena = 4ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
   if (c->arena_words == 0 && dflt_arena >= (1ull << 32))
     return fail(KVR_EINVAL, "cache too large for 32-bit arena offsets");
   if (!finite(c->alpha_cached) || !finite(c->alpha_miss))

@@ -331,42 +331,93 @@ __device__ int32_t leaf_rank(const Ptrs& P, const St& s, const int32_t* ar, int3
 
 // ---------------------------------------------------------------- allocation
 
-// Copying collector: move every live edge and child array of the active
-// semispace to the other one, compacted, and switch semispaces.  False (and
-// nothing switched) when the live data does not fit a semispace.
-__device__ bool collect(const Ptrs& P, St& s) {
-  uint64_t need = 0;
-  for (uint32_t x = 0; x < s.hwm; ++x) {
-    NodeRec nd = P.nodes[x];
-    if (nd.parent == -2) continue;
-    need += (uint64_t)nd.len;
-    if (nd.ccap > 0) need = ((need + 1u) & ~1ull) + 2ull * (uint64_t)nd.ccap;
+// Wave-cooperative copy of n words (eight loads in flight per lane).
+__device__ __forceinline__ void wave_copy(int32_t* dst, const int32_t* src, int32_t n) {
+  constexpr int kU = 8;
+  for (int32_t b = 0; b < n; b += kU * KVR_WAVE) {
+    int32_t v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int32_t k = b + u * KVR_WAVE + lane_id();
+      v[u] = k < n ? src[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int32_t k = b + u * KVR_WAVE + lane_id();
+      if (k < n) dst[k] = v[u];
+    }
   }
-  if (need > P.A) return false;
+}
+
+// Inclusive prefix sum over the wave's lanes.
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t v) {
+  for (int o = 1; o < KVR_WAVE; o <<= 1) {
+    const uint32_t w = (uint32_t)__shfl_up((int)v, o, KVR_WAVE);
+    if (lane_id() >= o) v += w;
+  }
+  return v;
+}
+
+// Copying collector: move every live edge and child array of the active
+// semispace to the other one, compacted, and switch semispaces.  Node slots
+// are taken 64 at a time: one lane reads each node, a prefix sum gives the
+// new offsets (edge padded to an even length, then the child array), and
+// the wave copies the blocks.  False (and nothing switched) when the live
+// data does not fit a semispace.
+__device__ bool collect(const Ptrs& P, St& s) {
   const int32_t* src = arena_of(P, s.arena_sel);
   int32_t* dst = arena_of(P, s.arena_sel ^ 1u);
-  uint32_t top = 0;
-  for (uint32_t x = 0; x < s.hwm; ++x) {
-    NodeRec nd = P.nodes[x];
-    if (nd.parent == -2) continue;
-    uint32_t noff = top;
-    for (int32_t k = lane_id(); k < nd.len; k += KVR_WAVE) dst[noff + k] = src[nd.off + k];
-    top += (uint32_t)nd.len;
-    uint32_t ncoff = 0;
-    if (nd.ccap > 0) {
-      top = (top + 1u) & ~1u;
-      ncoff = top;
-      for (int32_t k = lane_id(); k < 2 * nd.nchild; k += KVR_WAVE) dst[ncoff + k] = src[nd.coff + k];
-      top += 2u * (uint32_t)nd.ccap;
+  uint64_t top = 0;
+  // sizes first: the live data must fit
+  for (uint32_t b = 0; b < s.hwm; b += KVR_WAVE) {
+    const uint32_t x = b + (uint32_t)lane_id();
+    uint32_t sz = 0;
+    if (x < s.hwm) {
+      const NodeRec nd = P.nodes[x];
+      if (nd.parent != -2) sz = (((uint32_t)nd.len + 1u) & ~1u) + 2u * (uint32_t)nd.ccap;
     }
-    if (lane_id() == 0) {
+    top += (uint32_t)__builtin_amdgcn_readlane((int)wave_inclusive_sum(sz), KVR_WAVE - 1);
+  }
+  if (top > P.A) return false;
+  top = 0;
+  for (uint32_t b = 0; b < s.hwm; b += KVR_WAVE) {
+    const uint32_t x = b + (uint32_t)lane_id();
+    NodeRec nd;
+    nd.parent = -2;
+    nd.len = 0;
+    nd.ccap = 0;
+    nd.nchild = 0;
+    nd.off = 0;
+    nd.coff = 0;
+    if (x < s.hwm) nd = P.nodes[x];
+    const bool live = x < s.hwm && nd.parent != -2;
+    const uint32_t elen = live ? (((uint32_t)nd.len + 1u) & ~1u) : 0u;
+    const uint32_t sz = live ? elen + 2u * (uint32_t)nd.ccap : 0u;
+    const uint32_t incl = wave_inclusive_sum(sz);
+    const uint32_t noff = (uint32_t)top + incl - sz;
+    const uint32_t ncoff = noff + elen;
+    uint64_t todo = __ballot(live);
+    while (todo) {
+      const int j = first_lane(todo);
+      todo &= todo - 1;
+      const uint32_t so = (uint32_t)__builtin_amdgcn_readlane((int)nd.off, j);
+      const int32_t sl = __builtin_amdgcn_readlane(nd.len, j);
+      const uint32_t sc = (uint32_t)__builtin_amdgcn_readlane((int)nd.coff, j);
+      const int32_t snc = __builtin_amdgcn_readlane(nd.nchild, j);
+      const uint32_t dO = (uint32_t)__builtin_amdgcn_readlane((int)noff, j);
+      const uint32_t dC = (uint32_t)__builtin_amdgcn_readlane((int)ncoff, j);
+      wave_copy(dst + dO, src + so, sl);
+      if (snc > 0) wave_copy(dst + dC, src + sc, 2 * snc);
+    }
+    if (live) {
       P.nodes[x].off = noff;
-      P.nodes[x].coff = ncoff;
+      P.nodes[x].coff = nd.ccap > 0 ? ncoff : 0u;
     }
+    top += (uint32_t)__builtin_amdgcn_readlane((int)incl, KVR_WAVE - 1);
   }
   wave_mem_sync();
   s.arena_sel ^= 1u;
-  s.arena_top = top;
+  s.arena_top = (uint32_t)top;
   s.gc_runs += 1;
   return true;
 }

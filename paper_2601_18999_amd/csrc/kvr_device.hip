@@ -42,13 +42,29 @@ namespace kvr {
 
 // ---------------------------------------------------------------- kernels
 
-__global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
-  // dynamic LDS: the current query (max_query_tokens entries), then the
-  // staged candidate list (ucap entries of node, length, mark_top, parent)
+// Match q[0, L) on worker i, record h in hslot, count the matched tokens.
+__device__ __forceinline__ void match_worker(const StepArgs& a, uint32_t r, uint32_t i, const int32_t* q,
+                                             int32_t L, int32_t* hslot) {
+  Ptrs P = worker_ptrs(a.ws, a.L, r, i);
+  const uint32_t sel = P.hdr->arena_sel;
+  const int32_t h = match_lcp(P, sel, q, L);
+  if (lane_id() == 0) {
+    *hslot = h;
+    P.hdr->matched_tokens += (uint64_t)h;
+  }
+}
+
+// One workgroup per replica walks the batch in order.  The tree of a worker
+// changes only when a query is routed to it, so while wave 0 inserts query k
+// into the routed worker, the other waves already match query k+1 against
+// every other worker; only the routed worker is matched again afterwards.
+__global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
+  // dynamic LDS: two query buffers (max_query_tokens entries each; the next
+  // query is staged and matched while the current one is inserted), the
+  // precomputed draw words, then the staged candidate list
   extern __shared__ int32_t smem[];
-  int32_t* qs = smem;
-  // draw words precomputed by every wave before the insertion (8-byte aligned)
-  uint64_t* rw = reinterpret_cast<uint64_t*>(smem + ((a.L.maxL + 3u) & ~3u));
+  const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
+  uint64_t* rw = reinterpret_cast<uint64_t*>(smem + 2 * qstride);
   UStage ustage;
   {
     int32_t* ub = reinterpret_cast<int32_t*>(rw + a.rcap);
@@ -58,7 +74,7 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
     ustage.par = ub + 3 * a.ucap;
     ustage.cap = a.ucap;
   }
-  __shared__ int32_t h_sh[kMaxWorkers];
+  __shared__ int32_t h_sh[2][kMaxWorkers];  // h of the current and of the next query
   __shared__ double eh_sh[kMaxWorkers];
   __shared__ double ch_sh[kMaxWorkers];
   __shared__ int32_t best_sh;
@@ -77,26 +93,46 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
   __syncthreads();
   if (abort_sh) return;
 
+  // query 0: stage it and match it on every worker
+  {
+    const uint64_t o0 = a.offsets[0];
+    const int32_t L0 = (int32_t)(a.offsets[1] - o0);
+    for (int32_t x = (int32_t)threadIdx.x; x < L0; x += (int32_t)blockDim.x) smem[x] = a.tokens[o0 + x];
+    __syncthreads();
+    for (uint32_t i = wave; i < W; i += nwaves) match_worker(a, r, i, smem, L0, &h_sh[0][i]);
+  }
+  int32_t stale = -1;  // worker whose h for the current query is not known yet
   for (uint32_t k = 0; k < a.n; ++k) {
     const uint64_t o0 = a.offsets[k];
     const int32_t Lq = (int32_t)(a.offsets[k + 1] - o0);
     const int64_t t = a.arrival[k];
     const int32_t olen = a.out_len ? (int32_t)a.out_len[k] : 4;
-    for (int32_t x = (int32_t)threadIdx.x; x < Lq; x += (int32_t)blockDim.x) qs[x] = a.tokens[o0 + x];
+    const uint32_t cur = k & 1u;
+    int32_t* qs = smem + cur * qstride;
+    int32_t* qn = smem + (cur ^ 1u) * qstride;
+    const bool has_next = k + 1 < a.n;
+    int32_t Ln = 0;
+    uint64_t n0 = 0;
+    if (has_next) {
+      n0 = a.offsets[k + 1];
+      Ln = (int32_t)(a.offsets[k + 2] - n0);
+    }
     __syncthreads();
 
-    // completions and decay (one lane per worker), then the match (one wave per worker)
+    // completions and decay (wave 0, one lane per worker); the last wave
+    // matches the current query on the worker routed last time; the others
+    // stage the next query
     if (wave == 0 && (uint32_t)lane < W) {
       const int64_t tprev = rh->tprev;
       complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), t, tprev);
     }
-    for (uint32_t i = wave; i < W; i += nwaves) {
-      Ptrs P = worker_ptrs(a.ws, a.L, r, i);
-      const uint32_t sel = P.hdr->arena_sel;
-      int32_t h = match_lcp(P, sel, qs, Lq);
-      if (lane == 0) {
-        h_sh[i] = h;
-        P.hdr->matched_tokens += (uint64_t)h;
+    const uint32_t mwave = nwaves - 1;
+    if (stale >= 0 && wave == mwave) match_worker(a, r, (uint32_t)stale, qs, Lq, &h_sh[cur][stale]);
+    if (has_next) {
+      if (nwaves == 1) {
+        for (int32_t x = (int32_t)threadIdx.x; x < Ln; x += (int32_t)blockDim.x) qn[x] = a.tokens[n0 + x];
+      } else if (wave != mwave) {
+        for (int32_t x = (int32_t)threadIdx.x; x < Ln; x += (int32_t)(blockDim.x - KVR_WAVE)) qn[x] = a.tokens[n0 + x];
       }
     }
     __syncthreads();
@@ -104,7 +140,7 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
     if (wave == 0) {
       if ((uint32_t)lane < W) {
         double ch;
-        eh_sh[lane] = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[lane], Lq, &ch);
+        eh_sh[lane] = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[cur][lane], Lq, &ch);
         ch_sh[lane] = ch;
       }
       __builtin_amdgcn_wave_barrier();
@@ -118,18 +154,13 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
       __builtin_amdgcn_wave_barrier();
       const uint32_t best = (uint32_t)best_sh;
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
-      const int32_t hb = h_sh[best];
+      const int32_t hb = h_sh[cur][best];
       uint32_t err = 0;
       if (lane == 0) {
         err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
         if (a.hits) a.hits[orow] = hb;
-      }
-      if (a.all_hits && (uint32_t)lane < W)
-        a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[lane];
-      err = (uint32_t)__shfl((int)err, 0, KVR_WAVE);
-      if (lane == 0) {
         // draws this insertion will take: one per token loaded into a full cache
         const uint32_t size = P.hdr->size;
         const uint32_t nload = (uint32_t)(Lq - hb);
@@ -140,6 +171,8 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
           abort_sh = 1;
         }
       }
+      if (a.all_hits && (uint32_t)lane < W)
+        a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[cur][lane];
     }
     __syncthreads();
     if (abort_sh) break;
@@ -149,21 +182,21 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
     for (uint32_t d = threadIdx.x; d < rn; d += blockDim.x)
       rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
     if (rn) __syncthreads();
+
     if (wave == 0) {
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
-      uint32_t err = 0;
-      {
-        InsertArgs ia;
-        ia.seed = a.C.seed;
-        ia.jg = a.j0 + k;
-        ia.worker = best;
-        ia.replica = r;
-        ia.B = a.L.B;
-        ia.rn = rn;
-        ia.rw = rw;
-        int64_t dbg[4] = {0, 0, 0, 0};
-        err = rlt_insert(P, ia, qs, Lq, h_sh[best], ustage, dbg);
-        if (lane == 0 && err && atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
+      InsertArgs ia;
+      ia.seed = a.C.seed;
+      ia.jg = a.j0 + k;
+      ia.worker = best;
+      ia.replica = r;
+      ia.B = a.L.B;
+      ia.rn = rn;
+      ia.rw = rw;
+      int64_t dbg[4] = {0, 0, 0, 0};
+      const uint32_t err = rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, dbg);
+      if (lane == 0 && err) {
+        if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];
           g->err_replica = r;
           g->err_query = a.j0 + k;
@@ -171,11 +204,18 @@ __global__ void __launch_bounds__(1024) step_kernel(StepArgs a) {
           g->err_val[1] = dbg[2];
           g->err_val[2] = dbg[3];
         }
-      }
-      if (lane == 0 && err) {
         atomicOr(&g->status, err);
         abort_sh = 1;
       }
+    } else if (has_next) {
+      // run-ahead: the next query on every worker but the routed one
+      for (uint32_t i = wave - 1; i < W; i += nwaves - 1)
+        if (i != best) match_worker(a, r, i, qn, Ln, &h_sh[cur ^ 1u][i]);
+    }
+    stale = (int32_t)best;
+    if (nwaves == 1 && has_next) {
+      for (uint32_t i = 0; i < W; ++i)
+        if (i != best) match_worker(a, r, i, qn, Ln, &h_sh[cur ^ 1u][i]);
     }
     __syncthreads();
     if (abort_sh) break;
@@ -239,7 +279,7 @@ __global__ void stats_kernel(char* ws, Layout L) {
 // ---------------------------------------------------------------- launchers (host)
 
 size_t step_lds_bytes(uint32_t maxL, uint32_t ucap, uint32_t rcap) {
-  return (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint64_t) +
+  return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint64_t) +
          (size_t)ucap * 4u * sizeof(int32_t);
 }
 

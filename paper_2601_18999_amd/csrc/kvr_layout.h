@@ -30,7 +30,7 @@ namespace kvr {
 constexpr uint32_t kMaxWorkers = 64;
 constexpr uint32_t kWave = 64;
 #ifndef KVR_MAX_WAVES
-#define KVR_MAX_WAVES 16
+#define KVR_MAX_WAVES 8
 #endif
 constexpr uint32_t kMaxWavesPerBlock = KVR_MAX_WAVES;
 
@@ -150,7 +150,7 @@ inline Layout make_layout(const kvr_config& c) {
   // every non-root node holds >= 1 token, and an insertion adds at most a split
   // head and the new leaf before its evictions free space: B + 3 always fits
   L.NC = c.node_capacity ? c.node_capacity : c.cache_tokens + 3u;
-  uint64_t dflt_arena = 2ull * c.cache_tokens + 2ull * c.max_query_tokens + 4096ull;
+  uint64_t dflt_arena = 4ull * c.cache_tokens + 2ull * c.max_query_tokens + 4096ull;
   L.A = c.arena_words ? c.arena_words : (uint32_t)dflt_arena;
   L.A &= ~1u;  // even, so child arrays stay 8-byte aligned in both semispaces
   L.PC = c.pending_capacity;

@@ -21,6 +21,7 @@ inline int __shfl(int v, int, int) { return v; }
 inline int __builtin_amdgcn_readlane(int v, int) { return v; }
 inline int atomicSub(int* p, int v) { int o = *p; *p -= v; return o; }
 inline int __shfl_xor(int v, int, int) { return v; }
+inline int __shfl_up(int v, int, int) { return v; }
 inline int __ffsll(unsigned long long m) { return __builtin_ffsll((long long)m); }
 inline int __popcll(unsigned long long m) { return __builtin_popcountll(m); }
 inline int __clzll(long long m) { return m ? __builtin_clzll((unsigned long long)m) : 64; }
