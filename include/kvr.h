@@ -88,7 +88,7 @@ typedef struct kvr_config {
   int32_t evict;             /* KVR_EVICT_*                                        */
   int32_t router;            /* KVR_ROUTE_*                                        */
   int32_t update;            /* KVR_UPD_*                                          */
-  uint32_t pending_capacity; /* completion ring per (replica, worker), >= 1        */
+  uint32_t pending_capacity; /* completion ring per (replica, worker), >= 1; 65536 by default */
   uint32_t node_capacity;    /* nodes per (replica, worker); 0 = cache_tokens + 3  */
   uint32_t arena_words;      /* words per semispace per (replica, worker), 0 = default
                                 4*B + 2*max_query_tokens + 4096; else >= B + 2*max_q + 64 */

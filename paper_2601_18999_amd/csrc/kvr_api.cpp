@@ -130,7 +130,7 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->evict = KVR_EVICT_RLT;
   c->router = KVR_ROUTE_LBGR;
   c->update = KVR_UPD_NLMS;
-  c->pending_capacity = 4096;
+  c->pending_capacity = 65536;
   c->node_capacity = 0;
   c->arena_words = 0;
   c->alpha_cached = 0.0;  // App. A: 0 ms per 1k cached tokens
