@@ -17,6 +17,7 @@
 """
 from fractions import Fraction
 import math
+import os
 
 import numpy as np
 import pytest
@@ -35,11 +36,21 @@ def _paths_stream(paths, order, gap_us=83333, out_len=4):
 # ---------------------------------------------------------------------------
 # RNG
 
-def test_philox_known_answer_vector():
-    # Random123 known-answer vector for philox4x64-10, counter 0, key 0
-    out = O.philox4x64_10([0, 0, 0, 0], [0, 0])
-    assert [int(x) for x in out] == [0x16554D9ECA36314C, 0xDB20FE9D672D0FDC,
-                                      0xD7E772CEE186176B, 0x7E68B68AEC7BA23B]
+def _kat_vectors():
+    path = os.path.join(os.path.dirname(__file__), "golden", "philox4x64_10_kat.txt")
+    with open(path) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                w = [int(x, 16) for x in line.split()]
+                yield w[0:4], w[4:6], w[6:10]
+
+
+def test_philox_known_answer_vectors():
+    vecs = list(_kat_vectors())
+    assert len(vecs) == 2
+    for ctr, key, want in vecs:
+        assert [int(x) for x in O.philox4x64_10(ctr, key)] == want
+        assert SM.philox_word0(key[0], key[1], tuple(ctr)) == want[0]
 
 
 def test_philox_matches_numpy():
