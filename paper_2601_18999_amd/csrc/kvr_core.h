@@ -235,38 +235,66 @@ __device__ __forceinline__ int32_t mark_top(const St& s, const NodeRec& nd, int3
 // ---------------------------------------------------------------- array tools (wave)
 
 __device__ int32_t arr_find(const int32_t* a, uint32_t n, int32_t v) {
-  for (uint32_t b = 0; b < n; b += KVR_WAVE) {
-    uint32_t k = b + (uint32_t)lane_id();
-    bool hit = (k < n) && (a[k] == v);
-    uint64_t m = __ballot(hit);
-    if (m) return (int32_t)(b + (uint32_t)first_lane(m));
+  constexpr int kUnroll = 8;  // eight chunks per round trip
+  for (uint32_t b = 0; b < n; b += kUnroll * KVR_WAVE) {
+    int32_t x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t k = b + (uint32_t)(u * KVR_WAVE) + (uint32_t)lane_id();
+      x[u] = k < n ? a[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t k = b + (uint32_t)(u * KVR_WAVE) + (uint32_t)lane_id();
+      const uint64_t m = __ballot(k < n && x[u] == v);
+      if (m) return (int32_t)(b + (uint32_t)(u * KVR_WAVE) + (uint32_t)first_lane(m));
+    }
   }
   return -1;
 }
 
-// a[pos+1 .. n+1) = a[pos .. n); a[pos] = v
+// a[pos+1 .. n+1) = a[pos .. n); a[pos] = v.  Top-down rounds of eight
+// chunks: every load of a round completes before its stores are issued.
 __device__ void arr_insert(int32_t* a, uint32_t n, uint32_t pos, int32_t v) {
-  for (int64_t hi = (int64_t)n; hi > (int64_t)pos; hi -= KVR_WAVE) {
-    int64_t lo = hi - KVR_WAVE > (int64_t)pos ? hi - KVR_WAVE : (int64_t)pos;
-    int64_t k = lo + lane_id();
-    int32_t x = 0;
-    if (k < hi) x = a[k];
-    __builtin_amdgcn_wave_barrier();
-    if (k < hi) a[k + 1] = x;
+  constexpr int kUnroll = 8;
+  constexpr int64_t kSpan = (int64_t)kUnroll * KVR_WAVE;
+  for (int64_t hi = (int64_t)n; hi > (int64_t)pos; hi -= kSpan) {
+    const int64_t lo = hi - kSpan > (int64_t)pos ? hi - kSpan : (int64_t)pos;
+    int32_t x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t k = lo + u * KVR_WAVE + lane_id();
+      x[u] = k < hi ? a[k] : 0;
+    }
+    wave_mem_sync();
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t k = lo + u * KVR_WAVE + lane_id();
+      if (k < hi) a[k + 1] = x[u];
+    }
     wave_mem_sync();
   }
   if (lane_id() == 0) a[pos] = v;
   wave_mem_sync();
 }
 
-// a[pos .. n-1) = a[pos+1 .. n)
+// a[pos .. n-1) = a[pos+1 .. n), bottom-up rounds of eight chunks
 __device__ void arr_erase(int32_t* a, uint32_t n, uint32_t pos) {
-  for (uint32_t lo = pos; lo + 1 < n; lo += KVR_WAVE) {
-    uint32_t k = lo + (uint32_t)lane_id();
-    int32_t x = 0;
-    if (k + 1 < n) x = a[k + 1];
-    __builtin_amdgcn_wave_barrier();
-    if (k + 1 < n) a[k] = x;
+  constexpr int kUnroll = 8;
+  constexpr uint32_t kSpan = (uint32_t)kUnroll * KVR_WAVE;
+  for (uint32_t lo = pos; lo + 1 < n; lo += kSpan) {
+    int32_t x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t k = lo + (uint32_t)(u * KVR_WAVE) + (uint32_t)lane_id();
+      x[u] = k + 1 < n ? a[k + 1] : 0;
+    }
+    wave_mem_sync();
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t k = lo + (uint32_t)(u * KVR_WAVE) + (uint32_t)lane_id();
+      if (k + 1 < n) a[k] = x[u];
+    }
     wave_mem_sync();
   }
 }
@@ -321,7 +349,7 @@ __device__ int32_t extreme_leaf(const Ptrs& P, const int32_t* ar, int32_t x, boo
 
 // Index of the first (after=false) or one past the last (after=true) leaf of
 // the subtree of x in the leaf list, or -1.
-__device__ int32_t leaf_rank(const Ptrs& P, const St& s, const int32_t* ar, int32_t x, bool after) {
+__device__ __forceinline__ int32_t leaf_rank(const Ptrs& P, const St& s, const int32_t* ar, int32_t x, bool after) {
   int32_t lf = extreme_leaf(P, ar, x, after, s.hwm);
   if (lf < 0) return -1;
   int32_t pos = arr_find(P.leaf, s.nleaves, lf);
@@ -364,23 +392,25 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t v) {
 // new offsets (edge padded to an even length, then the child array), and
 // the wave copies the blocks.  False (and nothing switched) when the live
 // data does not fit a semispace.
-__device__ bool collect(const Ptrs& P, St& s) {
-  const int32_t* src = arena_of(P, s.arena_sel);
-  int32_t* dst = arena_of(P, s.arena_sel ^ 1u);
+// Out of line (it runs rarely) and with scalar arguments only, so the
+// caller's cache state never has to live in memory.  Returns the new arena
+// top, or ~0 when the live data does not fit.
+__device__ __noinline__ uint64_t collect_arena(NodeRec* nodes, const int32_t* src, int32_t* dst, uint32_t hwm,
+                                               uint32_t A) {
   uint64_t top = 0;
   // sizes first: the live data must fit
-  for (uint32_t b = 0; b < s.hwm; b += KVR_WAVE) {
+  for (uint32_t b = 0; b < hwm; b += KVR_WAVE) {
     const uint32_t x = b + (uint32_t)lane_id();
     uint32_t sz = 0;
-    if (x < s.hwm) {
-      const NodeRec nd = P.nodes[x];
+    if (x < hwm) {
+      const NodeRec nd = nodes[x];
       if (nd.parent != -2) sz = (((uint32_t)nd.len + 1u) & ~1u) + 2u * (uint32_t)nd.ccap;
     }
     top += (uint32_t)__builtin_amdgcn_readlane((int)wave_inclusive_sum(sz), KVR_WAVE - 1);
   }
-  if (top > P.A) return false;
+  if (top > A) return ~0ull;
   top = 0;
-  for (uint32_t b = 0; b < s.hwm; b += KVR_WAVE) {
+  for (uint32_t b = 0; b < hwm; b += KVR_WAVE) {
     const uint32_t x = b + (uint32_t)lane_id();
     NodeRec nd;
     nd.parent = -2;
@@ -389,8 +419,8 @@ __device__ bool collect(const Ptrs& P, St& s) {
     nd.nchild = 0;
     nd.off = 0;
     nd.coff = 0;
-    if (x < s.hwm) nd = P.nodes[x];
-    const bool live = x < s.hwm && nd.parent != -2;
+    if (x < hwm) nd = nodes[x];
+    const bool live = x < hwm && nd.parent != -2;
     const uint32_t elen = live ? (((uint32_t)nd.len + 1u) & ~1u) : 0u;
     const uint32_t sz = live ? elen + 2u * (uint32_t)nd.ccap : 0u;
     const uint32_t incl = wave_inclusive_sum(sz);
@@ -410,19 +440,25 @@ __device__ bool collect(const Ptrs& P, St& s) {
       if (snc > 0) wave_copy(dst + dC, src + sc, 2 * snc);
     }
     if (live) {
-      P.nodes[x].off = noff;
-      P.nodes[x].coff = nd.ccap > 0 ? ncoff : 0u;
+      nodes[x].off = noff;
+      nodes[x].coff = nd.ccap > 0 ? ncoff : 0u;
     }
     top += (uint32_t)__builtin_amdgcn_readlane((int)incl, KVR_WAVE - 1);
   }
   wave_mem_sync();
+  return top;
+}
+
+__device__ __forceinline__ bool collect(const Ptrs& P, St& s) {
+  const uint64_t top = collect_arena(P.nodes, arena_of(P, s.arena_sel), arena_of(P, s.arena_sel ^ 1u), s.hwm, P.A);
+  if (top == ~0ull) return false;
   s.arena_sel ^= 1u;
   s.arena_top = (uint32_t)top;
   s.gc_runs += 1;
   return true;
 }
 
-__device__ bool arena_alloc(const Ptrs& P, St& s, uint32_t words, bool even, uint32_t& off) {
+__device__ __forceinline__ bool arena_alloc(const Ptrs& P, St& s, uint32_t words, bool even, uint32_t& off) {
   uint64_t top = s.arena_top;
   if (even) top = (top + 1u) & ~1ull;
   if (top + words > P.A) {
@@ -442,7 +478,7 @@ __device__ bool arena_alloc(const Ptrs& P, St& s, uint32_t words, bool even, uin
   return true;
 }
 
-__device__ int32_t node_alloc(const Ptrs& P, St& s) {
+__device__ __forceinline__ int32_t node_alloc(const Ptrs& P, St& s) {
   int32_t id;
   if (s.free_head >= 0) {
     id = s.free_head;
@@ -458,7 +494,7 @@ __device__ int32_t node_alloc(const Ptrs& P, St& s) {
   return id;
 }
 
-__device__ void node_free(const Ptrs& P, St& s, int32_t id) {
+__device__ __forceinline__ void node_free(const Ptrs& P, St& s, int32_t id) {
   if (lane_id() == 0) {
     P.nodes[id].parent = -2;
     P.nodes[id].off = (uint32_t)s.free_head;
@@ -468,7 +504,7 @@ __device__ void node_free(const Ptrs& P, St& s, int32_t id) {
   s.nnodes -= 1;
 }
 
-__device__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c) {
+__device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c) {
   NodeRec na = P.nodes[a];
   if (na.nchild == na.ccap) {
     int32_t ncap = na.ccap ? 2 * na.ccap : 2;
@@ -503,7 +539,7 @@ __device__ int32_t child_slot(const int32_t* ar, const NodeRec& na, int32_t c) {
   return -1;
 }
 
-__device__ bool child_remove(const Ptrs& P, const St& s, int32_t a, int32_t c) {
+__device__ __forceinline__ bool child_remove(const Ptrs& P, const St& s, int32_t a, int32_t c) {
   NodeRec na = P.nodes[a];
   int32_t* ar = arena_of(P, s.arena_sel);
   int32_t pos = child_slot(ar, na, c);
@@ -520,7 +556,7 @@ __device__ bool child_remove(const Ptrs& P, const St& s, int32_t a, int32_t c) {
   return true;
 }
 
-__device__ bool child_replace(const Ptrs& P, const St& s, int32_t a, int32_t oldc, int32_t newc) {
+__device__ __forceinline__ bool child_replace(const Ptrs& P, const St& s, int32_t a, int32_t oldc, int32_t newc) {
   NodeRec na = P.nodes[a];
   int32_t* ar = arena_of(P, s.arena_sel);
   int32_t pos = child_slot(ar, na, oldc);
@@ -532,7 +568,7 @@ __device__ bool child_replace(const Ptrs& P, const St& s, int32_t a, int32_t old
 
 // Split node x at edge offset k (0 < k < len): a new head node takes
 // positions [0, k) and x keeps [k, len) below it, so every leaf keeps its id.
-__device__ int32_t split_node(const Ptrs& P, St& s, int32_t x, int32_t k) {
+__device__ __forceinline__ int32_t split_node(const Ptrs& P, St& s, int32_t x, int32_t k) {
   uint32_t coff;
   if (!arena_alloc(P, s, 4u, true, coff)) return -1;
   int32_t hd = node_alloc(P, s);
@@ -591,22 +627,27 @@ __device__ int32_t split_node(const Ptrs& P, St& s, int32_t x, int32_t k) {
 
 // U := the leaves (other than `excl`) whose leaf token is unmarked, in the
 // order of the leaf list (lexicographic order of root paths).
-__device__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
+__device__ __forceinline__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
+  constexpr int kUnroll = 4;  // four chunks of the leaf list per round trip
   uint32_t n = 0;
-  for (uint32_t b = 0; b < s.nleaves; b += KVR_WAVE) {
-    uint32_t k = b + (uint32_t)lane_id();
-    bool cand = false;
-    int32_t id = -1;
-    if (k < s.nleaves) {
-      id = P.leaf[k];
-      if (id != excl) {
-        NodeRec nd = P.nodes[id];
-        cand = !is_marked(s, nd, id, nd.len - 1);
-      }
+  for (uint32_t b = 0; b < s.nleaves; b += kUnroll * KVR_WAVE) {
+    int32_t id[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      id[v] = k < s.nleaves ? P.leaf[k] : -1;
     }
-    uint64_t m = __ballot(cand);
-    if (cand) P.U[n + (uint32_t)__popcll(m & lanemask_lt())] = id;
-    n += (uint32_t)__popcll(m);
+    NodeRec nd[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v)
+      if (id[v] > 0 && id[v] != excl) nd[v] = P.nodes[id[v]];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const bool cand = id[v] > 0 && id[v] != excl && !is_marked(s, nd[v], id[v], nd[v].len - 1);
+      const uint64_t m = __ballot(cand);
+      if (cand) P.U[n + (uint32_t)__popcll(m & lanemask_lt())] = id[v];
+      n += (uint32_t)__popcll(m);
+    }
   }
   wave_mem_sync();
   s.nU = n;
@@ -616,7 +657,7 @@ __device__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
 // The candidate at U[kk], node n with parent p, has just lost its last
 // token: drop it from the tree and the leaf list; its parent, if that became
 // an unmarked leaf, takes its place (and rank) in U, else the entry goes.
-__device__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk, int32_t n, int32_t p) {
+__device__ __forceinline__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk, int32_t n, int32_t p) {
   int32_t li = arr_find(P.leaf, s.nleaves, n);
   if (li < 0) {
     KVR_FAIL_CHECK(s, 12, n, s.nleaves, kk);
@@ -659,9 +700,14 @@ struct InsertArgs {
 
 // Word 0 of Philox4x64-10 for draw d of this insertion: key (seed, replica),
 // counter (query index, worker, d, 0).
+__device__ __noinline__ uint64_t draw_word_slow(uint64_t jg, uint64_t worker, uint64_t d, uint64_t seed,
+                                                uint64_t replica) {
+  return philox_word0(jg, worker, d, 0ull, seed, replica);
+}
+
 __device__ __forceinline__ uint64_t draw_word(const InsertArgs& ia, uint64_t d) {
   if (d < ia.rn) return ia.rw[d];
-  return philox_word0(ia.jg, ia.worker, d, 0ull, ia.seed, ia.replica);
+  return draw_word_slow(ia.jg, ia.worker, d, ia.seed, ia.replica);
 }
 
 // Evict with draws dctr .. dctr+cnt-1 (cnt <= wave width), one lane per
@@ -671,7 +717,7 @@ __device__ __forceinline__ uint64_t draw_word(const InsertArgs& ia, uint64_t d) 
 // the only event that changes U.  Commits the draws up to and including the
 // first such one, applies it, and returns the number of draws consumed in
 // `done`.  Identical to taking the draws one at a time.
-__device__ bool evict_block(const Ptrs& P, St& s, const InsertArgs& ia, uint64_t dctr, uint32_t cnt,
+__device__ __forceinline__ bool evict_block(const Ptrs& P, St& s, const InsertArgs& ia, uint64_t dctr, uint32_t cnt,
                             uint32_t& done) {
   const int lane = lane_id();
   const bool act = (uint32_t)lane < cnt;
@@ -746,23 +792,34 @@ struct UStage {
 };
 
 __device__ __forceinline__ bool stage_in(const Ptrs& P, St& s, const UStage& u) {
+  constexpr int kUnroll = 4;  // four chunks of the list per round trip
   bool bad = false;
-  for (uint32_t b = 0; b < s.nU; b += KVR_WAVE) {
-    const uint32_t k = b + (uint32_t)lane_id();
-    if (k < s.nU) {
-      const int32_t n = P.U[k];
-      if (n <= 0 || (uint32_t)n >= s.hwm) {
-        bad = true;
-      } else {
-        const NodeRec nd = P.nodes[n];
-        u.node[k] = n;
-        u.len[k] = nd.len;
-        u.top[k] = mark_top(s, nd, n);
-        u.par[k] = nd.parent;
+  for (uint32_t b = 0; b < s.nU; b += kUnroll * KVR_WAVE) {
+    int32_t n[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      n[v] = k < s.nU ? P.U[k] : 0;
+    }
+    NodeRec nd[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      const bool ok = k < s.nU && n[v] > 0 && (uint32_t)n[v] < s.hwm;
+      if (k < s.nU && !ok) bad = true;
+      if (ok) nd[v] = P.nodes[n[v]];
+    }
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      if (k < s.nU && n[v] > 0 && (uint32_t)n[v] < s.hwm) {
+        u.node[k] = n[v];
+        u.len[k] = nd[v].len;
+        u.top[k] = mark_top(s, nd[v], n[v]);
+        u.par[k] = nd[v].parent;
       }
     }
   }
-  wave_mem_sync();
   if (__ballot(bad)) {
     KVR_FAIL_CHECK(s, 14, s.nU, s.hwm, 0);
     return false;
@@ -805,54 +862,67 @@ __device__ __forceinline__ void stage_erase(const UStage& u, uint32_t n, uint32_
   }
 }
 
-// evict_block with U staged in LDS (same draws, same result).  A draw whose
-// candidate has more than `cnt` evictable tokens cannot exhaust it within
-// the block, so only the lanes drawing nearly exhausted candidates need
-// their rank among equal draws; the committed trims are LDS decrements.
+// evict_block with U staged in LDS (same draws, same result).  Every draw
+// of the block first trims its candidate with an LDS atomic; the values the
+// atomics return show whether some candidate ran out of evictable tokens.
+// Only then (rarely) is the first exhausting draw in draw order found
+// exactly and the draws after it are undone.
 __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const InsertArgs& ia, const UStage& u,
-                                                   uint64_t dctr, uint32_t cnt, uint32_t& done) {
+                                                   uint64_t dctr, uint32_t cnt, uint32_t& done, bool& changed) {
+  changed = false;
   const int lane = lane_id();
   const bool act = (uint32_t)lane < cnt;
   uint32_t kk = 0;
-  int32_t n = 0, len = 0, top = 0, par = 0;
+  int32_t top = 0, old = 0;
   if (act) {
     const uint64_t r64 = draw_word(ia, dctr + (uint64_t)lane);
     kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
-    n = u.node[kk];
-    len = u.len[kk];
     top = u.top[kk];
-    par = u.par[kk];
+    old = atomicSub(&u.len[kk], 1);
   }
-  const int32_t e = len - top;
-  if (__ballot(act && (e <= 0 || par < 0))) {
-    KVR_FAIL_CHECK(s, 11, n, len, top);
+  // the decrements of one candidate return distinct values len, len-1, ...;
+  // the one returning top + 1 took its last evictable token
+  uint64_t exm = __ballot(act && old == top + 1);
+  const uint64_t over = __ballot(act && old <= top);
+  int f = (int)cnt - 1;  // last committed draw
+  if (exm) {
+    // exhausting draw of each exhausted candidate, in draw order: the
+    // e-th of the lanes drawing it, e = its evictable tokens before the block
+    uint64_t todo = exm;
+    while (todo) {
+      const int x = first_lane(todo);
+      todo &= todo - 1ull;
+      const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk, x);
+      const int32_t tv = __builtin_amdgcn_readlane(top, x);
+      uint64_t m = __ballot(act && kk == v);
+      const int e = __popcll(__ballot(act && kk == v && old > tv));
+      for (int c = 1; c < e; ++c) m &= m - 1ull;
+      const int fx = first_lane(m);
+      if (fx < f) f = fx;
+    }
+    if (act && lane > f) atomicAdd(&u.len[kk], 1);
+    // every committed draw leaves its candidate with len >= top
+    if (__ballot(act && lane <= f && u.len[kk] < top)) {
+      KVR_FAIL_CHECK(s, 11, (int32_t)cnt, f, 1);
+      return false;
+    }
+    exm = 1ull << (uint32_t)f;
+  } else if (over) {
+    // a candidate without an evictable token
+    KVR_FAIL_CHECK(s, 11, (int32_t)cnt, first_lane(over), 0);
     return false;
   }
-  int f = (int)cnt - 1;  // last committed draw
-  uint64_t exm = 0;
-  const uint64_t risky = __ballot(act && e <= (int32_t)cnt);
-  if (risky) {
-    // rank of each risky draw among the draws on its candidate, in order
-    uint64_t todo = risky;
-    int32_t c = 0;
-    while (todo) {
-      const int j = first_lane(todo);
-      const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk, j);
-      const bool same = act && kk == v;
-      const uint64_t m = __ballot(same);
-      if (same) c = __popcll(m & lanemask_le());
-      todo &= ~m;
-    }
-    exm = __ballot(((risky >> lane) & 1ull) && c == e);
-    if (exm) f = first_lane(exm);
-  }
-  if (act && lane <= f) atomicSub(&u.len[kk], 1);
   done = (uint32_t)f + 1u;
   if (exm) {
+    changed = true;
     const uint32_t kkf = (uint32_t)__builtin_amdgcn_readlane((int)kk, f);
-    const int32_t nf = __builtin_amdgcn_readlane(n, f);
-    const int32_t pf = __builtin_amdgcn_readlane(par, f);
+    const int32_t nf = u.node[kkf];
+    const int32_t pf = u.par[kkf];
     const int32_t left = __builtin_amdgcn_readlane(top, f);
+    if (pf < 0 || nf <= 0) {
+      KVR_FAIL_CHECK(s, 11, nf, pf, 2);
+      return false;
+    }
     if (left > 0) {  // the next token is marked: no longer a candidate
       if (lane == 0) P.nodes[nf].len = left;
       wave_mem_sync();
@@ -1103,16 +1173,27 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         staged = true;
       }
       // draws for positions p, p+1, ...: never across a pending phase reset
-      uint32_t cnt = nev - k < (uint32_t)KVR_WAVE ? nev - k : (uint32_t)KVR_WAVE;
-      if (reset_at >= 0 && !applied && (uint32_t)(reset_at - p) < cnt) cnt = (uint32_t)(reset_at - p);
-      uint32_t done = 0;
+      uint32_t lim = nev;
+      if (reset_at >= 0 && !applied && (uint32_t)(reset_at - p) < nev - k) lim = k + (uint32_t)(reset_at - p);
       if (staged) {
-        if (!evict_block_staged(P, s, ia, ustage, dctr, cnt, done)) goto fail;
+        // blocks against the staged list until the limit or until U changes
+        while (k < lim) {
+          const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
+          uint32_t done = 0;
+          bool changed = false;
+          if (!evict_block_staged(P, s, ia, ustage, dctr, cnt, done, changed)) goto fail;
+          done = (uint32_t)__builtin_amdgcn_readfirstlane((int)done);
+          dctr += done;
+          k += done;
+          if (changed) break;
+        }
       } else {
+        const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
+        uint32_t done = 0;
         if (!evict_block(P, s, ia, dctr, cnt, done)) goto fail;
+        dctr += done;
+        k += done;
       }
-      dctr += done;
-      k += done;
     }
     if (staged) stage_out(P, s, ustage);
     if (reset_at >= 0 && !applied) {
@@ -1236,7 +1317,7 @@ __device__ void online_update(const Consts& C, WorkerHdr* w, const double phi[4]
 
 // Completions with t_done <= t (FIFO), then decay to t and drain the
 // observed-latency backlog.
-__device__ void complete_and_decay(const Consts& C, const Ptrs& P, int64_t t, int64_t tprev) {
+__device__ __forceinline__ void complete_and_decay(const Consts& C, const Ptrs& P, int64_t t, int64_t tprev) {
   WorkerHdr* w = P.hdr;
   const int64_t dt = C.dt_us;
   double Pl = w->P;
@@ -1299,7 +1380,7 @@ __device__ double lbgr_score(const Consts& C, const WorkerHdr* w, int32_t h, int
 // Commit a query on its routed worker: add the estimated service time to the
 // load estimate (Algorithm 2), advance the observed-latency queue and queue
 // the completion record.  Returns KVR_DEV_* bits.
-__device__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t L,
+__device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t L,
                                  int64_t t, int32_t olen) {
   WorkerHdr* w = P.hdr;
   const double base = chat + w->P;

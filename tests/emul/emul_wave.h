@@ -9,6 +9,7 @@
 #define KVR_WAVE 1
 #define __device__
 #define __forceinline__ inline
+#define __noinline__ __attribute__((noinline))
 #define __builtin_amdgcn_wave_barrier() ((void)0)
 #define __builtin_amdgcn_fence(order, scope) ((void)0)
 
@@ -19,7 +20,9 @@ struct int2 { int x, y; };
 inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
 inline int __shfl(int v, int, int) { return v; }
 inline int __builtin_amdgcn_readlane(int v, int) { return v; }
+inline int __builtin_amdgcn_readfirstlane(int v) { return v; }
 inline int atomicSub(int* p, int v) { int o = *p; *p -= v; return o; }
+inline int atomicAdd(int* p, int v) { int o = *p; *p += v; return o; }
 inline int __shfl_xor(int v, int, int) { return v; }
 inline int __shfl_up(int v, int, int) { return v; }
 inline int __ffsll(unsigned long long m) { return __builtin_ffsll((long long)m); }
