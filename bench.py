@@ -74,6 +74,56 @@ def cpu_baseline(stream, W, B, budget_s: float):
             "sample": f"replica 0, queries 0..{n} of the same stream, one thread, {dt:.1f} s"}
 
 
+def _pmc_rows(path: str, counter: str):
+    """(dispatch id, kernel name, value) of one counter from a rocprofv3 CSV."""
+    import csv
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if r.get("Counter_Name") == counter:
+                rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def traffic_from(args) -> int:
+    """HBM bytes per timed step-kernel launch: the counters (KiB per
+    dispatch) of the timed launches, each scaled by what the same counter
+    reads for the plain copy of --copy-probe-mib MiB."""
+    from workload import PRESETS
+    workload = PRESETS[args.config]["name"]
+    probe = args.copy_probe_mib << 20
+    if probe <= 0:
+        print("--traffic-from needs the --copy-probe-mib of the profiled runs", file=sys.stderr)
+        return 2
+    out = {"kernel_source_hash": kernel_source_hash(), "workload": workload, "steps": args.steps,
+           "warmup": args.warmup, "copy_probe_bytes": probe}
+    per = {}
+    for path, counter in zip(args.traffic_from, ("FETCH_SIZE", "WRITE_SIZE")):
+        rows = _pmc_rows(path, counter)
+        step = [v for _, name, v in rows if "step_kernel" in name]
+        if len(step) != args.warmup + args.steps:
+            print(f"{path}: {len(step)} step-kernel dispatches, expected {args.warmup + args.steps}",
+                  file=sys.stderr)
+            return 1
+        timed = step[args.warmup:]
+        # the probe: the last other dispatch whose count is near the probe size
+        cand = [v for _, name, v in rows if "kvr::" not in name and 0.5 * probe <= v * 1024 <= 2 * probe]
+        if not cand:
+            print(f"{path}: no copy-probe dispatch found", file=sys.stderr)
+            return 1
+        factor = cand[-1] * 1024 / probe
+        per[counter] = {"kib_per_launch": sum(timed) / len(timed), "probe_kib": cand[-1], "factor": factor,
+                        "bytes_per_launch": sum(timed) / len(timed) * 1024 / factor}
+    out["counters"] = per
+    out["bytes_per_launch"] = per["FETCH_SIZE"]["bytes_per_launch"] + per["WRITE_SIZE"]["bytes_per_launch"]
+    dst = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(dst, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -83,7 +133,16 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed region, copy this many MiB device to device with a plain "
+                         "copy kernel (the calibration run for rocprofv3 byte counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="compute HBM bytes per step-kernel launch from two rocprofv3 --pmc runs "
+                         "(FETCH_SIZE, WRITE_SIZE) of this benchmark with --copy-probe-mib, and "
+                         "write profiles/traffic_<workload>.json")
     args = ap.parse_args()
+    if args.traffic_from:
+        return traffic_from(args)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print("bench.py runs on one GPU only: replicas are independent, and this build measures "
@@ -179,6 +238,14 @@ def main() -> int:
     sim.close()
     del ds, out
     torch.cuda.empty_cache()
+    if args.copy_probe_mib:
+        src = torch.ones(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        line["copy_probe_bytes"] = src.numel()
+        del src, dst
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget)
     print(json.dumps(line), flush=True)

@@ -1176,17 +1176,27 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
       uint32_t lim = nev;
       if (reset_at >= 0 && !applied && (uint32_t)(reset_at - p) < nev - k) lim = k + (uint32_t)(reset_at - p);
       if (staged) {
-        // blocks against the staged list until the limit or until U changes
-        while (k < lim) {
-          const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
+        // blocks against the staged list until the limit or until U changes;
+        // the loop state is wave-uniform, so keep it in scalar registers
+        uint32_t ku = (uint32_t)__builtin_amdgcn_readfirstlane((int)k);
+        const uint32_t limu = (uint32_t)__builtin_amdgcn_readfirstlane((int)lim);
+        uint32_t du = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)dctr);
+        s.nU = (uint32_t)__builtin_amdgcn_readfirstlane((int)s.nU);
+        bool ok = true;
+        while (ku < limu) {
+          const uint32_t cnt = limu - ku < (uint32_t)KVR_WAVE ? limu - ku : (uint32_t)KVR_WAVE;
           uint32_t done = 0;
           bool changed = false;
-          if (!evict_block_staged(P, s, ia, ustage, dctr, cnt, done, changed)) goto fail;
+          ok = evict_block_staged(P, s, ia, ustage, (uint64_t)du, cnt, done, changed);
+          if (!ok) break;
           done = (uint32_t)__builtin_amdgcn_readfirstlane((int)done);
-          dctr += done;
-          k += done;
+          du += done;
+          ku += done;
           if (changed) break;
         }
+        k = ku;
+        dctr = du;
+        if (!ok) goto fail;
       } else {
         const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
         uint32_t done = 0;
