@@ -19,7 +19,7 @@ hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st)
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st);
 hipError_t set_step_lds_limit(size_t bytes);
-size_t step_lds_bytes(uint32_t maxL, uint32_t ucap, uint32_t rcap);
+size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap);
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -173,7 +173,7 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return fail_hip(e, "hipDeviceGetAttribute(max LDS per block)");
   const size_t static_lds = 2048;
-  const size_t qbytes = kvr::step_lds_bytes(L.maxL, 0, 0);
+  const size_t qbytes = kvr::step_lds_bytes(L.maxL, L.W, 0, 0);
   if (qbytes + static_lds > (size_t)lds_max)
     return fail(KVR_EINVAL, "max_query_tokens does not fit in LDS (" + std::to_string(lds_max) + " bytes)");
   size_t room = (size_t)lds_max - static_lds - qbytes;
@@ -184,7 +184,7 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   size_t ucap = room / 16u;
   if (ucap > 8192) ucap = 8192;
   if (ucap < 64) ucap = 0;
-  const size_t lds = kvr::step_lds_bytes(L.maxL, (uint32_t)ucap, (uint32_t)rcap);
+  const size_t lds = kvr::step_lds_bytes(L.maxL, L.W, (uint32_t)ucap, (uint32_t)rcap);
   if (lds > 65536) {
     e = kvr::set_step_lds_limit(lds);
     if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");

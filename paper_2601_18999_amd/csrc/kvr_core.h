@@ -623,6 +623,31 @@ __device__ __forceinline__ int32_t split_node(const Ptrs& P, St& s, int32_t x, i
   return hd;
 }
 
+// ---------------------------------------------------------------- match paths
+
+// The nodes a match entered, kept (in LDS) per worker so that the next match
+// on the same worker, and the insertion of a query routed there, can start
+// from them instead of walking the tree again.  Entry e = (node, depth
+// before its edge, depth after its edge); *cnt = number of entries, or
+// kPathMax + 1 when the path was longer than kPathMax or is unknown.
+constexpr int32_t kPathMax = 16;
+
+struct PathRef {
+  int32_t* node;
+  int32_t* start;
+  int32_t* end;
+  int32_t* cnt;
+};
+
+__device__ __forceinline__ void path_add(const PathRef& pr, int32_t& pc, int32_t node, int32_t start, int32_t end) {
+  if (pc < kPathMax && lane_id() == 0) {
+    pr.node[pc] = node;
+    pr.start[pc] = start;
+    pr.end[pc] = end;
+  }
+  pc = pc < kPathMax ? pc + 1 : kPathMax + 1;
+}
+
 // ---------------------------------------------------------------- RLT pieces
 
 // U := the leaves (other than `excl`) whose leaf token is unmarked, in the
@@ -688,6 +713,12 @@ __device__ __forceinline__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk
   return true;
 }
 
+// draws per lane in one staged eviction block
+#ifndef KVR_EVICT_DRAWS
+#define KVR_EVICT_DRAWS 4
+#endif
+constexpr int kEvictDraws = KVR_EVICT_DRAWS;
+
 struct InsertArgs {
   uint64_t seed;
   uint64_t jg;        // global query index
@@ -696,6 +727,10 @@ struct InsertArgs {
   uint32_t B;
   uint32_t rn;        // draw words 0..rn-1 are precomputed in rw
   const uint64_t* rw;
+  // when non-null: the words are being written by other waves, and are all
+  // there once *ready reaches ready_need (LDS counter, workgroup scope)
+  const uint32_t* ready;
+  uint32_t ready_need;
 };
 
 // Word 0 of Philox4x64-10 for draw d of this insertion: key (seed, replica),
@@ -862,63 +897,128 @@ __device__ __forceinline__ void stage_erase(const UStage& u, uint32_t n, uint32_
   }
 }
 
-// evict_block with U staged in LDS (same draws, same result).  Every draw
-// of the block first trims its candidate with an LDS atomic; the values the
-// atomics return show whether some candidate ran out of evictable tokens.
-// Only then (rarely) is the first exhausting draw in draw order found
-// exactly and the draws after it are undone.
+// evict_block with U staged in LDS (same draws, same result), kDraws draws
+// per lane: draw j of the block is taken by lane j % wave in slot j / wave.
+// Every draw of the block first trims its candidate with an LDS atomic; the
+// values the atomics return show whether some candidate ran out of
+// evictable tokens.  Only then (rarely) is the first exhausting draw in draw
+// order found exactly and the draws after it are undone.
+template <int kDraws>
 __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const InsertArgs& ia, const UStage& u,
                                                    uint64_t dctr, uint32_t cnt, uint32_t& done, bool& changed) {
   changed = false;
   const int lane = lane_id();
-  const bool act = (uint32_t)lane < cnt;
-  uint32_t kk = 0;
-  int32_t top = 0, old = 0;
-  if (act) {
-    const uint64_t r64 = draw_word(ia, dctr + (uint64_t)lane);
-    kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
-    top = u.top[kk];
-    old = atomicSub(&u.len[kk], 1);
+  bool act[kDraws];
+  uint64_t w[kDraws];
+  uint32_t kk[kDraws];
+  int32_t top[kDraws], old[kDraws];
+  // no divergent branch around the LDS accesses, so all of them can be in
+  // flight at once: inactive lanes read entry 0 and subtract 0
+  if (dctr + cnt <= ia.rn) {
+    // every active draw is precomputed; inactive lanes read the last word
+#pragma unroll
+    for (int r = 0; r < kDraws; ++r) {
+      uint64_t d = dctr + (uint64_t)(r * KVR_WAVE + lane);
+      if (d >= ia.rn) d = ia.rn - 1u;
+      w[r] = ia.rw[d];
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kDraws; ++r) {
+      const uint32_t j = (uint32_t)(r * KVR_WAVE + lane);
+      w[r] = j < cnt ? draw_word(ia, dctr + j) : 0ull;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kDraws; ++r) {
+    act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
+    kk[r] = act[r] ? (uint32_t)__umul64hi(w[r], (uint64_t)s.nU) : 0u;
+  }
+#pragma unroll
+  for (int r = 0; r < kDraws; ++r) {
+    top[r] = u.top[kk[r]];
+    old[r] = atomicSub(&u.len[kk[r]], act[r] ? 1 : 0);
   }
   // the decrements of one candidate return distinct values len, len-1, ...;
   // the one returning top + 1 took its last evictable token
-  uint64_t exm = __ballot(act && old == top + 1);
-  const uint64_t over = __ballot(act && old <= top);
+  uint64_t exm[kDraws];
+  uint64_t anyx = 0, over = 0;
+#pragma unroll
+  for (int r = 0; r < kDraws; ++r) {
+    exm[r] = __ballot(act[r] && old[r] == top[r] + 1);
+    anyx |= exm[r];
+    over |= __ballot(act[r] && old[r] <= top[r]);
+  }
   int f = (int)cnt - 1;  // last committed draw
-  if (exm) {
-    // exhausting draw of each exhausted candidate, in draw order: the
-    // e-th of the lanes drawing it, e = its evictable tokens before the block
-    uint64_t todo = exm;
-    while (todo) {
-      const int x = first_lane(todo);
-      todo &= todo - 1ull;
-      const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk, x);
-      const int32_t tv = __builtin_amdgcn_readlane(top, x);
-      uint64_t m = __ballot(act && kk == v);
-      const int e = __popcll(__ballot(act && kk == v && old > tv));
-      for (int c = 1; c < e; ++c) m &= m - 1ull;
-      const int fx = first_lane(m);
-      if (fx < f) f = fx;
+  if (anyx) {
+    // exhausting draw of each exhausted candidate, in draw order: the e-th
+    // of the draws on it, e = its evictable tokens before the block
+#pragma unroll
+    for (int rx = 0; rx < kDraws; ++rx) {
+      uint64_t todo = exm[rx];
+      while (todo) {
+        const int x = first_lane(todo);
+        todo &= todo - 1ull;
+        const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk[rx], x);
+        const int32_t tv = __builtin_amdgcn_readlane(top[rx], x);
+        int e = 0;
+#pragma unroll
+        for (int r = 0; r < kDraws; ++r) e += __popcll(__ballot(act[r] && kk[r] == v && old[r] > tv));
+        int fx = -1;
+#pragma unroll
+        for (int r = 0; r < kDraws; ++r) {
+          uint64_t m = __ballot(act[r] && kk[r] == v);
+          const int c = __popcll(m);
+          if (fx < 0) {
+            if (e <= c) {
+              for (int q = 1; q < e; ++q) m &= m - 1ull;
+              fx = r * KVR_WAVE + first_lane(m);
+            } else {
+              e -= c;
+            }
+          }
+        }
+        if (fx >= 0 && fx < f) f = fx;
+      }
     }
-    if (act && lane > f) atomicAdd(&u.len[kk], 1);
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < kDraws; ++r) {
+      const int j = r * KVR_WAVE + lane;
+      atomicAdd(&u.len[kk[r]], (act[r] && j > f) ? 1 : 0);
+    }
     // every committed draw leaves its candidate with len >= top
-    if (__ballot(act && lane <= f && u.len[kk] < top)) {
+#pragma unroll
+    for (int r = 0; r < kDraws; ++r) {
+      const int j = r * KVR_WAVE + lane;
+      if (act[r] && j <= f && u.len[kk[r]] < top[r]) bad = true;
+    }
+    if (__ballot(bad)) {
       KVR_FAIL_CHECK(s, 11, (int32_t)cnt, f, 1);
       return false;
     }
-    exm = 1ull << (uint32_t)f;
   } else if (over) {
     // a candidate without an evictable token
     KVR_FAIL_CHECK(s, 11, (int32_t)cnt, first_lane(over), 0);
     return false;
   }
+  // the exhausting draw's slot and lane
+  const int rf = f / KVR_WAVE, lf = f % KVR_WAVE;
+  uint32_t kkr = kk[0];
+  int32_t topr = top[0];
+#pragma unroll
+  for (int r = 1; r < kDraws; ++r)
+    if (rf == r) {
+      kkr = kk[r];
+      topr = top[r];
+    }
   done = (uint32_t)f + 1u;
-  if (exm) {
+  if (anyx) {
     changed = true;
-    const uint32_t kkf = (uint32_t)__builtin_amdgcn_readlane((int)kk, f);
+    const uint32_t kkf = (uint32_t)__builtin_amdgcn_readlane((int)kkr, lf);
     const int32_t nf = u.node[kkf];
     const int32_t pf = u.par[kkf];
-    const int32_t left = __builtin_amdgcn_readlane(top, f);
+    const int32_t left = __builtin_amdgcn_readlane(topr, lf);
     if (pf < 0 || nf <= 0) {
       KVR_FAIL_CHECK(s, 11, nf, pf, 2);
       return false;
@@ -969,22 +1069,69 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
 
 // RLT insertion of q[0, L) into the worker's cache; h = LCP(q, cache).
 // Returns the KVR_DEV_* error bits (0 on success).
+__device__ __forceinline__ NodeRec node_from_lane(const NodeRec& v, int e) {
+  NodeRec r;
+  r.parent = __builtin_amdgcn_readlane(v.parent, e);
+  r.off = (uint32_t)__builtin_amdgcn_readlane((int)v.off, e);
+  r.len = __builtin_amdgcn_readlane(v.len, e);
+  r.nchild = __builtin_amdgcn_readlane(v.nchild, e);
+  r.coff = (uint32_t)__builtin_amdgcn_readlane((int)v.coff, e);
+  r.ccap = __builtin_amdgcn_readlane(v.ccap, e);
+  r.mphase = (uint32_t)__builtin_amdgcn_readlane((int)v.mphase, e);
+  r.ma = __builtin_amdgcn_readlane(v.ma, e);
+  return r;
+}
+
+// RLT insertion of q[0, L) into the worker's cache; h = LCP(q, cache) and pr
+// holds the path of that match (or is marked unknown).  On return pr holds
+// the path of q in the updated cache.  Returns the KVR_DEV_* error bits (0
+// on success).
 __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
-                               int32_t h, const UStage& ustage, int64_t* dbg) {
+                               int32_t h, const UStage& ustage, const PathRef& pr, int64_t* dbg) {
   St s = load_st(P.hdr);
   const uint32_t B = ia.B;
   int32_t* ar = arena_of(P, s.arena_sel);
+  const int32_t pc = *pr.cnt;
+  const bool have_path = pc <= kPathMax;
+  bool split = false;
+  int32_t a = 0, l = 0, laststart = 0, pe = 0;
 
-  // ---- walk the cached part of the path and mark it
+  // ---- walk the cached part of the path and mark it: along the recorded
+  // path (node records of all its entries loaded at once) or, when there is
+  // none, by child lookups
+  NodeRec pre;
+  pre.parent = pre.len = pre.nchild = pre.ccap = pre.ma = 0;
+  pre.off = pre.coff = pre.mphase = 0;
+  if (KVR_WAVE >= kPathMax && have_path && lane_id() < pc) pre = P.nodes[pr.node[lane_id()]];
   int32_t x = 0, d = 0, last = 0, lastcov = 0;
   while (d < h) {
-    NodeRec nx = P.nodes[x];
-    int32_t c = child_find(ar, nx, qs[d]);
-    if (c <= 0 || (uint32_t)c >= s.hwm) {
-      KVR_FAIL_CHECK(s, 1, x, d, h);
-      goto fail;
+    int32_t c;
+    NodeRec nc;
+    if (have_path) {
+      if (pe >= pc || pr.start[pe] != d) {
+        KVR_FAIL_CHECK(s, 1, pe, d, h);
+        goto fail;
+      }
+      c = pr.node[pe];
+      if (c <= 0 || (uint32_t)c >= s.hwm) {
+        KVR_FAIL_CHECK(s, 1, c, d, h);
+        goto fail;
+      }
+      if (KVR_WAVE >= kPathMax) {
+        nc = node_from_lane(pre, pe);
+      } else {
+        nc = P.nodes[c];
+      }
+      ++pe;
+    } else {
+      NodeRec nx = P.nodes[x];
+      c = child_find(ar, nx, qs[d]);
+      if (c <= 0 || (uint32_t)c >= s.hwm) {
+        KVR_FAIL_CHECK(s, 1, x, d, h);
+        goto fail;
+      }
+      nc = P.nodes[c];
     }
-    NodeRec nc = P.nodes[c];
     int32_t cov = nc.len < h - d ? nc.len : h - d;
     if (cov <= 0) {
       KVR_FAIL_CHECK(s, 2, c, nc.len, d);
@@ -1017,30 +1164,28 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         P.nodes[c].mphase = s.phase;
         P.nodes[c].ma = nma;
       }
-      wave_mem_sync();
     } else {
       // |T| reaches B+1 at the `need`-th newly marked position of this edge
       int32_t need = (int32_t)(B + 1u - s.cnt);
-      int32_t pr;
+      int32_t rp;
       if (!rv) {
-        pr = ma + need - 1;
+        rp = ma + need - 1;
       } else {
         int32_t e1 = rlo < cov ? rlo : cov;
         int32_t s1 = e1 - ma > 0 ? e1 - ma : 0;
-        pr = need <= s1 ? ma + need - 1 : rhi + (need - s1) - 1;
+        rp = need <= s1 ? ma + need - 1 : rhi + (need - s1) - 1;
       }
       s.phase += 1;
       s.U_valid = 0;
-      s.cnt = (uint32_t)(cov - pr);
-      if (pr == 0) {
+      s.cnt = (uint32_t)(cov - rp);
+      if (rp == 0) {
         if (lane_id() == 0) {
           P.nodes[c].mphase = s.phase;
           P.nodes[c].ma = cov;
         }
-        wave_mem_sync();
       } else {
         s.rnode = c;
-        s.rlo = pr;
+        s.rlo = rp;
         s.rhi = cov;
         s.rphase = s.phase;
       }
@@ -1053,17 +1198,18 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         s.nU -= 1;
       }
     }
+    laststart = d;
     d += cov;
     last = c;
     lastcov = cov;
     x = c;
   }
+  wave_mem_sync();  // the marks above are read again below
 
   if (h < L) {
     const int32_t nload = L - h;
     // ---- attachment point: end of `last`, splitting it if needed
-    int32_t a = last;
-    bool split = false;
+    a = last;
     if (h > 0) {
       NodeRec nl = P.nodes[last];
       if (lastcov < nl.len) {
@@ -1107,7 +1253,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     ar = arena_of(P, s.arena_sel);
     for (int32_t k = lane_id(); k < nload; k += KVR_WAVE) ar[eoff + (uint32_t)k] = qs[h + k];
     wave_mem_sync();
-    int32_t l = node_alloc(P, s);
+    l = node_alloc(P, s);
     if (l < 0) goto fail;
     {
       NodeRec nl;
@@ -1140,6 +1286,18 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     uint64_t dctr = 0;
     uint32_t k = 0;
     bool staged = false;
+    InsertArgs iq = ia;
+    if (nev > 0 && iq.ready) {
+      // bounded wait; past it the words are computed here instead
+      uint32_t spins = 0;
+      while (__hip_atomic_load(iq.ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < iq.ready_need) {
+        if (++spins > (1u << 22)) {
+          iq.rn = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
     while (k < nev) {
       const int32_t p = h + (int32_t)nfree + (int32_t)k;
       if (reset_at >= 0 && !applied && p >= reset_at) {
@@ -1184,10 +1342,11 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         s.nU = (uint32_t)__builtin_amdgcn_readfirstlane((int)s.nU);
         bool ok = true;
         while (ku < limu) {
-          const uint32_t cnt = limu - ku < (uint32_t)KVR_WAVE ? limu - ku : (uint32_t)KVR_WAVE;
+          constexpr uint32_t kSpan = (uint32_t)kEvictDraws * KVR_WAVE;
+          const uint32_t cnt = limu - ku < kSpan ? limu - ku : kSpan;
           uint32_t done = 0;
           bool changed = false;
-          ok = evict_block_staged(P, s, ia, ustage, (uint64_t)du, cnt, done, changed);
+          ok = evict_block_staged<kEvictDraws>(P, s, iq, ustage, (uint64_t)du, cnt, done, changed);
           if (!ok) break;
           done = (uint32_t)__builtin_amdgcn_readfirstlane((int)done);
           du += done;
@@ -1200,7 +1359,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
       } else {
         const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
         uint32_t done = 0;
-        if (!evict_block(P, s, ia, dctr, cnt, done)) goto fail;
+        if (!evict_block(P, s, iq, dctr, cnt, done)) goto fail;
         dctr += done;
         k += done;
       }
@@ -1238,8 +1397,22 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
   }
   store_st(P.hdr, s);
   wave_mem_sync();
+  // ---- the path of q in the updated cache: the walked entries (the split
+  // head in place of the split node) and the new leaf
+  {
+    int32_t fc = have_path ? pe : kPathMax + 1;
+    if (fc <= kPathMax) {
+      if (split) {
+        int32_t f1 = fc - 1;
+        path_add(pr, f1, a, laststart, laststart + lastcov);
+      }
+      if (h < L) path_add(pr, fc, l, h, L);
+    }
+    if (lane_id() == 0) *pr.cnt = fc;
+  }
   return 0;
 fail:
+  if (lane_id() == 0) *pr.cnt = kPathMax + 1;
   store_st(P.hdr, s);
   if (dbg) {
     dbg[0] = s.dbg_check;
@@ -1274,22 +1447,73 @@ __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n)
   return n;
 }
 
-// h = length of the longest prefix of q[0, L) cached in the worker's tree.
-__device__ int32_t match_lcp(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L) {
+// Continue matching q[0, L) from inside node x (x = 0: the root), `off`
+// tokens into its edge, with d tokens matched so far.  Entries of the nodes
+// entered are appended at pc.  Returns h.
+__device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L, int32_t x, int32_t off,
+                              int32_t d, const PathRef& pr, int32_t& pc) {
   const int32_t* ar = arena_of(P, sel);
-  int32_t x = 0, h = 0;
-  while (h < L) {
+  if (x != 0 && d < L) {
+    const NodeRec nx = P.nodes[x];
+    if (off < nx.len) {  // the rest of this edge first
+      const int32_t rest = nx.len - off;
+      const int32_t n = rest < L - d ? rest : L - d;
+      const int32_t k = first_mismatch(ar + nx.off + off, qs + d, n);
+      d += k;
+      if (k < rest) return d;
+    }
+  }
+  while (d < L) {
     NodeRec nx = P.nodes[x];
-    int32_t c = child_find(ar, nx, qs[h]);
+    int32_t c = child_find(ar, nx, qs[d]);
     if (c < 0) break;
     NodeRec nc = P.nodes[c];
     if (nc.len <= 0) break;  // never true for a consistent tree
-    int32_t n = nc.len < L - h ? nc.len : L - h;
-    int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + h + 1, n - 1);
-    h += k;
+    path_add(pr, pc, c, d, d + nc.len);
+    int32_t n = nc.len < L - d ? nc.len : L - d;
+    int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + d + 1, n - 1);
+    d += k;
     if (k < nc.len) break;
     x = c;
   }
+  return d;
+}
+
+// h = length of the longest prefix of q[0, L) cached in the worker's tree,
+// recording the path.
+__device__ __forceinline__ int32_t match_lcp(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L,
+                                             const PathRef& pr) {
+  int32_t pc = 0;
+  const int32_t h = match_from(P, sel, qs, L, 0, 0, 0, pr, pc);
+  if (lane_id() == 0) *pr.cnt = pc;
+  return h;
+}
+
+// h of q_new on a worker whose tree holds the recorded match path of the
+// previous query q_old, h_old = h of q_old there, ell = LCP(q_old, q_new).
+// Up to depth min(h_old, ell) both walks are the same.  If the old match
+// stopped first (h_old < ell) the new one stops at the same point.  Else the
+// new one leaves q_old's path at depth ell: inside an edge that the old
+// match followed further it stops there; otherwise it continues from that
+// point.  The path record is updated to the new match.
+__device__ __forceinline__ int32_t match_incremental(const Ptrs& P, uint32_t sel, const int32_t* qn, int32_t Ln, int32_t h_old,
+                                     int32_t ell, const PathRef& pr) {
+  int32_t pc = *pr.cnt;
+  if (pc > kPathMax || ell == 0) return match_lcp(P, sel, qn, Ln, pr);
+  if (h_old < ell) return h_old;
+  // the entry holding depth ell: the last one starting above it
+  int32_t e = pc - 1;
+  while (e > 0 && pr.start[e] >= ell) --e;
+  const int32_t x = pr.node[e], st = pr.start[e], en = pr.end[e];
+  if (pc == 0 || st >= ell || en < ell) return match_lcp(P, sel, qn, Ln, pr);  // inconsistent record
+  pc = e + 1;
+  int32_t h;
+  if (ell == Ln || (ell < en && h_old > ell)) {
+    h = ell;
+  } else {
+    h = match_from(P, sel, qn, Ln, x, ell - st, ell, pr, pc);
+  }
+  if (lane_id() == 0) *pr.cnt = pc;
   return h;
 }
 

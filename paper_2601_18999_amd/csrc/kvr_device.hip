@@ -42,32 +42,86 @@ namespace kvr {
 
 // ---------------------------------------------------------------- kernels
 
-// Match q[0, L) on worker i, record h in hslot, count the matched tokens.
-__device__ __forceinline__ void match_worker(const StepArgs& a, uint32_t r, uint32_t i, const int32_t* q,
-                                             int32_t L, int32_t* hslot) {
-  Ptrs P = worker_ptrs(a.ws, a.L, r, i);
-  const uint32_t sel = P.hdr->arena_sel;
-  const int32_t h = match_lcp(P, sel, q, L);
+// Paths recorded in LDS: entries of worker i at [i * kPathMax, (i+1) * kPathMax)
+// of the node, start and end arrays, then one count per worker.
+struct PathArea {
+  int32_t* base;
+  uint32_t W;
+  __device__ PathRef of(uint32_t i) const {
+    PathRef p;
+    p.node = base + (size_t)i * kPathMax;
+    p.start = base + (size_t)(W + i) * kPathMax;
+    p.end = base + (size_t)(2 * W + i) * kPathMax;
+    p.cnt = base + (size_t)3 * W * kPathMax + i;
+    return p;
+  }
+};
+
+__device__ __forceinline__ void count_matched(const Ptrs& P, int32_t h, int32_t* hslot) {
   if (lane_id() == 0) {
     *hslot = h;
     P.hdr->matched_tokens += (uint64_t)h;
   }
 }
 
-// One workgroup per replica walks the batch in order.  The tree of a worker
+// Stage q_next[0, Ln) (threads t0, t0 + stride, ...) and fold each thread's
+// first position where it differs from q_cur into *ell (LDS minimum), so
+// that after the next barrier *ell = LCP(q_cur, q_next).
+__device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, int32_t Ln, int32_t* qn,
+                                           const int32_t* qc, int32_t Lc, uint32_t t0, uint32_t stride,
+                                           int32_t* ell) {
+  int32_t m = Lc < Ln ? Lc : Ln;
+  for (uint32_t x = t0; x < (uint32_t)Ln; x += stride) {
+    const int32_t v = tokens[n0 + x];
+    qn[x] = v;
+    if ((int32_t)x < m && qc[x] != v) m = (int32_t)x;
+  }
+  // minimum over the wave, then one LDS atomic per wave
+  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
+    const int32_t y = __shfl_xor(m, o, KVR_WAVE);
+    m = y < m ? y : m;
+  }
+  if (lane_id() == 0) atomicMin(ell, m);
+}
+
+// Lowest index among the minimal scores (lanes >= W hold +inf): the same
+// result as scanning i = 0..W-1 with a strict less-than.  -0.0 is folded
+// into +0.0 (they compare equal); a NaN makes the scan itself decide.
+__device__ __forceinline__ uint32_t wave_argmin(double eh, uint32_t W, const double* eh_sh) {
+  if (__ballot(eh != eh)) {
+    uint32_t best = 0;
+    for (uint32_t i = 1; i < W; ++i)
+      if (eh_sh[i] < eh_sh[best]) best = i;
+    return best;
+  }
+  const double z = eh + 0.0;
+  uint64_t b = (uint64_t)__double_as_longlong(z);
+  b = (b >> 63) ? ~b : (b | 0x8000000000000000ull);  // order-preserving key
+  const uint64_t mn = wave_min_u64(b);
+  return (uint32_t)first_lane(__ballot(b == mn));
+}
+
+// One workgroup per replica walks the batch in order.  A worker's tree
 // changes only when a query is routed to it, so while wave 0 inserts query k
-// into the routed worker, the other waves already match query k+1 against
-// every other worker; only the routed worker is matched again afterwards.
+// into the routed worker the other waves compute the draw words of that
+// insertion, the completions and decay at the next arrival, and the next
+// query's h on every other worker.  Matches are incremental: each worker
+// keeps the path of its last match, and the next query follows it up to
+// the longest common prefix of the two queries.  The routed worker's h for
+// the next query is completed from the path of the inserted query.
 __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
-  // dynamic LDS: two query buffers (max_query_tokens entries each; the next
-  // query is staged and matched while the current one is inserted), the
-  // precomputed draw words, then the staged candidate list
+  // dynamic LDS: two query buffers (max_query_tokens entries each), the draw
+  // words, the match paths, then the staged candidate list
   extern __shared__ int32_t smem[];
+  const uint32_t W = a.L.W;
   const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
   uint64_t* rw = reinterpret_cast<uint64_t*>(smem + 2 * qstride);
+  PathArea paths;
+  paths.base = reinterpret_cast<int32_t*>(rw + a.rcap);
+  paths.W = W;
   UStage ustage;
   {
-    int32_t* ub = reinterpret_cast<int32_t*>(rw + a.rcap);
+    int32_t* ub = paths.base + (size_t)W * (3 * kPathMax + 1);
     ustage.node = ub;
     ustage.len = ub + a.ucap;
     ustage.top = ub + 2 * a.ucap;
@@ -77,31 +131,41 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ int32_t h_sh[2][kMaxWorkers];  // h of the current and of the next query
   __shared__ double eh_sh[kMaxWorkers];
   __shared__ double ch_sh[kMaxWorkers];
+  __shared__ int32_t ell_sh[2];  // LCP(q_k, q_k+1) in slot k & 1
   __shared__ int32_t best_sh;
   __shared__ uint32_t abort_sh;
   __shared__ uint32_t nev_sh;
+  __shared__ uint32_t wready_sh;  // helper waves done with the draw words
 
   const uint32_t r = blockIdx.x;
-  const uint32_t W = a.L.W;
   const int lane = lane_id();
   const uint32_t wave = threadIdx.x / KVR_WAVE;
   const uint32_t nwaves = blockDim.x / KVR_WAVE;
+  const uint32_t nh = nwaves - 1;  // helper waves
   GlobalHdr* g = reinterpret_cast<GlobalHdr*>(a.ws + a.L.off_global);
   ReplicaHdr* rh = reinterpret_cast<ReplicaHdr*>(a.ws + a.L.off_rhdr) + r;
 
-  if (threadIdx.x == 0) abort_sh = __atomic_load_n(&g->status, __ATOMIC_RELAXED);
+  if (threadIdx.x == 0) {
+    abort_sh = __atomic_load_n(&g->status, __ATOMIC_RELAXED);
+    ell_sh[0] = 0x7fffffff;
+  }
   __syncthreads();
   if (abort_sh) return;
 
-  // query 0: stage it and match it on every worker
+  // query 0: stage it; completions and decay at its arrival; full matches
   {
     const uint64_t o0 = a.offsets[0];
     const int32_t L0 = (int32_t)(a.offsets[1] - o0);
     for (int32_t x = (int32_t)threadIdx.x; x < L0; x += (int32_t)blockDim.x) smem[x] = a.tokens[o0 + x];
+    if (wave == 0 && (uint32_t)lane < W)
+      complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[0], rh->tprev);
     __syncthreads();
-    for (uint32_t i = wave; i < W; i += nwaves) match_worker(a, r, i, smem, L0, &h_sh[0][i]);
+    for (uint32_t i = wave; i < W; i += nwaves) {
+      Ptrs P = worker_ptrs(a.ws, a.L, r, i);
+      count_matched(P, match_lcp(P, P.hdr->arena_sel, smem, L0, paths.of(i)), &h_sh[0][i]);
+    }
   }
-  int32_t stale = -1;  // worker whose h for the current query is not known yet
+  int32_t stale = -1, Lprev = 0;
   for (uint32_t k = 0; k < a.n; ++k) {
     const uint64_t o0 = a.offsets[k];
     const int32_t Lq = (int32_t)(a.offsets[k + 1] - o0);
@@ -119,45 +183,31 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     }
     __syncthreads();
 
-    // completions and decay (wave 0, one lane per worker); the last wave
-    // matches the current query on the worker routed last time; the others
-    // stage the next query
-    if (wave == 0 && (uint32_t)lane < W) {
-      const int64_t tprev = rh->tprev;
-      complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), t, tprev);
-    }
-    const uint32_t mwave = nwaves - 1;
-    if (stale >= 0 && wave == mwave) match_worker(a, r, (uint32_t)stale, qs, Lq, &h_sh[cur][stale]);
-    if (has_next) {
-      if (nwaves == 1) {
-        for (int32_t x = (int32_t)threadIdx.x; x < Ln; x += (int32_t)blockDim.x) qn[x] = a.tokens[n0 + x];
-      } else if (wave != mwave) {
-        for (int32_t x = (int32_t)threadIdx.x; x < Ln; x += (int32_t)(blockDim.x - KVR_WAVE)) qn[x] = a.tokens[n0 + x];
-      }
-    }
-    __syncthreads();
-
+    // ---- phase A.  Wave 0: the routed worker of the last query gets its h
+    // for this one; scores, argmin, commit.  Helpers: stage the next query.
     if (wave == 0) {
+      if (stale >= 0) {
+        Ptrs P = worker_ptrs(a.ws, a.L, r, (uint32_t)stale);
+        const int32_t h = match_incremental(P, P.hdr->arena_sel, qs, Lq, Lprev, ell_sh[cur ^ 1u],
+                                            paths.of((uint32_t)stale));
+        count_matched(P, h, &h_sh[cur][stale]);
+        __builtin_amdgcn_wave_barrier();
+      }
+      double eh = __builtin_huge_val();
       if ((uint32_t)lane < W) {
         double ch;
-        eh_sh[lane] = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[cur][lane], Lq, &ch);
+        eh = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[cur][lane], Lq, &ch);
         ch_sh[lane] = ch;
+        eh_sh[lane] = eh;
       }
       __builtin_amdgcn_wave_barrier();
-      if (lane == 0) {
-        uint32_t best = 0;  // argmin, lowest index on ties
-        for (uint32_t i = 1; i < W; ++i)
-          if (eh_sh[i] < eh_sh[best]) best = i;
-        best_sh = (int32_t)best;
-        rh->tprev = t;
-      }
-      __builtin_amdgcn_wave_barrier();
-      const uint32_t best = (uint32_t)best_sh;
+      const uint32_t best = wave_argmin(eh, W, eh_sh);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       const int32_t hb = h_sh[cur][best];
-      uint32_t err = 0;
       if (lane == 0) {
-        err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
+        best_sh = (int32_t)best;
+        wready_sh = 0;
+        const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
         if (a.hits) a.hits[orow] = hb;
@@ -173,17 +223,23 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       }
       if (a.all_hits && (uint32_t)lane < W)
         a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[cur][lane];
+      if (nh == 0 && has_next) stage_next(a.tokens, n0, Ln, qn, qs, Lq, (uint32_t)lane, KVR_WAVE, &ell_sh[cur]);
+    } else if (has_next) {
+      stage_next(a.tokens, n0, Ln, qn, qs, Lq, threadIdx.x - KVR_WAVE, blockDim.x - KVR_WAVE, &ell_sh[cur]);
     }
     __syncthreads();
     if (abort_sh) break;
     const uint32_t best = (uint32_t)best_sh;
     const uint32_t nev = nev_sh;
     const uint32_t rn = nev < a.rcap ? nev : a.rcap;
-    for (uint32_t d = threadIdx.x; d < rn; d += blockDim.x)
-      rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
-    if (rn) __syncthreads();
+    const int32_t ell = ell_sh[cur];
 
+    // ---- phase B.  Wave 0: RLT insertion.  Helpers: the insertion's draw
+    // words first, then completions and decay at the next arrival and the
+    // next query's h on the other workers.
     if (wave == 0) {
+      if (nh == 0)
+        for (uint32_t d = (uint32_t)lane; d < rn; d += KVR_WAVE) rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       InsertArgs ia;
       ia.seed = a.C.seed;
@@ -193,8 +249,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.B = a.L.B;
       ia.rn = rn;
       ia.rw = rw;
+      ia.ready = nh ? &wready_sh : nullptr;
+      ia.ready_need = nh;
       int64_t dbg[4] = {0, 0, 0, 0};
-      const uint32_t err = rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, dbg);
+      const uint32_t err = rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, paths.of(best), dbg);
       if (lane == 0 && err) {
         if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];
@@ -207,20 +265,45 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         atomicOr(&g->status, err);
         abort_sh = 1;
       }
-    } else if (has_next) {
-      // run-ahead: the next query on every worker but the routed one
-      for (uint32_t i = wave - 1; i < W; i += nwaves - 1)
-        if (i != best) match_worker(a, r, i, qn, Ln, &h_sh[cur ^ 1u][i]);
+      if (nh == 0 && has_next) {
+        if ((uint32_t)lane < W)
+          complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
+        if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
+        for (uint32_t i = 0; i < W; ++i)
+          if (i != best) {
+            Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
+            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
+                          &h_sh[cur ^ 1u][i]);
+          }
+      }
+    } else {
+      for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
+        rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (has_next) {
+        if (wave == 1) {
+          if ((uint32_t)lane < W)
+            complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
+          if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
+        }
+        for (uint32_t i = wave - 1; i < W; i += nh)
+          if (i != best) {
+            Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
+            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
+                          &h_sh[cur ^ 1u][i]);
+          }
+      }
     }
     stale = (int32_t)best;
-    if (nwaves == 1 && has_next) {
-      for (uint32_t i = 0; i < W; ++i)
-        if (i != best) match_worker(a, r, i, qn, Ln, &h_sh[cur ^ 1u][i]);
-    }
+    Lprev = Lq;
     __syncthreads();
     if (abort_sh) break;
   }
-  if (threadIdx.x == 0 && r == 0 && !abort_sh && a.n > 0) g->last_arrival = a.arrival[a.n - 1];
+  if (threadIdx.x == 0 && !abort_sh && a.n > 0) {
+    rh->tprev = a.arrival[a.n - 1];
+    if (r == 0) g->last_arrival = a.arrival[a.n - 1];
+  }
 }
 
 __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
@@ -278,9 +361,9 @@ __global__ void stats_kernel(char* ws, Layout L) {
 
 // ---------------------------------------------------------------- launchers (host)
 
-size_t step_lds_bytes(uint32_t maxL, uint32_t ucap, uint32_t rcap) {
+size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap) {
   return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint64_t) +
-         (size_t)ucap * 4u * sizeof(int32_t);
+         (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
 }
 
 
@@ -298,7 +381,7 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(validate_tokens_kernel, dim3(1024), dim3(256), 0, st, a.ws, a.L, a.tokens,
                      a.offsets, a.n);
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
-  const size_t lds = step_lds_bytes(a.L.maxL, a.ucap, a.rcap);
+  const size_t lds = step_lds_bytes(a.L.maxL, a.L.W, a.ucap, a.rcap);
   hipLaunchKernelGGL(step_kernel, dim3(a.L.R), dim3(64 * waves), lds, st, a);
   return hipGetLastError();
 }

@@ -21,6 +21,13 @@ inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
 inline int __shfl(int v, int, int) { return v; }
 inline int __builtin_amdgcn_readlane(int v, int) { return v; }
 inline int __builtin_amdgcn_readfirstlane(int v) { return v; }
+inline void __builtin_amdgcn_s_sleep(int) {}
+#define __ATOMIC_ACQUIRE_EMUL 0
+template <typename T> inline T __hip_atomic_load(const T* p, int, int) { return *p; }
+template <typename T> inline T __hip_atomic_fetch_add(T* p, T v, int, int) { T o = *p; *p += v; return o; }
+#ifndef __HIP_MEMORY_SCOPE_WORKGROUP
+#define __HIP_MEMORY_SCOPE_WORKGROUP 3
+#endif
 inline int atomicSub(int* p, int v) { int o = *p; *p -= v; return o; }
 inline int atomicAdd(int* p, int v) { int o = *p; *p += v; return o; }
 inline int __shfl_xor(int v, int, int) { return v; }

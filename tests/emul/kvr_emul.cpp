@@ -41,32 +41,64 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   ustage.cap = ucap;
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
+  // per-worker match paths (LDS on the device)
+  std::vector<int32_t> pbuf((size_t)W * (3 * kPathMax + 1));
+  auto path_of = [&](uint32_t i) {
+    PathRef p;
+    p.node = pbuf.data() + (size_t)i * kPathMax;
+    p.start = pbuf.data() + (size_t)(W + i) * kPathMax;
+    p.end = pbuf.data() + (size_t)(2 * W + i) * kPathMax;
+    p.cnt = pbuf.data() + (size_t)3 * W * kPathMax + i;
+    return p;
+  };
   for (uint32_t r = 0; r < L.R; ++r) {
+    // the schedule of step_kernel for one replica, one batch: completions of
+    // query 0 and full matches first; then per query the stale worker's
+    // incremental match, scores, route, commit, insert, completions of the
+    // next query and incremental matches of it on the other workers
+    int32_t h[2][kMaxWorkers];
     int64_t tprev = 0;
+    if (n > 0) {
+      for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), arrival[0], tprev);
+      for (uint32_t i = 0; i < W; ++i) {
+        Ptrs P = worker_ptrs(ws, L, r, i);
+        h[0][i] = match_lcp(P, P.hdr->arena_sel, tokens + offsets[0], (int32_t)(offsets[1] - offsets[0]), path_of(i));
+        P.hdr->matched_tokens += (uint64_t)h[0][i];
+      }
+    }
+    int32_t stale = -1, Lprev = 0, ell_prev = 0;
     for (uint64_t j = 0; j < n; ++j) {
+      const int cur = (int)(j & 1u);
       const int32_t* qs = tokens + offsets[j];
       const int32_t Lq = (int32_t)(offsets[j + 1] - offsets[j]);
       const int64_t t = arrival[j];
       const int32_t olen = out_len ? (int32_t)out_len[j] : 4;
-      int32_t h[kMaxWorkers];
+      const bool has_next = j + 1 < n;
+      const int32_t* qn = has_next ? tokens + offsets[j + 1] : nullptr;
+      const int32_t Ln = has_next ? (int32_t)(offsets[j + 2] - offsets[j + 1]) : 0;
       double eh[kMaxWorkers], ch[kMaxWorkers];
-      for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), t, tprev);
-      for (uint32_t i = 0; i < W; ++i) {
-        Ptrs P = worker_ptrs(ws, L, r, i);
-        h[i] = match_lcp(P, P.hdr->arena_sel, qs, Lq);
-        P.hdr->matched_tokens += (uint64_t)h[i];
+      if (stale >= 0) {
+        Ptrs P = worker_ptrs(ws, L, r, (uint32_t)stale);
+        h[cur][stale] = match_incremental(P, P.hdr->arena_sel, qs, Lq, Lprev, ell_prev, path_of((uint32_t)stale));
+        P.hdr->matched_tokens += (uint64_t)h[cur][stale];
       }
-      for (uint32_t i = 0; i < W; ++i) eh[i] = lbgr_score(C, worker_ptrs(ws, L, r, i).hdr, h[i], Lq, &ch[i]);
+      for (uint32_t i = 0; i < W; ++i)
+        eh[i] = lbgr_score(C, worker_ptrs(ws, L, r, i).hdr, h[cur][i], Lq, &ch[i]);
       uint32_t best = 0;
       for (uint32_t i = 1; i < W; ++i)
         if (eh[i] < eh[best]) best = i;
-      tprev = t;
       Ptrs P = worker_ptrs(ws, L, r, best);
-      uint32_t err = commit_route(C, P, ch[best], h[best], Lq, t, olen);
+      uint32_t err = commit_route(C, P, ch[best], h[cur][best], Lq, t, olen);
       if (route) route[r * n + j] = (int32_t)best;
-      if (hits) hits[r * n + j] = h[best];
+      if (hits) hits[r * n + j] = h[cur][best];
       if (all_hits)
-        for (uint32_t i = 0; i < W; ++i) all_hits[(r * n + j) * W + i] = h[i];
+        for (uint32_t i = 0; i < W; ++i) all_hits[(r * n + j) * W + i] = h[cur][i];
+      // LCP of this query and the next
+      int32_t ell = 0;
+      if (has_next) {
+        const int32_t m = Lq < Ln ? Lq : Ln;
+        while (ell < m && qs[ell] == qn[ell]) ++ell;
+      }
       if (!err) {
         InsertArgs ia;
         ia.seed = C.seed;
@@ -76,9 +108,24 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.B = L.B;
         ia.rn = 0;
         ia.rw = nullptr;
-        err = rlt_insert(P, ia, qs, Lq, h[best], ustage, nullptr);
+        ia.ready = nullptr;
+        ia.ready_need = 0;
+        err = rlt_insert(P, ia, qs, Lq, h[cur][best], ustage, path_of(best), nullptr);
       }
       if (err) return (int)err;
+      if (has_next) {
+        for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), arrival[j + 1], t);
+        for (uint32_t i = 0; i < W; ++i) {
+          if (i == best) continue;
+          Ptrs Pi = worker_ptrs(ws, L, r, i);
+          h[cur ^ 1][i] = match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h[cur][i], ell, path_of(i));
+          Pi.hdr->matched_tokens += (uint64_t)h[cur ^ 1][i];
+        }
+      }
+      stale = (int32_t)best;
+      Lprev = Lq;
+      ell_prev = ell;
+      tprev = t;
     }
   }
   for (uint32_t r = 0; r < L.R; ++r)
