@@ -177,10 +177,11 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   if (qbytes + static_lds > (size_t)lds_max)
     return fail(KVR_EINVAL, "max_query_tokens does not fit in LDS (" + std::to_string(lds_max) + " bytes)");
   size_t room = (size_t)lds_max - static_lds - qbytes;
-  // precomputed draw words first (8 B each, up to 4096), then candidates
-  size_t rcap = room / 2 / 8u;
-  if (rcap > 4096) rcap = 4096;
-  room -= rcap * 8u;
+  // high halves of the draw words first (4 B each, as many as one query can
+  // take, within 3/5 of the room), then candidates
+  size_t rcap = room * 3u / 5u / 4u;
+  if (rcap > L.maxL) rcap = L.maxL;
+  room -= rcap * 4u;
   size_t ucap = room / 16u;
   if (ucap > 8192) ucap = 8192;
   if (ucap < 64) ucap = 0;

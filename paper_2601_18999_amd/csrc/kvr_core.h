@@ -725,8 +725,8 @@ struct InsertArgs {
   uint32_t worker;    // routed worker
   uint32_t replica;
   uint32_t B;
-  uint32_t rn;        // draw words 0..rn-1 are precomputed in rw
-  const uint64_t* rw;
+  uint32_t rn;        // the high halves of draw words 0..rn-1 are precomputed in rw
+  const uint32_t* rw;
   // when non-null: the words are being written by other waves, and are all
   // there once *ready reaches ready_need (LDS counter, workgroup scope)
   const uint32_t* ready;
@@ -741,8 +741,17 @@ __device__ __noinline__ uint64_t draw_word_slow(uint64_t jg, uint64_t worker, ui
 }
 
 __device__ __forceinline__ uint64_t draw_word(const InsertArgs& ia, uint64_t d) {
-  if (d < ia.rn) return ia.rw[d];
   return draw_word_slow(ia.jg, ia.worker, d, ia.seed, ia.replica);
+}
+
+// Index floor(r * n / 2^64) of a draw from the high half of r alone: with
+// A = r_hi * n, the index is (A + floor(r_lo * n / 2^32)) / 2^32, and the
+// second term (< n) can carry into the high half only when the low half of A
+// is above 2^32 - n.  Returns false in that case (the full word decides).
+__device__ __forceinline__ bool draw_index_hi(uint32_t r_hi, uint32_t n, uint32_t& k) {
+  const uint64_t A = (uint64_t)r_hi * n;
+  k = (uint32_t)(A >> 32);
+  return (uint32_t)A <= 0xffffffffu - n + 1u;
 }
 
 // Evict with draws dctr .. dctr+cnt-1 (cnt <= wave width), one lane per
@@ -758,11 +767,11 @@ __device__ __forceinline__ bool evict_block(const Ptrs& P, St& s, const InsertAr
   const bool act = (uint32_t)lane < cnt;
   uint32_t kk = 0;
   int32_t n = 0;
-  if (act) {
-    const uint64_t r64 = draw_word(ia, dctr + (uint64_t)lane);
-    kk = (uint32_t)__umul64hi(r64, (uint64_t)s.nU);
-    n = P.U[kk];
-  }
+  const uint64_t d = dctr + (uint64_t)lane;
+  bool exact = false;
+  if (act && d < ia.rn) exact = draw_index_hi(ia.rw[d], s.nU, kk);
+  if (act && !exact) kk = (uint32_t)__umul64hi(draw_word(ia, d), (uint64_t)s.nU);
+  if (act) n = P.U[kk];
   if (__ballot(act && (n <= 0 || (uint32_t)n >= s.hwm))) {
     KVR_FAIL_CHECK(s, 10, kk, n, s.nU);
     return false;
@@ -909,30 +918,35 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
   changed = false;
   const int lane = lane_id();
   bool act[kDraws];
-  uint64_t w[kDraws];
   uint32_t kk[kDraws];
   int32_t top[kDraws], old[kDraws];
   // no divergent branch around the LDS accesses, so all of them can be in
   // flight at once: inactive lanes read entry 0 and subtract 0
+  bool exact = true;
   if (dctr + cnt <= ia.rn) {
-    // every active draw is precomputed; inactive lanes read the last word
+    // every active draw's high half is precomputed; inactive lanes read the
+    // last one
 #pragma unroll
     for (int r = 0; r < kDraws; ++r) {
       uint64_t d = dctr + (uint64_t)(r * KVR_WAVE + lane);
+      act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
       if (d >= ia.rn) d = ia.rn - 1u;
-      w[r] = ia.rw[d];
+      uint32_t k = 0;
+      const bool ok = draw_index_hi(ia.rw[d], s.nU, k);
+      kk[r] = act[r] ? k : 0u;
+      if (act[r] && !ok) exact = false;
     }
   } else {
 #pragma unroll
-    for (int r = 0; r < kDraws; ++r) {
-      const uint32_t j = (uint32_t)(r * KVR_WAVE + lane);
-      w[r] = j < cnt ? draw_word(ia, dctr + j) : 0ull;
-    }
+    for (int r = 0; r < kDraws; ++r) act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
+    exact = false;
   }
+  if (__ballot(!exact)) {
+    // rare: whole words for this block
 #pragma unroll
-  for (int r = 0; r < kDraws; ++r) {
-    act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
-    kk[r] = act[r] ? (uint32_t)__umul64hi(w[r], (uint64_t)s.nU) : 0u;
+    for (int r = 0; r < kDraws; ++r)
+      kk[r] = act[r] ? (uint32_t)__umul64hi(draw_word(ia, dctr + (uint64_t)(r * KVR_WAVE + lane)), (uint64_t)s.nU)
+                     : 0u;
   }
 #pragma unroll
   for (int r = 0; r < kDraws; ++r) {

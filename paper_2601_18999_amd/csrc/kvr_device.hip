@@ -110,12 +110,12 @@ __device__ __forceinline__ uint32_t wave_argmin(double eh, uint32_t W, const dou
 // the longest common prefix of the two queries.  The routed worker's h for
 // the next query is completed from the path of the inserted query.
 __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
-  // dynamic LDS: two query buffers (max_query_tokens entries each), the draw
-  // words, the match paths, then the staged candidate list
+  // dynamic LDS: two query buffers (max_query_tokens entries each), the high
+  // halves of the draw words, the match paths, then the staged candidate list
   extern __shared__ int32_t smem[];
   const uint32_t W = a.L.W;
   const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
-  uint64_t* rw = reinterpret_cast<uint64_t*>(smem + 2 * qstride);
+  uint32_t* rw = reinterpret_cast<uint32_t*>(smem + 2 * qstride);
   PathArea paths;
   paths.base = reinterpret_cast<int32_t*>(rw + a.rcap);
   paths.W = W;
@@ -239,7 +239,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     // next query's h on the other workers.
     if (wave == 0) {
       if (nh == 0)
-        for (uint32_t d = (uint32_t)lane; d < rn; d += KVR_WAVE) rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
+        for (uint32_t d = (uint32_t)lane; d < rn; d += KVR_WAVE)
+          rw[d] = (uint32_t)(philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r) >> 32);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       InsertArgs ia;
       ia.seed = a.C.seed;
@@ -278,7 +279,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       }
     } else {
       for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
-        rw[d] = philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r);
+        rw[d] = (uint32_t)(philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r) >> 32);
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
       if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (has_next) {
@@ -362,7 +363,7 @@ __global__ void stats_kernel(char* ws, Layout L) {
 // ---------------------------------------------------------------- launchers (host)
 
 size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap) {
-  return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint64_t) +
+  return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint32_t) +
          (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
 }
 

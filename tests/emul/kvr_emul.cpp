@@ -41,6 +41,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   ustage.cap = ucap;
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
+  std::vector<uint32_t> rwbuf;
   // per-worker match paths (LDS on the device)
   std::vector<int32_t> pbuf((size_t)W * (3 * kPathMax + 1));
   auto path_of = [&](uint32_t i) {
@@ -100,14 +101,21 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         while (ell < m && qs[ell] == qn[ell]) ++ell;
       }
       if (!err) {
+        // high halves of the insertion's draw words, as the helper waves
+        // compute them on the device
+        const uint32_t nload = (uint32_t)(Lq - h[cur][best]);
+        const uint32_t nfree = L.B - P.hdr->size;
+        const uint32_t nev = nload > nfree ? nload - nfree : 0u;
+        rwbuf.resize(nev ? nev : 1);
+        for (uint32_t d = 0; d < nev; ++d) rwbuf[d] = (uint32_t)(philox_word0(j, best, d, 0ull, C.seed, r) >> 32);
         InsertArgs ia;
         ia.seed = C.seed;
         ia.jg = j;
         ia.worker = best;
         ia.replica = r;
         ia.B = L.B;
-        ia.rn = 0;
-        ia.rw = nullptr;
+        ia.rn = nev;
+        ia.rw = rwbuf.data();
         ia.ready = nullptr;
         ia.ready_need = 0;
         err = rlt_insert(P, ia, qs, Lq, h[cur][best], ustage, path_of(best), nullptr);
@@ -131,4 +139,17 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) worker_stats(worker_ptrs(ws, L, r, i), out + (uint64_t)r * W + i);
   return 0;
+}
+
+// The draw index of the eviction blocks: from the high half of the word when
+// that decides it, else from the whole word.
+extern "C" uint32_t emul_draw_index(uint64_t r64, uint32_t n) {
+  uint32_t k = 0;
+  if (draw_index_hi((uint32_t)(r64 >> 32), n, k)) return k;
+  return (uint32_t)__umul64hi(r64, (uint64_t)n);
+}
+
+extern "C" int emul_draw_index_decided(uint64_t r64, uint32_t n) {
+  uint32_t k = 0;
+  return draw_index_hi((uint32_t)(r64 >> 32), n, k) ? 1 : 0;
 }

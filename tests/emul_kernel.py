@@ -40,6 +40,10 @@ def lib():
         _lib = ctypes.CDLL(build())
         _lib.emul_run.restype = ctypes.c_int
         _lib.emul_run.argtypes = [ctypes.POINTER(K.KvrConfig), ctypes.c_uint64] + [ctypes.c_void_p] * 9 + [ctypes.c_uint32]
+        _lib.emul_draw_index.restype = ctypes.c_uint32
+        _lib.emul_draw_index.argtypes = [ctypes.c_uint64, ctypes.c_uint32]
+        _lib.emul_draw_index_decided.restype = ctypes.c_int
+        _lib.emul_draw_index_decided.argtypes = [ctypes.c_uint64, ctypes.c_uint32]
     return _lib
 
 

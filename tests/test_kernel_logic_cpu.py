@@ -75,3 +75,28 @@ def test_candidate_staging_capacity(ucap):
         W = int(rng.integers(1, 4))
         B = int(max(s.max_len, rng.integers(10, 120)))
         _compare(s, 2, W, B, ucap=ucap, seed=case)
+
+
+def test_draw_index_from_high_half():
+    """The eviction blocks index U with floor(r * |U| / 2^64) from the high
+    32 bits of r when they decide it, and from the whole word otherwise: the
+    result must equal the full product for every word, including words whose
+    low half carries into the index."""
+    lib = E.lib()
+    rng = np.random.default_rng(77)
+    M = (1 << 64) - 1
+    for n in [1, 2, 3, 7, 96, 203, 4096, 8191, 262147, (1 << 31) + 11]:
+        words = [int(x) for x in rng.integers(0, 2**63, size=300, dtype=np.uint64)] + [0, M, 1 << 63]
+        # words whose high half puts r_hi * n just below a multiple of 2^32,
+        # with the largest low half: the carry case
+        for m in range(1, 40):
+            r_hi = ((m << 32) - 1) // n
+            for lo in (0, 1, (1 << 31), (1 << 32) - 1):
+                w = ((r_hi & 0xFFFFFFFF) << 32) | lo
+                words.append(w)
+        decided = 0
+        for w in words:
+            assert lib.emul_draw_index(w, n) == (w * n) >> 64, (hex(w), n)
+            decided += lib.emul_draw_index_decided(w, n)
+        if n <= 8192:
+            assert decided >= 300  # the random words are (almost surely) all decided
