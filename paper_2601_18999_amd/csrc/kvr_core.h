@@ -1265,7 +1265,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     uint32_t eoff;
     if (!arena_alloc(P, s, (uint32_t)nload, false, eoff)) goto fail;
     ar = arena_of(P, s.arena_sel);
-    for (int32_t k = lane_id(); k < nload; k += KVR_WAVE) ar[eoff + (uint32_t)k] = qs[h + k];
+    wave_copy(ar + eoff, qs + h, nload);
     wave_mem_sync();
     l = node_alloc(P, s);
     if (l < 0) goto fail;

@@ -70,11 +70,23 @@ __device__ __forceinline__ void count_matched(const Ptrs& P, int32_t h, int32_t*
 __device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, int32_t Ln, int32_t* qn,
                                            const int32_t* qc, int32_t Lc, uint32_t t0, uint32_t stride,
                                            int32_t* ell) {
+  constexpr int kUnroll = 8;  // loads in flight per thread
   int32_t m = Lc < Ln ? Lc : Ln;
-  for (uint32_t x = t0; x < (uint32_t)Ln; x += stride) {
-    const int32_t v = tokens[n0 + x];
-    qn[x] = v;
-    if ((int32_t)x < m && qc[x] != v) m = (int32_t)x;
+  for (uint32_t b = t0; b < (uint32_t)Ln; b += kUnroll * stride) {
+    int32_t v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t x = b + (uint32_t)u * stride;
+      v[u] = x < (uint32_t)Ln ? tokens[n0 + x] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t x = b + (uint32_t)u * stride;
+      if (x < (uint32_t)Ln) {
+        qn[x] = v[u];
+        if ((int32_t)x < m && qc[x] != v[u]) m = (int32_t)x;
+      }
+    }
   }
   // minimum over the wave, then one LDS atomic per wave
   for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
