@@ -1439,10 +1439,13 @@ fail:
 
 // ---------------------------------------------------------------- matching
 
-// First index k < n with e[k] != q[k], or n.  Eight wave-wide loads are in
-// flight per iteration (512 tokens on a 64-lane wave).
+// First index k < n with e[k] != q[k], or n.  KVR_MATCH_UNROLL wave-wide
+// loads are in flight per iteration (64 tokens each on a 64-lane wave).
+#ifndef KVR_MATCH_UNROLL
+#define KVR_MATCH_UNROLL 8
+#endif
 __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n) {
-  constexpr int kUnroll = 8;
+  constexpr int kUnroll = KVR_MATCH_UNROLL;
   for (int32_t b = 0; b < n; b += kUnroll * KVR_WAVE) {
     int32_t ev[kUnroll], qv[kUnroll];
 #pragma unroll
