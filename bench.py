@@ -59,7 +59,8 @@ def log(msg: str) -> None:
 
 def cpu_baseline(stream, W, B, budget_s: float):
     """The CPU oracle, single-threaded, on replica 0 of the same stream: the
-    first n queries, n doubled until one run takes at least budget_s / 2."""
+    first n queries, n grown until one run takes at least budget_s (the cost
+    per query grows as the caches fill, so the last steps grow by 1.4x)."""
     from oracle import oracle as O
     n = min(1000, stream.n)
     while True:
@@ -67,9 +68,9 @@ def cpu_baseline(stream, W, B, budget_s: float):
         O.run(stream, W, B, replica=0, n=n)
         dt = time.perf_counter() - t0
         log(f"cpu oracle: {n} queries in {dt:.1f} s")
-        if dt >= budget_s / 2 or n >= stream.n:
+        if dt >= budget_s or n >= stream.n:
             break
-        n = min(stream.n, 2 * n)
+        n = min(stream.n, int(n * (2.0 if dt < budget_s / 3 else 1.4)))
     return {"value": n / dt, "unit": "queries/s", "cores": 1, "kind": "oracle",
             "sample": f"replica 0, queries 0..{n} of the same stream, one thread, {dt:.1f} s"}
 
@@ -131,7 +132,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--batch", type=int, default=2000)
     ap.add_argument("--config", type=int, default=5)
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, copy this many MiB device to device with a plain "
