@@ -57,6 +57,7 @@
 #include <cstring>
 #include <deque>
 #include <map>
+#include <set>
 #include <vector>
 
 extern "C" {
@@ -70,7 +71,8 @@ typedef struct orc_config {
   uint64_t seed;              // Philox key word 0
   int32_t evict;              // 0 = RLT, 1 = L-LRU
   int32_t update;             // 0 = NLMS, 1 = RLS, 2 = none
-  int32_t u_mode;             // 0 = maintained ordered candidate list, 1 = recompute U at each draw
+  int32_t u_mode;             // 0 = maintained ordered candidate list (RLT) or ordered leaf set
+                              // (L-LRU), 1 = recompute U / scan every leaf at each eviction
   int32_t check;              // 1 = check invariants after every step
   double alpha_cached;        // s per 1k tokens (App. A: 0 ms per 1k tokens)
   double alpha_miss;          // s per 1k tokens (App. A: 1000 ms per 1k tokens)
@@ -169,7 +171,8 @@ struct Worker {
   std::vector<int32_t> free_ids;
   uint64_t size = 0;           // |S_i| in tokens
   uint32_t phase = 1, cnt = 0; // marking set T = {v : mark(v) == phase}, |T| = cnt
-  std::vector<int32_t> U;      // ordered candidate list (u_mode 0)
+  std::vector<int32_t> U;      // ordered candidate list (RLT, u_mode 0)
+  std::set<std::pair<uint64_t, int32_t>> lru_leaves;  // (stamp, id) of every leaf (L-LRU, u_mode 0)
   bool U_valid = false;
   double P = 0.0;              // estimated queue load
   double theta[4] = {0, 0, 0, 0};
@@ -348,36 +351,62 @@ void insert_rlt(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
   }
 }
 
-// L-LRU insertion: every access stamps the token; a miss with a full cache
-// evicts the leaf (other than the insertion point) with the oldest stamp.
+// L-LRU insertion (Sec. 3.2): every access stamps the token; a miss with a
+// full cache evicts the leaf (other than the insertion point) with the
+// oldest stamp.  Stamps (query index, position) are unique, so there are no
+// ties.  u_mode 1 scans every node for that leaf; u_mode 0 keeps the leaves
+// in a set ordered by stamp (the same leaf, found faster).
+void lru_set_stamp(Sim& s, Worker& w, int32_t id, uint64_t stamp) {
+  Node& n = w.nodes[id];
+  if (s.cfg.u_mode == 0 && id != 0 && n.kids.empty()) {
+    w.lru_leaves.erase({n.stamp, id});
+    w.lru_leaves.insert({stamp, id});
+  }
+  n.stamp = stamp;
+}
+
 void insert_lru(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
   Worker& w = s.w[i];
   const uint32_t B = s.cfg.cache_tokens;
+  const bool scan = s.cfg.u_mode == 1;
   int32_t u = 0;
   for (int32_t p = 0; p < L; ++p) {
     uint64_t stamp = (jg << 32) | (uint64_t)(uint32_t)p;
     auto it = w.nodes[u].kids.find(q[p]);
     if (it != w.nodes[u].kids.end()) {
       u = it->second;
-      w.nodes[u].stamp = stamp;
+      lru_set_stamp(s, w, u, stamp);
       continue;
     }
     if (w.size == B) {
       int32_t best = -1;
-      for (int32_t x = 1; x < (int32_t)w.nodes.size(); ++x) {
-        const Node& n = w.nodes[x];
-        if (!n.alive || !n.kids.empty() || x == u) continue;
-        if (best < 0 || n.stamp < w.nodes[best].stamp) best = x;
+      if (scan) {
+        for (int32_t x = 1; x < (int32_t)w.nodes.size(); ++x) {
+          const Node& n = w.nodes[x];
+          if (!n.alive || !n.kids.empty() || x == u) continue;
+          if (best < 0 || n.stamp < w.nodes[best].stamp) best = x;
+        }
+      } else {
+        for (auto jt = w.lru_leaves.begin(); jt != w.lru_leaves.end(); ++jt)
+          if (jt->second != u) {
+            best = jt->second;
+            break;
+          }
       }
       if (best < 0) {
         s.error |= 4;
         return;
       }
+      const int32_t par = w.nodes[best].parent;
+      if (!scan) w.lru_leaves.erase({w.nodes[best].stamp, best});
       remove_leaf(w, best);
+      if (!scan && par != 0 && w.nodes[par].kids.empty()) w.lru_leaves.insert({w.nodes[par].stamp, par});
       w.st.evictions += 1;
     }
+    if (!scan && u != 0 && w.nodes[u].kids.empty()) w.lru_leaves.erase({w.nodes[u].stamp, u});
     int32_t nv = new_node(w, q[p], u);
     w.nodes[nv].stamp = stamp;
+    if (!scan) w.lru_leaves.insert({stamp, nv});
     w.st.loads += 1;
     u = nv;
   }

@@ -152,9 +152,11 @@ def test_oracle_equals_bruteforce_model(evict, update):
                 assert ws["phase"] == sw.phase and ws["forced_resets"] == sw.forced
 
 
-def test_candidate_list_equals_definition():
-    """The maintained ordered candidate list gives the same run as
-    recomputing U from its definition at every draw."""
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_candidate_list_equals_definition(evict):
+    """The maintained ordered candidate list (RLT), or the leaf set ordered
+    by stamp (L-LRU), gives the same run as recomputing U from its
+    definition, or scanning every leaf, at each eviction."""
     rng = np.random.default_rng(5)
     for case in range(12):
         sp = small_spec(n=int(rng.integers(100, 250)), groups=int(rng.integers(2, 8)),
@@ -163,8 +165,8 @@ def test_candidate_list_equals_definition():
         s = generate(sp)
         W = int(rng.integers(1, 4))
         B = int(max(s.max_len, rng.integers(40, 300)))
-        a = O.run(s, W, B, replica=case, u_mode=0, all_hits=True)
-        b = O.run(s, W, B, replica=case, u_mode=1, all_hits=True)
+        a = O.run(s, W, B, replica=case, u_mode=0, all_hits=True, evict=evict)
+        b = O.run(s, W, B, replica=case, u_mode=1, all_hits=True, evict=evict)
         np.testing.assert_array_equal(a["route"], b["route"])
         np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
         assert a["workers"] == b["workers"]
