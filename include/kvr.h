@@ -16,7 +16,9 @@
  *      mark every token of the path, reset the marking set when it would
  *      exceed B, and evict a uniformly random unmarked leaf token before
  *      loading a missing token into a full cache (Eq. 3: no other cache
- *      changes).
+ *      changes); or, with evict = KVR_EVICT_LRU, with L-LRU (Sec. 3.2):
+ *      every access stamps the tokens of its path and the leaf token
+ *      accessed least recently is evicted.
  * Replicas see the same stream and differ only in the random key of RLT.
  *
  * Conventions
@@ -62,7 +64,7 @@ typedef enum kvr_status {
   KVR_ESTATE = -5     /* the context is in an error state */
 } kvr_status;
 
-enum { KVR_EVICT_RLT = 0, KVR_EVICT_LRU = 1 }; /* L-LRU on the device: not built yet */
+enum { KVR_EVICT_RLT = 0, KVR_EVICT_LRU = 1 }; /* L-LRU: Sec. 3.2; at most 2^32 - 1 queries per context */
 enum { KVR_ROUTE_LBGR = 0 };
 enum { KVR_UPD_NLMS = 0, KVR_UPD_RLS = 1, KVR_UPD_NONE = 2 };
 

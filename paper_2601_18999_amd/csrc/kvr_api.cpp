@@ -63,9 +63,7 @@ kvr_status validate(const kvr_config* c) {
     return fail(KVR_EINVAL, "max_query_tokens must be in 1..cache_tokens");
   if (c->max_query_tokens > 16384)
     return fail(KVR_EINVAL, "max_query_tokens above 16384 does not fit the LDS query buffers");
-  if (c->evict == KVR_EVICT_LRU)
-    return fail(KVR_EINVAL, "L-LRU eviction is not built on the device (RLT only)");
-  if (c->evict != KVR_EVICT_RLT) return fail(KVR_EINVAL, "unknown evict policy");
+  if (c->evict != KVR_EVICT_RLT && c->evict != KVR_EVICT_LRU) return fail(KVR_EINVAL, "unknown evict policy");
   if (c->router != KVR_ROUTE_LBGR) return fail(KVR_EINVAL, "unknown router");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
@@ -230,6 +228,8 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens, co
   if (n == 0) return KVR_OK;
   if (!d_tokens || !d_offsets || !d_arrival_us) return fail(KVR_EINVAL, "tokens, offsets and arrival_us are required");
   if (n > (1u << 30)) return fail(KVR_EINVAL, "batch too large");
+  if (ctx->C.evict == KVR_EVICT_LRU && ctx->queries_done + n > 0xffffffffull)
+    return fail(KVR_EINVAL, "L-LRU access stamps hold 32-bit query indices: at most 2^32 - 1 queries per context");
   kvr::StepArgs a;
   a.ws = ctx->ws;
   a.L = ctx->L;

@@ -112,6 +112,7 @@ struct Ptrs {
   int32_t* U;
   PendRec* pend;
   uint64_t* scratch;
+  int32_t* stamp0;  // L-LRU: last access of each arena word (semispace 1 at + A); null for RLT
   uint32_t A, NC, PC;
 };
 
@@ -125,6 +126,7 @@ __device__ __forceinline__ Ptrs worker_ptrs(char* ws, const Layout& L, uint32_t 
   P.U = reinterpret_cast<int32_t*>(ws + L.off_U + w * L.leaf_stride);
   P.pend = reinterpret_cast<PendRec*>(ws + L.off_pend + w * L.pend_stride);
   P.scratch = reinterpret_cast<uint64_t*>(ws + L.off_scratch + w * L.scratch_stride);
+  P.stamp0 = L.off_stamp < L.total ? reinterpret_cast<int32_t*>(ws + L.off_stamp + w * L.arena_stride) : nullptr;
   P.A = L.A;
   P.NC = L.NC;
   P.PC = L.PC;
@@ -396,7 +398,7 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t v) {
 // caller's cache state never has to live in memory.  Returns the new arena
 // top, or ~0 when the live data does not fit.
 __device__ __noinline__ uint64_t collect_arena(NodeRec* nodes, const int32_t* src, int32_t* dst, uint32_t hwm,
-                                               uint32_t A) {
+                                               uint32_t A, const int32_t* ssrc, int32_t* sdst) {
   uint64_t top = 0;
   // sizes first: the live data must fit
   for (uint32_t b = 0; b < hwm; b += KVR_WAVE) {
@@ -437,6 +439,7 @@ __device__ __noinline__ uint64_t collect_arena(NodeRec* nodes, const int32_t* sr
       const uint32_t dO = (uint32_t)__builtin_amdgcn_readlane((int)noff, j);
       const uint32_t dC = (uint32_t)__builtin_amdgcn_readlane((int)ncoff, j);
       wave_copy(dst + dO, src + so, sl);
+      if (ssrc) wave_copy(sdst + dO, ssrc + so, sl);
       if (snc > 0) wave_copy(dst + dC, src + sc, 2 * snc);
     }
     if (live) {
@@ -450,7 +453,10 @@ __device__ __noinline__ uint64_t collect_arena(NodeRec* nodes, const int32_t* sr
 }
 
 __device__ __forceinline__ bool collect(const Ptrs& P, St& s) {
-  const uint64_t top = collect_arena(P.nodes, arena_of(P, s.arena_sel), arena_of(P, s.arena_sel ^ 1u), s.hwm, P.A);
+  const uint64_t top =
+      collect_arena(P.nodes, arena_of(P, s.arena_sel), arena_of(P, s.arena_sel ^ 1u), s.hwm, P.A,
+                    P.stamp0 ? P.stamp0 + (size_t)s.arena_sel * P.A : nullptr,
+                    P.stamp0 ? P.stamp0 + (size_t)(s.arena_sel ^ 1u) * P.A : nullptr);
   if (top == ~0ull) return false;
   s.arena_sel ^= 1u;
   s.arena_top = (uint32_t)top;
@@ -1438,6 +1444,246 @@ fail:
 }
 
 // ---------------------------------------------------------------- matching
+
+// ---------------------------------------------------------------- L-LRU
+
+// L-LRU (Sec. 3.2): every access stamps the tokens of its path with the
+// global query index; a miss in a full cache evicts the leaf token accessed
+// least recently.  One query's path holds at most one leaf token, so no two
+// leaf tokens share a stamp and the stamp alone orders them.  Along an edge
+// the stamps never increase with depth (an access covers a prefix), so once
+// a leaf's tail token is the least recent, the tokens above it with the same
+// stamp follow it in the eviction order: they go as one segment.
+
+// Index in the leaf list of the leaf whose last token has the oldest stamp,
+// skipping node `excl`; -1 if there is none.
+__device__ __forceinline__ int32_t lru_pick(const Ptrs& P, const St& s, const int32_t* st, int32_t excl) {
+  constexpr int kUnroll = 4;
+  uint64_t best = ~0ull;  // (stamp << 32) | list index
+  for (uint32_t b = 0; b < s.nleaves; b += kUnroll * KVR_WAVE) {
+    int32_t id[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      id[v] = k < s.nleaves ? P.leaf[k] : -1;
+      if (id[v] == excl || (uint32_t)id[v] >= s.hwm) id[v] = -1;
+    }
+    NodeRec nd[kUnroll];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v)
+      if (id[v] > 0) nd[v] = P.nodes[id[v]];
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();
+      if (id[v] > 0 && nd[v].len > 0) {
+        const uint64_t key = ((uint64_t)(uint32_t)st[nd[v].off + (uint32_t)(nd[v].len - 1)] << 32) | k;
+        best = key < best ? key : best;
+      }
+    }
+  }
+  best = wave_min_u64(best);
+  return best == ~0ull ? -1 : (int32_t)(uint32_t)best;
+}
+
+// Number of tokens at the end of the edge [off, off+len) stamped j, at most cap.
+__device__ __forceinline__ int32_t lru_segment(const int32_t* st, uint32_t off, int32_t len, uint32_t j, int32_t cap) {
+  int32_t c = 0;
+  while (c < len && c < cap) {
+    const int32_t k = len - 1 - c - lane_id();
+    const uint64_t m = __ballot(k < 0 || (uint32_t)st[off + (uint32_t)(k < 0 ? 0 : k)] != j);
+    if (m) {
+      c += first_lane(m);
+      break;
+    }
+    c += KVR_WAVE;
+  }
+  c = c < len ? c : len;
+  return c < cap ? c : cap;
+}
+
+// Stamp positions [0, n) of the edge at arena offset off with j.
+__device__ __forceinline__ void lru_stamp(int32_t* st, uint32_t off, int32_t n, uint32_t j) {
+  for (int32_t k = lane_id(); k < n; k += KVR_WAVE) st[off + (uint32_t)k] = (int32_t)j;
+}
+
+// L-LRU insertion of q[0, L) into the worker's cache (the oracle's insertion
+// loop with the evictions taken before the loads: loaded tokens and the
+// insertion point carry the current stamp, the newest, so they are never the
+// least recent leaf and the evicted tokens are the same).  h and pr as for
+// rlt_insert.  Returns the KVR_DEV_* error bits.
+__device__ __forceinline__ uint32_t lru_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
+                                               int32_t h, const PathRef& pr, int64_t* dbg) {
+  St s = load_st(P.hdr);
+  const uint32_t B = ia.B;
+  const uint32_t jq = (uint32_t)ia.jg;
+  int32_t* ar = arena_of(P, s.arena_sel);
+  int32_t* st = P.stamp0 + (size_t)s.arena_sel * P.A;
+  const int32_t pc = *pr.cnt;
+  const bool have_path = pc <= kPathMax;
+  bool split = false;
+  int32_t a = 0, l = 0, laststart = 0, pe = 0;
+  int32_t x = 0, d = 0, last = 0, lastcov = 0;
+
+  // ---- walk the cached part of the path, stamping it
+  while (d < h) {
+    int32_t c;
+    if (have_path) {
+      if (pe >= pc || pr.start[pe] != d) {
+        KVR_FAIL_CHECK(s, 21, pe, d, h);
+        goto fail;
+      }
+      c = pr.node[pe++];
+    } else {
+      NodeRec nx = P.nodes[x];
+      c = child_find(ar, nx, qs[d]);
+    }
+    if (c <= 0 || (uint32_t)c >= s.hwm) {
+      KVR_FAIL_CHECK(s, 21, c, d, h);
+      goto fail;
+    }
+    const NodeRec nc = P.nodes[c];
+    const int32_t cov = nc.len < h - d ? nc.len : h - d;
+    if (cov <= 0) {
+      KVR_FAIL_CHECK(s, 22, c, nc.len, d);
+      goto fail;
+    }
+    lru_stamp(st, nc.off, cov, jq);
+    laststart = d;
+    d += cov;
+    last = c;
+    lastcov = cov;
+    x = c;
+  }
+  wave_mem_sync();
+
+  if (h < L) {
+    const int32_t nload = L - h;
+    // ---- attachment point: end of `last`, splitting it if needed
+    a = last;
+    if (h > 0) {
+      const NodeRec nl = P.nodes[last];
+      if (lastcov < nl.len) {
+        a = split_node(P, s, last, lastcov);
+        if (a < 0) goto fail;
+        split = true;
+      }
+    }
+    // ---- the new leaf holding q[h, L), stamped; it takes the list slot of
+    // the attachment point when that was a leaf, else a new one
+    int32_t pos = (int32_t)s.nleaves;
+    bool replace = false;
+    {
+      const NodeRec na = P.nodes[a];
+      if (a != 0 && na.nchild == 0) {
+        pos = arr_find(P.leaf, s.nleaves, a);
+        replace = true;
+        if (pos < 0) {
+          KVR_FAIL_CHECK(s, 23, a, s.nleaves, 0);
+          goto fail;
+        }
+      }
+    }
+    uint32_t eoff;
+    if (!arena_alloc(P, s, (uint32_t)nload, false, eoff)) goto fail;
+    ar = arena_of(P, s.arena_sel);
+    st = P.stamp0 + (size_t)s.arena_sel * P.A;
+    wave_copy(ar + eoff, qs + h, nload);
+    lru_stamp(st, eoff, nload, jq);
+    wave_mem_sync();
+    l = node_alloc(P, s);
+    if (l < 0) goto fail;
+    {
+      NodeRec nl;
+      nl.parent = a;
+      nl.off = eoff;
+      nl.len = nload;
+      nl.nchild = 0;
+      nl.coff = 0;
+      nl.ccap = 0;
+      nl.mphase = 0;
+      nl.ma = 0;
+      node_put(P, l, nl);
+    }
+    if (!child_add(P, s, a, qs[h], l)) goto fail;
+    ar = arena_of(P, s.arena_sel);
+    st = P.stamp0 + (size_t)s.arena_sel * P.A;
+    if (lane_id() == 0) P.leaf[pos] = l;
+    if (!replace) s.nleaves += 1;
+    wave_mem_sync();
+
+    // ---- evictions: whole stamp segments of the least recent leaf
+    const uint32_t nfree = B - s.size;
+    const uint32_t nev = (uint32_t)nload > nfree ? (uint32_t)nload - nfree : 0u;
+    uint32_t rem = nev;
+    while (rem > 0) {
+      const int32_t li = lru_pick(P, s, st, l);
+      if (li < 0) {
+        KVR_FAIL_CHECK(s, 24, rem, s.nleaves, L);
+        goto fail;
+      }
+      const int32_t v = P.leaf[li];
+      const NodeRec nv = P.nodes[v];
+      if (nv.nchild != 0 || nv.len <= 0 || nv.parent < 0) {
+        KVR_FAIL_CHECK(s, 25, v, nv.nchild, nv.len);
+        goto fail;
+      }
+      const uint32_t jv = (uint32_t)st[nv.off + (uint32_t)(nv.len - 1)];
+      const int32_t t = lru_segment(st, nv.off, nv.len, jv, (int32_t)rem);
+      if (t <= 0) {
+        KVR_FAIL_CHECK(s, 26, v, nv.len, (int64_t)jv);
+        goto fail;
+      }
+      rem -= (uint32_t)t;
+      if (t < nv.len) {
+        if (lane_id() == 0) P.nodes[v].len = nv.len - t;
+      } else {
+        // the node empties: drop it; its parent, if now a leaf, takes its slot
+        const int32_t pv = nv.parent;
+        if (!child_remove(P, s, pv, v)) {
+          KVR_FAIL_CHECK(s, 27, v, pv, 0);
+          goto fail;
+        }
+        node_free(P, s, v);
+        const NodeRec np = P.nodes[pv];
+        if (pv != 0 && np.nchild == 0) {
+          if (lane_id() == 0) P.leaf[li] = pv;
+        } else {
+          const int32_t lastid = P.leaf[s.nleaves - 1];
+          if (lane_id() == 0) P.leaf[li] = lastid;
+          s.nleaves -= 1;
+        }
+      }
+      wave_mem_sync();
+    }
+    s.size = s.size + (uint32_t)nload - nev;
+    s.loads += (uint64_t)nload;
+    s.evictions += nev;
+  }
+  store_st(P.hdr, s);
+  wave_mem_sync();
+  {
+    int32_t fc = have_path ? pe : kPathMax + 1;
+    if (fc <= kPathMax) {
+      if (split) {
+        int32_t f1 = fc - 1;
+        path_add(pr, f1, a, laststart, laststart + lastcov);
+      }
+      if (h < L) path_add(pr, fc, l, h, L);
+    }
+    if (lane_id() == 0) *pr.cnt = fc;
+  }
+  return 0;
+fail:
+  if (lane_id() == 0) *pr.cnt = kPathMax + 1;
+  store_st(P.hdr, s);
+  if (dbg) {
+    dbg[0] = s.dbg_check;
+    dbg[1] = s.dbg_val[0];
+    dbg[2] = s.dbg_val[1];
+    dbg[3] = s.dbg_val[2];
+  }
+  return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
 
 // First index k < n with e[k] != q[k], or n.  KVR_MATCH_UNROLL wave-wide
 // loads are in flight per iteration (64 tokens each on a 64-lane wave).

@@ -243,7 +243,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     if (abort_sh) break;
     const uint32_t best = (uint32_t)best_sh;
     const uint32_t nev = nev_sh;
-    const uint32_t rn = nev < a.rcap ? nev : a.rcap;
+    // draw words: RLT only
+    const uint32_t rn = a.C.evict == KVR_EVICT_RLT ? (nev < a.rcap ? nev : a.rcap) : 0u;
     const int32_t ell = ell_sh[cur];
 
     // ---- phase B.  Wave 0: RLT insertion.  Helpers: the insertion's draw
@@ -262,10 +263,12 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.B = a.L.B;
       ia.rn = rn;
       ia.rw = rw;
-      ia.ready = nh ? &wready_sh : nullptr;
+      ia.ready = nh && rn ? &wready_sh : nullptr;
       ia.ready_need = nh;
       int64_t dbg[4] = {0, 0, 0, 0};
-      const uint32_t err = rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, paths.of(best), dbg);
+      const uint32_t err = a.C.evict == KVR_EVICT_RLT
+                               ? rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, paths.of(best), dbg)
+                               : lru_insert(P, ia, qs, Lq, h_sh[cur][best], paths.of(best), dbg);
       if (lane == 0 && err) {
         if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];

@@ -17,6 +17,8 @@
 //   pending rings   completion records (FIFO per worker)
 //   scratch         stack for the digest walk of kvr_stats
 //   stats out       kvr_worker_stats staging for kvr_stats
+//   stamps          (L-LRU only) last access of every edge token, laid out
+//                   like the arenas
 #ifndef KVR_LAYOUT_H
 #define KVR_LAYOUT_H
 
@@ -107,7 +109,7 @@ struct Layout {
   uint32_t R, W, B, maxL, NC, A, PC;
   uint32_t pad0;
   uint64_t off_global, off_rhdr, off_whdr, off_nodes, off_arena, off_leaf, off_U, off_pend,
-      off_scratch, off_stats, total;
+      off_scratch, off_stats, off_stamp, total;
   uint64_t node_stride, arena_stride, leaf_stride, pend_stride, scratch_stride;
 };
 
@@ -181,6 +183,10 @@ inline Layout make_layout(const kvr_config& c) {
   o += RW * L.scratch_stride;
   L.off_stats = o;
   o = align_up(o + RW * sizeof(kvr_worker_stats), 256);
+  // L-LRU only: the last access (global query index) of every edge token,
+  // at the same offsets as the tokens in both semispaces
+  L.off_stamp = o;
+  if (c.evict == KVR_EVICT_LRU) o += RW * L.arena_stride;
   L.total = o;
   return L;
 }

@@ -118,7 +118,8 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.rw = rwbuf.data();
         ia.ready = nullptr;
         ia.ready_need = 0;
-        err = rlt_insert(P, ia, qs, Lq, h[cur][best], ustage, path_of(best), nullptr);
+        err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lq, h[cur][best], ustage, path_of(best), nullptr)
+                                       : lru_insert(P, ia, qs, Lq, h[cur][best], path_of(best), nullptr);
       }
       if (err) return (int)err;
       if (has_next) {

@@ -35,7 +35,7 @@ def test_config_default_holds_paper_constants():
 
 BAD = [
     dict(num_workers=0), dict(num_workers=65), dict(cache_tokens=0), dict(max_query_tokens=0),
-    dict(max_query_tokens=1001), dict(evict=K.KVR_EVICT_LRU), dict(evict=7), dict(router=3),
+    dict(max_query_tokens=1001), dict(evict=7), dict(router=3),
     dict(update=9), dict(pending_capacity=0), dict(node_capacity=1), dict(arena_words=10),
     dict(rho=0.0), dict(rho=1.5), dict(rho=math.nan), dict(decay_interval_us=0), dict(lr=-1.0),
     dict(lr=math.inf), dict(nlms_eps=-1.0), dict(rls_p0=0.0), dict(alpha_miss=math.nan),

@@ -10,11 +10,12 @@ from oracle import oracle as O
 from workload import PRESETS, generate, small_spec
 
 
-def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, **cfg):
-    e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, ucap=ucap, **cfg)
+def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", **cfg):
+    e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, ucap=ucap,
+              evict={"rlt": 0, "lru": 1}[evict], **cfg)
     assert e["rc"] == 0
     for r in range(R):
-        o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed)
+        o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict)
         np.testing.assert_array_equal(e["route"][r], o["route"])
         np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
         for i in range(W):
@@ -100,3 +101,30 @@ def test_draw_index_from_high_half():
             decided += lib.emul_draw_index_decided(w, n)
         if n <= 8192:
             assert decided >= 300  # the random words are (almost surely) all decided
+
+
+@pytest.mark.parametrize("block", range(3))
+def test_lru_random_instances(block):
+    """L-LRU on the compressed tree (stamp segments, unordered leaf list)
+    against the oracle's per-token L-LRU."""
+    rng = np.random.default_rng(500 + block)
+    for case in range(40):
+        vocab = int(rng.integers(2, 12))
+        sp = small_spec(n=int(rng.integers(20, 160)), groups=int(rng.integers(1, 8)),
+                        prefix_len=(1, int(rng.integers(2, 30))), suffix_len=(1, int(rng.integers(2, 20))),
+                        vocab=vocab, seed=3000 * block + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 5))
+        B = int(max(s.max_len, rng.integers(2, 150)))
+        e = _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case, evict="lru")
+        # no randomness: every replica is the same
+        np.testing.assert_array_equal(e["route"][0], e["route"][1])
+
+
+def test_lru_collector_and_presets():
+    s = generate(small_spec(n=400, groups=6, prefix_len=(10, 70), suffix_len=(5, 50), vocab=30))
+    W, B = 3, 320
+    e = _compare(s, 1, W, B, evict="lru", arena_words=B + 2 * s.max_len + 100)
+    assert sum(w["gc_runs"] for w in e["workers"][0]) > 20
+    p = PRESETS[2]
+    _compare(generate(p["stream"]).head(3000), 1, p["W"], p["B"], evict="lru")
