@@ -25,22 +25,24 @@ from gpu_helpers import compare_worker, note
 pytestmark = pytest.mark.gpu
 
 BATCH = 2000
-# (config, sampled replicas, prefix compared with the oracle)
+# (config, sampled replicas, prefix compared with the oracle, eviction)
 CASES = [
-    (3, [0, 85, 170, 255], 24000),
-    (4, [0, 42, 127], 24000),
-    (5, [0, 31], 8000),
+    (3, [0, 85, 170, 255], 24000, "rlt"),
+    (4, [0, 42, 127], 24000, "rlt"),
+    (5, [0, 31], 8000, "rlt"),
+    (3, [0, 255], 24000, "lru"),
+    (5, [0, 31], 8000, "lru"),
 ]
 
 
-def _oracle_many(stream, W, B, replicas, n):
+def _oracle_many(stream, W, B, replicas, n, evict):
     with cf.ThreadPoolExecutor(max_workers=len(replicas)) as ex:
-        futs = {r: ex.submit(O.run, stream, W, B, replica=r, n=n, all_hits=True) for r in replicas}
+        futs = {r: ex.submit(O.run, stream, W, B, replica=r, n=n, all_hits=True, evict=evict) for r in replicas}
         return {r: f.result() for r, f in futs.items()}
 
 
-@pytest.mark.parametrize("cfg,replicas,nprefix", CASES, ids=[f"config{c[0]}" for c in CASES])
-def test_full_size(cfg, replicas, nprefix):
+@pytest.mark.parametrize("cfg,replicas,nprefix,evict", CASES, ids=[f"config{c[0]}-{c[3]}" for c in CASES])
+def test_full_size(cfg, replicas, nprefix, evict):
     p = PRESETS[cfg]
     R, W, B = p["R"], p["W"], p["B"]
     t0 = time.time()
@@ -50,9 +52,9 @@ def test_full_size(cfg, replicas, nprefix):
 
     # the oracle runs on host threads while the GPU works
     pool = cf.ThreadPoolExecutor(max_workers=1)
-    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix)
+    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix, evict)
 
-    sim = K.Simulator(R, W, B, s.max_len)
+    sim = K.Simulator(R, W, B, s.max_len, evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict])
     try:
         ds = sim.upload(s)
         route = np.empty((R, s.n), np.int32)
@@ -96,7 +98,9 @@ def test_full_size(cfg, replicas, nprefix):
     ev = sum(w["evictions"] for w in orc[replicas[0]]["workers"])
     ph = sum(w["phase"] - 1 for w in orc[replicas[0]]["workers"])
     note(f"  oracle replica {replicas[0]}: {ev} evictions, {ph} phase resets in the prefix")
-    assert ev > 10 * B and ph > 0, (ev, ph)  # the prefix runs deep into eviction
+    assert ev > 10 * B and (ph > 0 or evict == "lru"), (ev, ph)  # the prefix runs deep into eviction
+    if evict == "lru":  # no randomness: every replica is the same over the whole stream
+        assert (route == route[0:1]).all() and (hits == hits[0:1]).all()
 
     # ---- whole stream: properties
     lens = s.lengths.astype(np.int64)

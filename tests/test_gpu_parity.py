@@ -196,3 +196,56 @@ def test_capacity_errors_are_reported():
     st, bits = sim.check()
     assert st == K.KVR_ECAPACITY and bits & 16
     sim.close()
+
+
+# ---------------------------------------------------------------- L-LRU
+
+LRU = dict(evict=K.KVR_EVICT_LRU)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_lru_small_random_parity(case):
+    rng = np.random.default_rng(700 + case)
+    vocab = int(rng.integers(2, 40))
+    sp = small_spec(n=int(rng.integers(60, 400)), groups=int(rng.integers(1, 9)),
+                    prefix_len=(1, int(rng.integers(3, 90))), suffix_len=(1, int(rng.integers(2, 70))),
+                    vocab=vocab, seed=50 + case)
+    s = generate(sp)
+    W = int(rng.integers(1, 7))
+    B = int(max(s.max_len, rng.integers(2, 600)))
+    upd = ["nlms", "rls", "none"][case % 3]
+    note(f"lru case {case}: W={W} B={B} n={s.n} vocab={vocab} update={upd}")
+    res, stats = gpu_run(s, 3, W, B, update=upd, seed=case, **LRU)
+    assert_parity(s, res, stats, W, B, range(3), update=upd, seed=case, evict="lru")
+    for r in range(1, 3):  # no randomness in L-LRU: the replicas are identical
+        np.testing.assert_array_equal(res["route"][0], res["route"][r])
+
+
+def test_lru_collector_under_small_arena():
+    s = generate(small_spec(n=500, groups=6, prefix_len=(10, 70), suffix_len=(5, 50), vocab=30))
+    W, B = 3, 320
+    res, stats = gpu_run(s, 2, W, B, arena_words=B + 2 * s.max_len + 100, **LRU)
+    assert sum(w["gc_runs"] for rr in stats for w in rr) > 20
+    assert_parity(s, res, stats, W, B, range(2), evict="lru")
+
+
+def test_lru_theorem1_worst_case():
+    """Theorem 1 construction: B-L+2 paths with a shared (L-1)-token prefix
+    queried cyclically; L-LRU misses the last token of every query once
+    the cache is full."""
+    for B, L in [(10, 4), (33, 7), (64, 2)]:
+        n = B - L + 2
+        prefix = list(range(1000, 1000 + L - 1))
+        paths = [prefix + [k] for k in range(n)]
+        s = generate({"kind": "paths", "paths": paths, "order": list(range(n)) * 6})
+        res, stats = gpu_run(s, 2, 1, B, **LRU)
+        assert res["status"] == K.KVR_OK
+        assert (res["hits"][:, n:] == L - 1).all()
+        assert stats[0][0]["evictions"] == 6 * n - n + 1
+
+
+def test_lru_config2_full():
+    p = PRESETS[2]
+    s = generate(p["stream"])
+    res, stats = gpu_run(s, 4, p["W"], p["B"], batch=2500, **LRU)
+    assert_parity(s, res, stats, p["W"], p["B"], [0, 3], evict="lru")
