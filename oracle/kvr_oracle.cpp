@@ -84,6 +84,12 @@ typedef struct orc_config {
   int64_t true_cached_us;     // observed-latency model, us per cached token
   int64_t true_miss_us;       // us per missed token
   int64_t true_out_us;        // us per output token
+  // routing (Sec. 5 "Baselines"): 0 = LBGR, 1 = random, 2 = round robin,
+  // 3 = cache-aware (highest hit or least loaded, by a load-balance threshold)
+  int32_t router;
+  int32_t ca_balance_abs;     // cache-aware: imbalance when max - min in-flight > this ...
+  double ca_balance_rel;      // ... and max > this * min
+  double ca_cache_threshold;  // cache-aware: best hit / |q| above this routes to the best hit
 } orc_config;
 
 typedef struct orc_worker_stats {
@@ -506,6 +512,34 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int64_t t, int32_t o
     phis[4 * i + 2] = x3;
     phis[4 * i + 3] = x4;
     if (i == 0 || eh < ehat[best]) best = i;
+  }
+  // 4'. the baseline routers of Sec. 5 replace the LBGR choice
+  if (c.router == 1) {
+    // random: a uniform worker from word 0 of Philox4x64-10, key
+    // (seed, replica), counter (query index, 0, 0, 1)
+    const uint64_t ctr[4] = {jg, 0, 0, 1}, key[2] = {c.seed, s.replica};
+    uint64_t out[4];
+    philox4x64_10(ctr, key, out);
+    best = (uint32_t)(((unsigned __int128)out[0] * W) >> 64);
+  } else if (c.router == 2) {
+    // round robin over the global query index
+    best = (uint32_t)(jg % W);
+  } else if (c.router == 3) {
+    // cache-aware: in-flight load = queries routed and not completed by t
+    uint32_t lo = 0, hi = 0, hmax = 0, small = 0;
+    for (uint32_t i = 1; i < W; ++i) {
+      if (s.w[i].pend.size() < s.w[lo].pend.size()) lo = i;
+      if (s.w[i].pend.size() > s.w[hi].pend.size()) hi = i;
+      if (h[i] > h[hmax]) hmax = i;
+      if (s.w[i].size < s.w[small].size) small = i;
+    }
+    const uint64_t lmin = s.w[lo].pend.size(), lmax = s.w[hi].pend.size();
+    if (lmax - lmin > (uint64_t)c.ca_balance_abs && (double)lmax > c.ca_balance_rel * (double)lmin)
+      best = lo;  // imbalanced: the least loaded
+    else if ((double)h[hmax] > c.ca_cache_threshold * (double)L)
+      best = hmax;  // the highest hit
+    else
+      best = small;  // low hits everywhere: the emptiest cache
   }
   // 5. commit: load increment, observed latency, pending completion
   Worker& w = s.w[best];

@@ -40,6 +40,10 @@ class OrcConfig(ctypes.Structure):
         ("true_cached_us", ctypes.c_int64),
         ("true_miss_us", ctypes.c_int64),
         ("true_out_us", ctypes.c_int64),
+        ("router", ctypes.c_int32),
+        ("ca_balance_abs", ctypes.c_int32),
+        ("ca_balance_rel", ctypes.c_double),
+        ("ca_cache_threshold", ctypes.c_double),
     ]
 
 
@@ -88,7 +92,10 @@ DEFAULTS: Dict[str, Any] = dict(
     seed=0, evict="rlt", update="nlms", u_mode=0, check=0,
     alpha_cached=0.0, alpha_miss=1.0, rho=31.0 / 32.0, decay_interval_us=20000,
     lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
-    true_cached_us=0, true_miss_us=1000, true_out_us=10000)
+    true_cached_us=0, true_miss_us=1000, true_out_us=10000,
+    router="lbgr", ca_balance_abs=32, ca_balance_rel=1.0001, ca_cache_threshold=0.5)
+
+ROUTER = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
 
 
 def make_config(W: int, B: int, **kw) -> OrcConfig:
@@ -106,6 +113,10 @@ def make_config(W: int, B: int, **kw) -> OrcConfig:
         setattr(c, f, float(p[f]))
     for f in ("decay_interval_us", "true_cached_us", "true_miss_us", "true_out_us"):
         setattr(c, f, int(p[f]))
+    c.router = ROUTER[p["router"]] if isinstance(p["router"], str) else int(p["router"])
+    c.ca_balance_abs = int(p["ca_balance_abs"])
+    c.ca_balance_rel = float(p["ca_balance_rel"])
+    c.ca_cache_threshold = float(p["ca_cache_threshold"])
     return c
 
 
