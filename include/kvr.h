@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 1u
+#define KVR_ABI_VERSION 2u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -65,7 +65,14 @@ typedef enum kvr_status {
 } kvr_status;
 
 enum { KVR_EVICT_RLT = 0, KVR_EVICT_LRU = 1 }; /* L-LRU: Sec. 3.2; at most 2^32 - 1 queries per context */
-enum { KVR_ROUTE_LBGR = 0 };
+/* Routers: LBGR (Algorithm 2) and the baselines of Sec. 5: uniformly random
+ * (word 0 of Philox4x64-10, key (seed, replica), counter (query index, 0, 0,
+ * 1), times W, high 64 bits), round robin over the global query index, and
+ * cache-aware: the least loaded worker (fewest queries in flight) when the
+ * loads are imbalanced, else the highest hit when its share of the query
+ * exceeds a threshold, else the worker with the fewest cached tokens; ties
+ * go to the lowest index. */
+enum { KVR_ROUTE_LBGR = 0, KVR_ROUTE_RANDOM = 1, KVR_ROUTE_ROUND_ROBIN = 2, KVR_ROUTE_CACHE_AWARE = 3 };
 enum { KVR_UPD_NLMS = 0, KVR_UPD_RLS = 1, KVR_UPD_NONE = 2 };
 
 /* Device status bits (kvr_check reports the first one as a kvr_status). */
@@ -104,6 +111,10 @@ typedef struct kvr_config {
   int64_t true_cached_us;    /* observed-latency model: us per cached token (0)    */
   int64_t true_miss_us;      /* us per missed token (1000)                         */
   int64_t true_out_us;       /* us per output token (10000)                        */
+  int32_t ca_balance_abs;    /* cache-aware: imbalanced when max - min in flight > this (32) */
+  int32_t pad0;
+  double ca_balance_rel;     /* ... and max > this * min (1.0001)                  */
+  double ca_cache_threshold; /* cache-aware: highest hit / |q| above this (0.5)    */
 } kvr_config;
 
 /* Final per-(replica, worker) state and counters (kvr_stats). */

@@ -19,9 +19,9 @@ KVR_OK, KVR_EINVAL, KVR_ENOMEM, KVR_EDEVICE, KVR_ECAPACITY, KVR_ESTATE = 0, -1, 
 STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVICE",
                 -4: "KVR_ECAPACITY", -5: "KVR_ESTATE"}
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
-KVR_ROUTE_LBGR = 0
+KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 1
+KVR_ABI_VERSION = 2
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
@@ -52,6 +52,10 @@ class KvrConfig(ctypes.Structure):
         ("true_cached_us", ctypes.c_int64),
         ("true_miss_us", ctypes.c_int64),
         ("true_out_us", ctypes.c_int64),
+        ("ca_balance_abs", ctypes.c_int32),
+        ("pad0", ctypes.c_int32),
+        ("ca_balance_rel", ctypes.c_double),
+        ("ca_cache_threshold", ctypes.c_double),
     ]
 
 

@@ -64,7 +64,10 @@ kvr_status validate(const kvr_config* c) {
   if (c->max_query_tokens > 16384)
     return fail(KVR_EINVAL, "max_query_tokens above 16384 does not fit the LDS query buffers");
   if (c->evict != KVR_EVICT_RLT && c->evict != KVR_EVICT_LRU) return fail(KVR_EINVAL, "unknown evict policy");
-  if (c->router != KVR_ROUTE_LBGR) return fail(KVR_EINVAL, "unknown router");
+  if (c->router < KVR_ROUTE_LBGR || c->router > KVR_ROUTE_CACHE_AWARE) return fail(KVR_EINVAL, "unknown router");
+  if (c->router == KVR_ROUTE_CACHE_AWARE &&
+      (c->ca_balance_abs < 0 || !(c->ca_balance_rel >= 0.0) || !(c->ca_cache_threshold >= 0.0)))
+    return fail(KVR_EINVAL, "cache-aware thresholds must be >= 0");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
   if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
@@ -127,6 +130,10 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->seed = 0;
   c->evict = KVR_EVICT_RLT;
   c->router = KVR_ROUTE_LBGR;
+  c->ca_balance_abs = 32;
+  c->pad0 = 0;
+  c->ca_balance_rel = 1.0001;
+  c->ca_cache_threshold = 0.5;
   c->update = KVR_UPD_NLMS;
   c->pending_capacity = 65536;
   c->node_capacity = 0;
@@ -204,6 +211,10 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   c->C.true_out_us = cfg->true_out_us;
   c->C.update = cfg->update;
   c->C.evict = cfg->evict;
+  c->C.router = cfg->router;
+  c->C.ca_balance_abs = cfg->ca_balance_abs;
+  c->C.ca_balance_rel = cfg->ca_balance_rel;
+  c->C.ca_cache_threshold = cfg->ca_cache_threshold;
   c->ws = static_cast<char*>(d_workspace);
   c->stream = static_cast<hipStream_t>(hip_stream);
   c->device = dev;

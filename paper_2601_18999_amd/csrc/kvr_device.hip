@@ -113,6 +113,42 @@ __device__ __forceinline__ uint32_t wave_argmin(double eh, uint32_t W, const dou
   return (uint32_t)first_lane(__ballot(b == mn));
 }
 
+// Lowest lane among the minima of v (lanes >= W excluded).
+__device__ __forceinline__ uint32_t wave_argmin_u32(uint32_t v, uint32_t W) {
+  const uint64_t key = (uint32_t)lane_id() < W ? (((uint64_t)v << 32) | (uint32_t)lane_id()) : ~0ull;
+  return (uint32_t)(wave_min_u64(key) & 0xffffffffull);
+}
+
+// The routed worker of query k (global index j0 + k): the LBGR argmin, or
+// one of the baseline routers of Sec. 5.  Wave-uniform; one lane per worker.
+__device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, uint32_t k, uint32_t W, double eh,
+                                                 const int32_t* hrow, int32_t Lq, const double* eh_sh) {
+  const uint64_t jg = a.j0 + k;
+  if (a.C.router == KVR_ROUTE_RANDOM)
+    return (uint32_t)__umul64hi(philox_word0(jg, 0ull, 0ull, 1ull, a.C.seed, r), (uint64_t)W);
+  if (a.C.router == KVR_ROUTE_ROUND_ROBIN) return (uint32_t)(jg % W);
+  if (a.C.router == KVR_ROUTE_CACHE_AWARE) {
+    uint32_t load = 0, size = 0, h = 0;
+    if ((uint32_t)lane_id() < W) {
+      const WorkerHdr* w = worker_ptrs(a.ws, a.L, r, (uint32_t)lane_id()).hdr;
+      load = w->pend_count;
+      size = w->size;
+      h = (uint32_t)hrow[lane_id()];
+    }
+    const uint32_t lo = wave_argmin_u32(load, W);
+    const uint32_t hi = wave_argmin_u32(~load, W);
+    const uint32_t hmax = wave_argmin_u32(~h, W);
+    const uint32_t small = wave_argmin_u32(size, W);
+    const uint32_t lmin = (uint32_t)__builtin_amdgcn_readlane((int)load, (int)lo);
+    const uint32_t lmax = (uint32_t)__builtin_amdgcn_readlane((int)load, (int)hi);
+    const int32_t hbest = hrow[hmax];
+    if (lmax - lmin > (uint32_t)a.C.ca_balance_abs && (double)lmax > a.C.ca_balance_rel * (double)lmin) return lo;
+    if ((double)hbest > a.C.ca_cache_threshold * (double)Lq) return hmax;
+    return small;
+  }
+  return wave_argmin(eh, W, eh_sh);
+}
+
 // One workgroup per replica walks the batch in order.  A worker's tree
 // changes only when a query is routed to it, so while wave 0 inserts query k
 // into the routed worker the other waves compute the draw words of that
@@ -213,7 +249,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         eh_sh[lane] = eh;
       }
       __builtin_amdgcn_wave_barrier();
-      const uint32_t best = wave_argmin(eh, W, eh_sh);
+      const uint32_t best = route_choice(a, r, k, W, eh, h_sh[cur], Lq, eh_sh);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       const int32_t hb = h_sh[cur][best];
       if (lane == 0) {

@@ -120,6 +120,9 @@ struct Consts {
   int64_t dt_us, true_cached_us, true_miss_us, true_out_us;
   int32_t update;
   int32_t evict;
+  int32_t router;
+  int32_t ca_balance_abs;
+  double ca_balance_rel, ca_cache_threshold;
 };
 
 // Arguments of one batch for the step kernel (device pointers).

@@ -88,6 +88,29 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       uint32_t best = 0;
       for (uint32_t i = 1; i < W; ++i)
         if (eh[i] < eh[best]) best = i;
+      // the baseline routers, as step_kernel's route_choice takes them
+      if (cfg->router == KVR_ROUTE_RANDOM) {
+        best = (uint32_t)__umul64hi(philox_word0(j, 0ull, 0ull, 1ull, C.seed, r), (uint64_t)W);
+      } else if (cfg->router == KVR_ROUTE_ROUND_ROBIN) {
+        best = (uint32_t)(j % W);
+      } else if (cfg->router == KVR_ROUTE_CACHE_AWARE) {
+        uint32_t lo = 0, hi = 0, hmax = 0, small = 0;
+        auto load = [&](uint32_t i) { return worker_ptrs(ws, L, r, i).hdr->pend_count; };
+        auto size = [&](uint32_t i) { return worker_ptrs(ws, L, r, i).hdr->size; };
+        for (uint32_t i = 1; i < W; ++i) {
+          if (load(i) < load(lo)) lo = i;
+          if (load(i) > load(hi)) hi = i;
+          if (h[cur][i] > h[cur][hmax]) hmax = i;
+          if (size(i) < size(small)) small = i;
+        }
+        if (load(hi) - load(lo) > (uint32_t)cfg->ca_balance_abs &&
+            (double)load(hi) > cfg->ca_balance_rel * (double)load(lo))
+          best = lo;
+        else if ((double)h[cur][hmax] > cfg->ca_cache_threshold * (double)Lq)
+          best = hmax;
+        else
+          best = small;
+      }
       Ptrs P = worker_ptrs(ws, L, r, best);
       uint32_t err = commit_route(C, P, ch[best], h[cur][best], Lq, t, olen);
       if (route) route[r * n + j] = (int32_t)best;

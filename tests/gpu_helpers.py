@@ -44,11 +44,12 @@ def compare_worker(g, c, where=""):
 
 
 def assert_parity(stream, res, stats, W, B, replicas, n=None, update="nlms", seed=0, check_stats=True,
-                  evict="rlt"):
+                  evict="rlt", **okw):
+    """okw: further oracle settings (router, cache-aware thresholds)."""
     n = stream.n if n is None else n
     assert res["status"] == K.KVR_OK, (res["status"], res["bits"])
     for r in replicas:
-        o = O.run(stream, W, B, replica=int(r), n=n, all_hits=True, update=update, seed=seed, evict=evict)
+        o = O.run(stream, W, B, replica=int(r), n=n, all_hits=True, update=update, seed=seed, evict=evict, **okw)
         assert o["rc"] == 0
         rt = res["route"][r][:n]
         bad = np.nonzero(rt != o["route"])[0]

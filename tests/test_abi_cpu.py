@@ -35,11 +35,11 @@ def test_config_default_holds_paper_constants():
 
 BAD = [
     dict(num_workers=0), dict(num_workers=65), dict(cache_tokens=0), dict(max_query_tokens=0),
-    dict(max_query_tokens=1001), dict(evict=7), dict(router=3),
+    dict(max_query_tokens=1001), dict(evict=7), dict(router=4), dict(router=-1), dict(router=3, ca_balance_abs=-1),
     dict(update=9), dict(pending_capacity=0), dict(node_capacity=1), dict(arena_words=10),
     dict(rho=0.0), dict(rho=1.5), dict(rho=math.nan), dict(decay_interval_us=0), dict(lr=-1.0),
     dict(lr=math.inf), dict(nlms_eps=-1.0), dict(rls_p0=0.0), dict(alpha_miss=math.nan),
-    dict(true_miss_us=-1), dict(num_replicas=0), dict(abi_version=2), dict(struct_size=8),
+    dict(true_miss_us=-1), dict(num_replicas=0), dict(abi_version=1), dict(struct_size=8),
 ]
 
 

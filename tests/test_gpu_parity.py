@@ -249,3 +249,28 @@ def test_lru_config2_full():
     s = generate(p["stream"])
     res, stats = gpu_run(s, 4, p["W"], p["B"], batch=2500, **LRU)
     assert_parity(s, res, stats, p["W"], p["B"], [0, 3], evict="lru")
+
+
+# ---------------------------------------------------------------- baseline routers
+
+ROUTER = {"random": K.KVR_ROUTE_RANDOM, "round_robin": K.KVR_ROUTE_ROUND_ROBIN,
+          "cache_aware": K.KVR_ROUTE_CACHE_AWARE}
+
+
+@pytest.mark.parametrize("router", sorted(ROUTER))
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_baseline_router_parity(router, evict):
+    rng = np.random.default_rng(31 + len(router) + 7 * (evict == "lru"))
+    for case in range(3):
+        sp = small_spec(n=int(rng.integers(100, 400)), groups=int(rng.integers(2, 9)),
+                        prefix_len=(1, int(rng.integers(3, 90))), suffix_len=(1, int(rng.integers(2, 40))),
+                        vocab=int(rng.integers(2, 40)), seed=900 + case)
+        s = generate(sp)
+        s.arrival_us = np.cumsum(rng.integers(1, 3000, size=s.n)).astype(np.int64)
+        W = int(rng.integers(2, 7))
+        B = int(max(s.max_len, rng.integers(20, 600)))
+        ab = int(rng.integers(0, 8))
+        note(f"{router}/{evict} case {case}: W={W} B={B} n={s.n} balance_abs={ab}")
+        res, stats = gpu_run(s, 3, W, B, seed=case, router=ROUTER[router], ca_balance_abs=ab,
+                             evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict])
+        assert_parity(s, res, stats, W, B, range(3), seed=case, evict=evict, router=router, ca_balance_abs=ab)

@@ -10,12 +10,16 @@ from oracle import oracle as O
 from workload import PRESETS, generate, small_spec
 
 
-def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", **cfg):
+ROUTERS = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
+
+
+def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", router="lbgr", **cfg):
     e = E.run(s, R, W, B, update={"nlms": 0, "rls": 1, "none": 2}[update], seed=seed, ucap=ucap,
-              evict={"rlt": 0, "lru": 1}[evict], **cfg)
+              evict={"rlt": 0, "lru": 1}[evict], router=ROUTERS[router], **cfg)
     assert e["rc"] == 0
     for r in range(R):
-        o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict)
+        o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict, router=router,
+                  **{k: v for k, v in cfg.items() if k.startswith("ca_")})
         np.testing.assert_array_equal(e["route"][r], o["route"])
         np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
         for i in range(W):
@@ -128,3 +132,18 @@ def test_lru_collector_and_presets():
     assert sum(w["gc_runs"] for w in e["workers"][0]) > 20
     p = PRESETS[2]
     _compare(generate(p["stream"]).head(3000), 1, p["W"], p["B"], evict="lru")
+
+
+@pytest.mark.parametrize("router", ["random", "round_robin", "cache_aware"])
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_baseline_routers(router, evict):
+    rng = np.random.default_rng(40 + len(router) + (evict == "lru"))
+    for case in range(15):
+        sp = small_spec(n=int(rng.integers(40, 200)), groups=int(rng.integers(1, 8)),
+                        prefix_len=(1, int(rng.integers(2, 40))), suffix_len=(1, int(rng.integers(2, 20))),
+                        vocab=int(rng.integers(2, 12)), seed=7000 + case)
+        s = generate(sp)
+        s.arrival_us = np.cumsum(rng.integers(1, 3000, size=s.n)).astype(np.int64)  # loads build up
+        W = int(rng.integers(1, 6))
+        B = int(max(s.max_len, rng.integers(2, 150)))
+        _compare(s, 2, W, B, seed=case, evict=evict, router=router, ca_balance_abs=int(rng.integers(0, 6)))

@@ -366,3 +366,58 @@ def test_invariants_hold(seed):
         assert w["resident"] == w["loads"] - w["evictions"]
         assert w["marked_count"] == w["cnt"] <= B
         assert w["load_est"] >= 0.0
+
+
+# ---------------------------------------------------------------------------
+# baseline routers (Sec. 5 "Baselines")
+
+def test_round_robin_cycles_through_workers():
+    s = generate(small_spec(n=97, groups=3, prefix_len=(3, 9), suffix_len=(1, 5), vocab=7))
+    for W in (1, 3, 5):
+        r = O.run(s, W, 40, router="round_robin")
+        assert r["rc"] == 0
+        assert list(r["route"]) == [j % W for j in range(s.n)]
+
+
+def test_random_router_is_uniform_and_keyed():
+    """Random routing draws word 0 of Philox4x64-10 (numpy's implementation
+    here) with key (seed, replica) and counter (j, 0, 0, 1); the routes are
+    uniform over the workers and differ between replicas."""
+    s = generate(small_spec(n=4000, groups=4, prefix_len=(2, 6), suffix_len=(1, 4), vocab=50))
+    W = 5
+    r0 = O.run(s, W, 10**6, router="random", replica=0, seed=3)
+    r1 = O.run(s, W, 10**6, router="random", replica=1, seed=3)
+    want = [(SM.philox_word0(3, 0, (j, 0, 0, 1)) * W) >> 64 for j in range(s.n)]
+    assert list(r0["route"]) == want
+    assert (r0["route"] != r1["route"]).mean() > 0.7
+    counts = np.bincount(r0["route"], minlength=W)
+    chi2 = float(((counts - s.n / W) ** 2 / (s.n / W)).sum())
+    assert chi2 < 18.5  # chi-square, 4 degrees of freedom, p = 0.001
+
+
+def test_cache_aware_switches_on_load_imbalance():
+    """W = 2, queries sharing one long prefix, arrivals 1 us apart (nothing
+    completes): the highest hit (worker 0) takes queries until it has more
+    than ca_balance_abs more in flight than worker 1; then the least loaded
+    worker takes one, and the two alternate."""
+    prefix = list(range(100, 150))
+    paths = [prefix + [1000 + k] * 10 for k in range(40)]
+    s = generate({"kind": "paths", "paths": paths, "order": list(range(40)), "gap_us": 1})
+    r = O.run(s, 2, 10**5, router="cache_aware", ca_balance_abs=32)
+    assert r["rc"] == 0
+    route = list(r["route"])
+    # query 0: no hits anywhere, equal caches -> worker 0; then worker 0 has
+    # the prefix (hit share 50/60 > 0.5) until 33 queries are in flight there
+    assert route[:33] == [0] * 33
+    assert route[33:37] == [1, 0, 1, 0]
+
+
+def test_cache_aware_low_hits_go_to_the_emptiest_cache():
+    """Unrelated queries (hit share 0): each goes to the worker with the
+    fewest cached tokens, the lowest index on ties."""
+    paths = [[10 * k + t for t in range(5 + k)] for k in range(6)]
+    s = generate({"kind": "paths", "paths": paths, "order": list(range(6)), "gap_us": 10**7})
+    r = O.run(s, 3, 10**5, router="cache_aware")
+    assert r["rc"] == 0
+    # sizes after each query: w0 5 | w1 6 | w2 7 | w0 5+8 | w1 6+9 | w2 7+10
+    assert list(r["route"]) == [0, 1, 2, 0, 1, 2]
