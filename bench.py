@@ -57,7 +57,7 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt"):
+def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr"):
     """The CPU oracle, single-threaded, on replica 0 of the same stream: the
     first n queries, n grown until one run takes at least budget_s (the cost
     per query grows as the caches fill, so the last steps grow by 1.4x)."""
@@ -65,7 +65,7 @@ def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt"):
     n = min(1000, stream.n)
     while True:
         t0 = time.perf_counter()
-        O.run(stream, W, B, replica=0, n=n, evict=evict)
+        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router)
         dt = time.perf_counter() - t0
         log(f"cpu oracle: {n} queries in {dt:.1f} s")
         if dt >= budget_s or n >= stream.n:
@@ -134,6 +134,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--evict", choices=["rlt", "lru"], default="rlt",
                     help="eviction policy: RLT (the method) or L-LRU (its baseline)")
+    ap.add_argument("--router", choices=["lbgr", "random", "round_robin", "cache_aware"], default="lbgr",
+                    help="router: LBGR (the method) or one of its baselines")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -168,7 +170,9 @@ def main() -> int:
         return 2
     dev = torch.device("cuda:0")
     evict = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[args.evict]
-    sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict)
+    router = {"lbgr": K.KVR_ROUTE_LBGR, "random": K.KVR_ROUTE_RANDOM, "round_robin": K.KVR_ROUTE_ROUND_ROBIN,
+              "cache_aware": K.KVR_ROUTE_CACHE_AWARE}[args.router]
+    sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router)
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -213,7 +217,7 @@ def main() -> int:
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
-    traffic = load_traffic(workload) if args.evict == "rlt" else None
+    traffic = load_traffic(workload) if (args.evict, args.router) == ("rlt", "lbgr") else None
     line = {
         "metric": "routed queries/sec",
         "value": nq / (kernel_ms * 1e-3),
@@ -227,12 +231,14 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "i32+f64",
         "data": "synthetic",
-        "config": {"workload": workload, "eviction": args.evict, "replicas": R, "workers": W, "cache_tokens": B,
+        "config": {"workload": workload, "eviction": args.evict, "router": args.router, "replicas": R,
+                   "workers": W, "cache_tokens": B,
                    "batch_queries": args.batch, "timed_queries": q - q0,
                    "first_timed_query": q0, "stream_queries": stream.n},
         "prefix_matched_tokens_per_s": d["matched_tokens"] / (kernel_ms * 1e-3),
         "routed_hit_tokens_per_s": d["hit_tokens"] / (kernel_ms * 1e-3),
         "evictions_per_s": d["evictions"] / (kernel_ms * 1e-3),
+        "hit_rate": d["hit_tokens"] / d["prompt_tokens"],
         "wall_s": wall,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
@@ -251,7 +257,7 @@ def main() -> int:
         line["copy_probe_bytes"] = src.numel()
         del src, dst
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict)
+        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router)
     print(json.dumps(line), flush=True)
     return 0
 
