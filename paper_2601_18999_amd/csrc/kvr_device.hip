@@ -184,6 +184,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ uint32_t abort_sh;
   __shared__ uint32_t nev_sh;
   __shared__ uint32_t wready_sh;  // helper waves done with the draw words
+  __shared__ uint32_t next_sh;    // next worker for the helpers' matches
 
   const uint32_t r = blockIdx.x;
   const int lane = lane_id();
@@ -255,6 +256,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       if (lane == 0) {
         best_sh = (int32_t)best;
         wready_sh = 0;
+        next_sh = 0;
         const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
@@ -339,12 +341,19 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
             complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
           if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
         }
-        for (uint32_t i = wave - 1; i < W; i += nh)
-          if (i != best) {
-            Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
-                          &h_sh[cur ^ 1u][i]);
-          }
+        // workers taken one at a time from an LDS counter, so a wave that
+        // drew long matches takes fewer; the index is wave-uniform (lane
+        // 0's atomic, read back from lane 0) and the loop is bounded by W
+        for (uint32_t it = 0; it < W; ++it) {
+          uint32_t got = 0;
+          if (lane == 0) got = atomicAdd(&next_sh, 1u);
+          const uint32_t i = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
+          if (i >= W) break;
+          if (i == best) continue;
+          Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
+          count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
+                        &h_sh[cur ^ 1u][i]);
+        }
       }
     }
     stale = (int32_t)best;
