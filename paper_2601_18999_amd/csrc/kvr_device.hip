@@ -214,7 +214,6 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       count_matched(P, match_lcp(P, P.hdr->arena_sel, smem, L0, paths.of(i)), &h_sh[0][i]);
     }
   }
-  int32_t stale = -1, Lprev = 0;
   for (uint32_t k = 0; k < a.n; ++k) {
     const uint64_t o0 = a.offsets[k];
     const int32_t Lq = (int32_t)(a.offsets[k + 1] - o0);
@@ -232,16 +231,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     }
     __syncthreads();
 
-    // ---- phase A.  Wave 0: the routed worker of the last query gets its h
-    // for this one; scores, argmin, commit.  Helpers: stage the next query.
+    // ---- phase A.  Wave 0: scores, argmin, commit.  Helpers: stage the
+    // next query.
     if (wave == 0) {
-      if (stale >= 0) {
-        Ptrs P = worker_ptrs(a.ws, a.L, r, (uint32_t)stale);
-        const int32_t h = match_incremental(P, P.hdr->arena_sel, qs, Lq, Lprev, ell_sh[cur ^ 1u],
-                                            paths.of((uint32_t)stale));
-        count_matched(P, h, &h_sh[cur][stale]);
-        __builtin_amdgcn_wave_barrier();
-      }
       double eh = __builtin_huge_val();
       if ((uint32_t)lane < W) {
         double ch;
@@ -285,9 +277,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     const uint32_t rn = a.C.evict == KVR_EVICT_RLT ? (nev < a.rcap ? nev : a.rcap) : 0u;
     const int32_t ell = ell_sh[cur];
 
-    // ---- phase B.  Wave 0: RLT insertion.  Helpers: the insertion's draw
-    // words first, then completions and decay at the next arrival and the
-    // next query's h on the other workers.
+    // ---- phase B.  Wave 0: the insertion, then the routed worker's h for
+    // the next query.  Helpers: the insertion's draw words first, then
+    // completions and decay at the next arrival and the next query's h on
+    // the other workers.
     if (wave == 0) {
       if (nh == 0)
         for (uint32_t d = (uint32_t)lane; d < rn; d += KVR_WAVE)
@@ -318,6 +311,13 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         }
         atomicOr(&g->status, err);
         abort_sh = 1;
+      }
+      // the routed worker's h for the next query, from the path of the
+      // query just inserted (all of it is cached now: the old h is Lq)
+      if (has_next && !err) {
+        Ptrs Pb = worker_ptrs(a.ws, a.L, r, best);
+        count_matched(Pb, match_incremental(Pb, Pb.hdr->arena_sel, qn, Ln, Lq, ell, paths.of(best)),
+                      &h_sh[cur ^ 1u][best]);
       }
       if (nh == 0 && has_next) {
         if ((uint32_t)lane < W)
@@ -356,8 +356,6 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         }
       }
     }
-    stale = (int32_t)best;
-    Lprev = Lq;
     __syncthreads();
     if (abort_sh) break;
   }
