@@ -500,12 +500,13 @@ __device__ __forceinline__ int32_t node_alloc(const Ptrs& P, St& s) {
   return id;
 }
 
+// No fence: a freed record is read again only by a later allocation, after
+// the fences that end this insertion.
 __device__ __forceinline__ void node_free(const Ptrs& P, St& s, int32_t id) {
   if (lane_id() == 0) {
     P.nodes[id].parent = -2;
     P.nodes[id].off = (uint32_t)s.free_head;
   }
-  wave_mem_sync();
   s.free_head = id;
   s.nnodes -= 1;
 }
@@ -543,6 +544,25 @@ __device__ int32_t child_slot(const int32_t* ar, const NodeRec& na, int32_t c) {
     if (m) return b + first_lane(m);
   }
   return -1;
+}
+
+// Remove child c of node a, whose record (as read by the caller) is na; na
+// is updated to the new child count.
+__device__ __forceinline__ bool child_remove_rec(const Ptrs& P, const St& s, int32_t a, NodeRec& na, int32_t c) {
+  int32_t* ar = arena_of(P, s.arena_sel);
+  int32_t pos = child_slot(ar, na, c);
+  if (pos < 0) return false;
+  int32_t last = na.nchild - 1;
+  if (lane_id() == 0) {
+    if (pos != last) {
+      ar[na.coff + 2 * pos] = ar[na.coff + 2 * last];
+      ar[na.coff + 2 * pos + 1] = ar[na.coff + 2 * last + 1];
+    }
+    P.nodes[a].nchild = last;
+  }
+  wave_mem_sync();
+  na.nchild = last;
+  return true;
 }
 
 __device__ __forceinline__ bool child_remove(const Ptrs& P, const St& s, int32_t a, int32_t c) {
@@ -1050,18 +1070,19 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
       s.nU -= 1;
       return true;
     }
-    // the node is empty: drop it; its parent may take its place
+    // the node is empty: drop it; its parent may take its place.  The
+    // parent's record is read together with the leaf list.
+    NodeRec np = P.nodes[pf];
     const int32_t li = arr_find(P.leaf, s.nleaves, nf);
     if (li < 0) {
       KVR_FAIL_CHECK(s, 12, nf, s.nleaves, kkf);
       return false;
     }
-    if (!child_remove(P, s, pf, nf)) {
+    if (!child_remove_rec(P, s, pf, np, nf)) {
       KVR_FAIL_CHECK(s, 13, nf, pf, 0);
       return false;
     }
     node_free(P, s, nf);
-    const NodeRec np = P.nodes[pf];
     if (pf != 0 && np.nchild == 0) {
       if (lane == 0) P.leaf[li] = pf;
       wave_mem_sync();
