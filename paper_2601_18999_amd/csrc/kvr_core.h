@@ -951,14 +951,19 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
   bool exact = true;
   if (dctr + cnt <= ia.rn) {
     // every active draw's high half is precomputed; inactive lanes read the
-    // last one
+    // last one.  All the loads first, so they are in flight together.
+    uint32_t wv[kDraws];
 #pragma unroll
     for (int r = 0; r < kDraws; ++r) {
       uint64_t d = dctr + (uint64_t)(r * KVR_WAVE + lane);
-      act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
       if (d >= ia.rn) d = ia.rn - 1u;
+      wv[r] = ia.rw[d];
+    }
+#pragma unroll
+    for (int r = 0; r < kDraws; ++r) {
+      act[r] = (uint32_t)(r * KVR_WAVE + lane) < cnt;
       uint32_t k = 0;
-      const bool ok = draw_index_hi(ia.rw[d], s.nU, k);
+      const bool ok = draw_index_hi(wv[r], s.nU, k);
       kk[r] = act[r] ? k : 0u;
       if (act[r] && !ok) exact = false;
     }
