@@ -28,7 +28,12 @@
 //
 // Readings of points the paper leaves open (each one is listed with its
 // reason in the design notes of the repository):
-//   - only the prompt q_j is inserted (responses never recur here);
+//   - by default only the prompt q_j is inserted (synthetic responses never
+//     recur); with cache_responses the stream holds complete token paths
+//     Gamma_j = q_j || a_j (Sec. 3.2 "Cache Matching and Arrival Model")
+//     whose last o_j tokens are the response: the whole path is inserted,
+//     while the match, the routing features and the cost use the prompt
+//     (the response is not known when the query is routed);
 //   - the insertion point (the parent of the token being loaded) is never
 //     evicted while its child is loaded, so the tree stays prefix-closed;
 //   - "uniformly at random" = index floor(r * |U| / 2^64) into U sorted by
@@ -90,6 +95,9 @@ typedef struct orc_config {
   int32_t ca_balance_abs;     // cache-aware: imbalance when max - min in-flight > this ...
   double ca_balance_rel;      // ... and max > this * min
   double ca_cache_threshold;  // cache-aware: best hit / |q| above this routes to the best hit
+  // 1 = a path is q_j || a_j with |a_j| = out_len[j]; insert all of it
+  int32_t cache_responses;
+  int32_t pad1;
 } orc_config;
 
 typedef struct orc_worker_stats {
@@ -452,7 +460,9 @@ void online_update(Sim& s, Worker& w, const double phi[4], double e) {
 
 int64_t tick(const orc_config& c, int64_t t) { return t / c.decay_interval_us; }
 
-void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int64_t t, int32_t o,
+// Query jg: prompt q[0, L), inserted path q[0, Lpath) (Lpath = L unless
+// responses are cached), arrival t, output length o.
+void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int32_t Lpath, int64_t t, int32_t o,
           int32_t* route_out, int32_t* hit_out, int32_t* all_hits_row) {
   const orc_config& c = s.cfg;
   const uint32_t W = c.num_workers;
@@ -567,9 +577,9 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int64_t t, int32_t o
   if (hit_out) *hit_out = (int32_t)hb;
   // 6. insert the path into the routed worker's cache
   if (c.evict == 0)
-    insert_rlt(s, best, q, L, jg);
+    insert_rlt(s, best, q, Lpath, jg);
   else
-    insert_lru(s, best, q, L, jg);
+    insert_lru(s, best, q, Lpath, jg);
 }
 
 // Per-token path hash H(v) = mix64(H(parent) + GOLDEN * (tok + 1)), H(root) = 0.
@@ -640,9 +650,14 @@ int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* 
   }
   for (uint64_t j = 0; j < n; ++j) {
     const int32_t* q = tokens + offsets[j];
-    int32_t L = (int32_t)(offsets[j + 1] - offsets[j]);
+    const int32_t Lpath = (int32_t)(offsets[j + 1] - offsets[j]);
     int32_t o = out_len ? (int32_t)out_len[j] : 4;
-    step(s, j, q, L, arrival_us[j], o, route ? route + j : nullptr, hits ? hits + j : nullptr,
+    const int32_t L = cfg->cache_responses ? Lpath - o : Lpath;  // the prompt
+    if (L < 1) {
+      s.error |= 1;
+      break;
+    }
+    step(s, j, q, L, Lpath, arrival_us[j], o, route ? route + j : nullptr, hits ? hits + j : nullptr,
          all_hits ? all_hits + j * cfg->num_workers : nullptr);
     if (s.error) break;
     if (cfg->check && !check_invariants(s)) {

@@ -44,6 +44,8 @@ class OrcConfig(ctypes.Structure):
         ("ca_balance_abs", ctypes.c_int32),
         ("ca_balance_rel", ctypes.c_double),
         ("ca_cache_threshold", ctypes.c_double),
+        ("cache_responses", ctypes.c_int32),
+        ("pad1", ctypes.c_int32),
     ]
 
 
@@ -93,7 +95,8 @@ DEFAULTS: Dict[str, Any] = dict(
     alpha_cached=0.0, alpha_miss=1.0, rho=31.0 / 32.0, decay_interval_us=20000,
     lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
     true_cached_us=0, true_miss_us=1000, true_out_us=10000,
-    router="lbgr", ca_balance_abs=32, ca_balance_rel=1.0001, ca_cache_threshold=0.5)
+    router="lbgr", ca_balance_abs=32, ca_balance_rel=1.0001, ca_cache_threshold=0.5,
+    cache_responses=0)
 
 ROUTER = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
 
@@ -117,6 +120,7 @@ def make_config(W: int, B: int, **kw) -> OrcConfig:
     c.ca_balance_abs = int(p["ca_balance_abs"])
     c.ca_balance_rel = float(p["ca_balance_rel"])
     c.ca_cache_threshold = float(p["ca_cache_threshold"])
+    c.cache_responses = int(p["cache_responses"])
     return c
 
 

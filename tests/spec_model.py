@@ -85,8 +85,9 @@ class SpecSim:
     def __init__(self, W: int, B: int, replica: int = 0, seed: int = 0, evict: str = "rlt",
                  update: str = "nlms", alpha_cached=0.0, alpha_miss=1.0, rho=31 / 32,
                  decay_interval_us=20000, lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
-                 true_cached_us=0, true_miss_us=1000, true_out_us=10000):
+                 true_cached_us=0, true_miss_us=1000, true_out_us=10000, cache_responses=0):
         self.W, self.B, self.r, self.seed = W, B, replica, seed
+        self.responses = bool(cache_responses)
         self.evict, self.update = evict, update
         self.ac, self.am, self.rho, self.dt = alpha_cached, alpha_miss, rho, decay_interval_us
         self.lr, self.eps = lr, nlms_eps
@@ -120,7 +121,10 @@ class SpecSim:
             w.Pm = [[(w.Pm[a][b] - k[a] * pi[b]) / self.lr for b in range(4)] for a in range(4)]
 
     def step(self, jg: int, q, t: int, o: int):
-        q = tuple(int(x) for x in q)
+        path = tuple(int(x) for x in q)
+        # with cached responses the path is prompt || response and only the
+        # prompt is known when routing
+        q = path[: len(path) - o] if self.responses else path
         L = len(q)
         for w in self.w:
             while w.pend and w.pend[0]["t_done"] <= t:
@@ -161,9 +165,9 @@ class SpecSim:
         w.pend.append({"t_route": t, "t_done": t + e_us, "chat": chats[best], "base": base,
                        "e_obs": e_us * 1e-6, "phi": phis[best]})
         if self.evict == "rlt":
-            self._insert_rlt(best, q, jg)
+            self._insert_rlt(best, path, jg)
         else:
-            self._insert_lru(best, q, jg)
+            self._insert_lru(best, path, jg)
         return best, hb, h
 
     def _insert_rlt(self, i: int, q, jg: int):

@@ -14,6 +14,9 @@
 * Exact expected hits of RLT by enumerating every random choice.
 * LBGR closed forms: decayed load, full release on completion, one NLMS
   step, RLS = exponentially weighted ridge least squares.
+* Cached responses (complete paths q || a): the brute-force model, the
+  reduction to prompt-only caching when every response is empty, and the
+  match and cache contents as closed forms over the routed history.
 """
 from fractions import Fraction
 import math
@@ -421,3 +424,97 @@ def test_cache_aware_low_hits_go_to_the_emptiest_cache():
     assert r["rc"] == 0
     # sizes after each query: w0 5 | w1 6 | w2 7 | w0 5+8 | w1 6+9 | w2 7+10
     assert list(r["route"]) == [0, 1, 2, 0, 1, 2]
+
+
+# ---------------------------------------------------------------------------
+# cached responses: a path is q_j || a_j, the last out_len[j] tokens
+
+def _random_response_stream(rng, n, vocab, max_prompt, max_resp, B):
+    paths, olen = [], []
+    for _ in range(n):
+        L = int(rng.integers(1, max(1, min(max_prompt, B - max_resp)) + 1))
+        o = int(rng.integers(0, max_resp + 1))
+        paths.append([int(x) for x in rng.integers(0, vocab, size=L + o)])
+        olen.append(o)
+    gaps = rng.integers(1, 400000, size=n)
+    s = _paths_stream(paths, list(range(n)))
+    s.arrival_us = np.cumsum(gaps).astype(np.int64)
+    s.out_len = np.array(olen, dtype=np.uint16)
+    return s
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_responses_equal_bruteforce_model(evict):
+    rng = np.random.default_rng(77 + len(evict))
+    for case in range(60):
+        W = int(rng.integers(1, 4))
+        B = int(rng.integers(4, 14))
+        vocab = int(rng.integers(2, 5))
+        n = int(rng.integers(5, 30))
+        s = _random_response_stream(rng, n, vocab, 5, 3, B)
+        replica = int(rng.integers(0, 1000))
+        kw = dict(evict=evict, seed=int(rng.integers(0, 2**32)), cache_responses=1)
+        r = O.run(s, W, B, replica=replica, all_hits=True, check=1, **kw)
+        assert r["rc"] == 0
+        sim, routes, hits, allh = SM.run_spec(s, W, B, replica=replica, **kw)
+        np.testing.assert_array_equal(r["route"], routes)
+        np.testing.assert_array_equal(r["all_hits"], allh)
+        prompts = s.lengths - s.out_len.astype(np.int64)
+        assert (r["hits"] <= prompts).all()
+        for i in range(W):
+            ws, sw = r["workers"][i], sim.w[i]
+            assert ws["evictions"] == sw.evictions and ws["loads"] == sw.loads
+            assert (ws["resident"], ws["digest_sum"], ws["digest_xor"]) == _digest_of_set(sw.S)
+            assert ws["load_est"] == sw.P and ws["theta"] == sw.theta
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_empty_responses_reduce_to_prompt_caching(evict):
+    s = generate(small_spec(n=250, groups=4, prefix_len=(4, 20), suffix_len=(1, 12), vocab=8))
+    s.out_len = np.zeros(s.n, dtype=np.uint16)
+    a = O.run(s, 3, 60, replica=3, all_hits=True, evict=evict)
+    b = O.run(s, 3, 60, replica=3, all_hits=True, evict=evict, cache_responses=1)
+    np.testing.assert_array_equal(a["route"], b["route"])
+    np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
+    assert a["workers"] == b["workers"]
+    assert sum(w["evictions"] for w in a["workers"]) > 0
+
+
+def test_responses_match_and_contents_over_routed_history():
+    """Nothing evicted: h_ij is the longest common prefix of the prompt with
+    any complete path routed to worker i before, the cache of i holds exactly
+    the prefixes of those paths, and only a prompt's tokens count as hits."""
+    sp = {"kind": "sessions", "n_sessions": 40, "turns": (1, 5), "start_len": 6,
+          "ext_len": (1, 6), "vocab": 5, "responses": True, "out_len": 3, "turn_rate": 3.0}
+    s = generate(sp)
+    W, B = 3, 10**6
+    r = O.run(s, W, B, all_hits=True, cache_responses=1)
+    assert r["rc"] == 0 and sum(w["evictions"] for w in r["workers"]) == 0
+    paths = [tuple(int(x) for x in s.query(j)) for j in range(s.n)]
+    prompts = [p[: len(p) - int(s.out_len[j])] for j, p in enumerate(paths)]
+    seen = [set() for _ in range(W)]
+    seen_prompts = [set() for _ in range(W)]
+
+    def lcp_max(xs, q):
+        best = 0
+        for x in xs:
+            l = 0
+            while l < min(len(x), len(q)) and x[l] == q[l]:
+                l += 1
+            best = max(best, l)
+        return best
+
+    carried = 0
+    for j in range(s.n):
+        for i in range(W):
+            assert r["all_hits"][j, i] == lcp_max(seen[i], prompts[j])
+        i = int(r["route"][j])
+        # the hit reaches into a cached response: more than any prompt gives
+        carried += int(r["hits"][j] > lcp_max(seen_prompts[i], prompts[j]))
+        seen[i].add(paths[j])
+        seen_prompts[i].add(prompts[j])
+    for i in range(W):
+        prefixes = {x[:k] for x in seen[i] for k in range(1, len(x) + 1)}
+        assert r["workers"][i]["resident"] == len(prefixes) == r["workers"][i]["loads"]
+    # a later turn's prompt contains the previous turn's response, and hits reach into it
+    assert carried > 0

@@ -17,6 +17,12 @@ workload families (Sec. 5 "Workloads"; App. A):
 Arrivals are a Poisson process (exponential gaps) unless a recipe says
 otherwise; times are integer microseconds.  Output length is 4 tokens
 (the paper's default) unless set.
+
+With ``responses: True`` every path is a complete token path q_j || a_j
+(Sec. 3.2 "Cache Matching and Arrival Model"): the last ``out_len[j]``
+tokens are a synthetic response.  In ``sessions`` the response of a turn is
+part of the next turn's prompt (a conversation carries its answers); in the
+other recipes it is fresh random tokens that never recur.
 """
 from __future__ import annotations
 
@@ -182,6 +188,10 @@ def _gen_sessions(sp: Dict[str, Any], rng: np.random.Generator) -> Stream:
     start_len = int(sp["start_len"])
     turns = rng.integers(tlo, thi + 1, size=ns)
     ext = rng.integers(elo, ehi + 1, size=int(turns.sum()))
+    if sp.get("responses"):
+        # a turn's extension is followed by its response, which the next
+        # turn's prompt then contains
+        ext = ext + int(sp.get("out_len", 4))
     ext_off = np.zeros(ns + 1, dtype=np.int64)
     ext_off[1:] = np.cumsum(turns)
     shared_start = bool(sp.get("shared_start", False))
@@ -258,11 +268,34 @@ _KINDS = {"groups": _gen_groups, "two_level": _gen_two_level,
           "sessions": _gen_sessions, "paths": _gen_paths}
 
 
+def _append_responses(st: Stream, vocab: int, rng: np.random.Generator) -> Stream:
+    """Append out_len[j] fresh random response tokens to every query."""
+    o = st.out_len.astype(np.int64)
+    qlen = st.lengths + o
+    resp = rng.integers(0, vocab, size=int(o.sum()), dtype=np.int32)
+
+    def fill(tok, off):
+        ro = 0
+        for j in range(st.n):
+            a, L = int(off[j]), int(st.lengths[j])
+            tok[a:a + L] = st.query(j)
+            tok[a + L:a + L + int(o[j])] = resp[ro:ro + int(o[j])]
+            ro += int(o[j])
+
+    tokens, offsets = _assemble(qlen, fill)
+    return Stream(tokens, offsets, st.arrival_us, st.out_len, st.spec)
+
+
 def generate(spec: Dict[str, Any], seed: Optional[int] = None) -> Stream:
     """Draw the stream described by ``spec`` (deterministic in ``seed``)."""
     seed = int(spec.get("seed", 0) if seed is None else seed)
     rng = np.random.default_rng(seed)
-    return _KINDS[spec["kind"]](dict(spec), rng)
+    st = _KINDS[spec["kind"]](dict(spec), rng)
+    if spec.get("responses") and spec["kind"] != "sessions":
+        # drawn after the prompts from a generator of their own, so the
+        # prompts are those of the same spec without responses
+        st = _append_responses(st, int(spec.get("vocab", 32000)), np.random.default_rng([seed, 1]))
+    return st
 
 
 # ---------------------------------------------------------------------------
