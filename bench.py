@@ -57,7 +57,7 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr"):
+def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr", responses: int = 0):
     """The CPU oracle, single-threaded, on replica 0 of the same stream: the
     first n queries, n grown until one run takes at least budget_s (the cost
     per query grows as the caches fill, so the last steps grow by 1.4x)."""
@@ -65,7 +65,7 @@ def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str 
     n = min(1000, stream.n)
     while True:
         t0 = time.perf_counter()
-        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router)
+        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses)
         dt = time.perf_counter() - t0
         log(f"cpu oracle: {n} queries in {dt:.1f} s")
         if dt >= budget_s or n >= stream.n:
@@ -136,6 +136,9 @@ def main() -> int:
                     help="eviction policy: RLT (the method) or L-LRU (its baseline)")
     ap.add_argument("--router", choices=["lbgr", "random", "round_robin", "cache_aware"], default="lbgr",
                     help="router: LBGR (the method) or one of its baselines")
+    ap.add_argument("--responses", action="store_true",
+                    help="cache complete token paths q||a (each query followed by its response; in the "
+                         "multi-turn workload a turn's response is part of the next prompt)")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -162,7 +165,7 @@ def main() -> int:
     p = PRESETS[args.config]
     R, W, B = p["R"], p["W"], p["B"]
     t0 = time.perf_counter()
-    stream = generate(p["stream"])
+    stream = generate(dict(p["stream"], responses=True) if args.responses else p["stream"])
     log(f"{p['name']}: {stream.n} queries, {stream.tokens.size} tokens ({time.perf_counter() - t0:.1f} s)")
     need = (args.warmup + args.steps) * args.batch
     if need > stream.n:
@@ -172,7 +175,8 @@ def main() -> int:
     evict = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[args.evict]
     router = {"lbgr": K.KVR_ROUTE_LBGR, "random": K.KVR_ROUTE_RANDOM, "round_robin": K.KVR_ROUTE_ROUND_ROBIN,
               "cache_aware": K.KVR_ROUTE_CACHE_AWARE}[args.router]
-    sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router)
+    sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router,
+                      cache_responses=int(args.responses))
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -207,17 +211,19 @@ def main() -> int:
     d = {k: after[k] - before[k] for k in after}
     kernel_ms = sum(a.elapsed_time(b) for a, b in ev)
     nq = R * (q - q0)
-    lens = stream.lengths[q0:q].astype("int64")
-    prompt = int(lens.sum()) * R
+    paths = stream.lengths[q0:q].astype("int64")
+    path_tokens = int(paths.sum()) * R
+    prompt = path_tokens - (int(stream.out_len[q0:q].astype("int64").sum()) * R if args.responses else 0)
     assert prompt == d["prompt_tokens"]
-    # algorithmic bytes of the timed launches: query staging, edge tokens
-    # compared on every worker, edge tokens written for loaded tokens, one
-    # candidate/node read-modify-write per eviction, LBGR + completion record
-    alg_bytes = (4 * prompt + 4 * d["matched_tokens"] + 4 * d["loads"] + 32 * d["evictions"]
+    # algorithmic bytes of the timed launches: query (path) staging, edge
+    # tokens compared on every worker, edge tokens written for loaded tokens,
+    # one candidate/node read-modify-write per eviction, LBGR + completion
+    # record
+    alg_bytes = (4 * path_tokens + 4 * d["matched_tokens"] + 4 * d["loads"] + 32 * d["evictions"]
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
-    traffic = load_traffic(workload) if (args.evict, args.router) == ("rlt", "lbgr") else None
+    traffic = load_traffic(workload) if (args.evict, args.router, args.responses) == ("rlt", "lbgr", False) else None
     line = {
         "metric": "routed queries/sec",
         "value": nq / (kernel_ms * 1e-3),
@@ -231,7 +237,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "i32+f64",
         "data": "synthetic",
-        "config": {"workload": workload, "eviction": args.evict, "router": args.router, "replicas": R,
+        "config": {"workload": workload + ("_responses" if args.responses else ""), "eviction": args.evict,
+                   "router": args.router, "cached_responses": bool(args.responses), "replicas": R,
                    "workers": W, "cache_tokens": B,
                    "batch_queries": args.batch, "timed_queries": q - q0,
                    "first_timed_query": q0, "stream_queries": stream.n},
@@ -257,7 +264,8 @@ def main() -> int:
         line["copy_probe_bytes"] = src.numel()
         del src, dst
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router)
+        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router,
+                                            int(args.responses))
     print(json.dumps(line), flush=True)
     return 0
 

@@ -35,7 +35,8 @@
  *   - Errors are status codes; nothing is thrown across the ABI.  Errors the
  *     host can see (bad configuration, bad arguments, NULL pointers) return
  *     before any device work.  Errors only the device can see (a query of
- *     length 0 or above max_query_tokens, a negative token, decreasing
+ *     length 0 or above max_query_tokens, with cache_responses a path no
+ *     longer than its response, a negative token, decreasing
  *     arrival times, a full completion ring, a full node table or arena) set
  *     a sticky status word in the workspace: an invalid batch is rejected
  *     as a whole before any state changes (KVR_EINVAL), a capacity overflow
@@ -53,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 2u
+#define KVR_ABI_VERSION 3u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -77,7 +78,8 @@ enum { KVR_UPD_NLMS = 0, KVR_UPD_RLS = 1, KVR_UPD_NONE = 2 };
 
 /* Device status bits (kvr_check reports the first one as a kvr_status). */
 enum {
-  KVR_DEV_BAD_LENGTH = 1u,   /* a query of length 0 or > max_query_tokens  */
+  KVR_DEV_BAD_LENGTH = 1u,   /* a query of length 0 or > max_query_tokens, or a
+                                path no longer than its cached response     */
   KVR_DEV_BAD_TOKEN = 2u,    /* a negative token id                        */
   KVR_DEV_BAD_ARRIVAL = 4u,  /* arrival times decrease                     */
   KVR_DEV_PENDING_FULL = 8u, /* completion ring of a worker is full        */
@@ -115,6 +117,16 @@ typedef struct kvr_config {
   int32_t pad0;
   double ca_balance_rel;     /* ... and max > this * min (1.0001)                  */
   double ca_cache_threshold; /* cache-aware: highest hit / |q| above this (0.5)    */
+  /* 0 (default): a query is its prompt q_j and only the prompt is cached.
+   * 1: a query is the complete token path Gamma_j = q_j || a_j of Sec. 3.2
+   * ("Cache Matching and Arrival Model"): its last out_len[j] tokens are the
+   * response a_j (out_len = 4 when d_out_len is NULL).  The match h_ij, the
+   * routing features, the hit counts and the observed-latency cost use the
+   * prompt, which is all the router sees; the insertion and its evictions
+   * take the whole path.  Every path must then be longer than its response
+   * (a prompt of >= 1 token), and max_query_tokens bounds the path. */
+  int32_t cache_responses;
+  int32_t pad1;
 } kvr_config;
 
 /* Final per-(replica, worker) state and counters (kvr_stats). */

@@ -68,6 +68,7 @@ kvr_status validate(const kvr_config* c) {
   if (c->router == KVR_ROUTE_CACHE_AWARE &&
       (c->ca_balance_abs < 0 || !(c->ca_balance_rel >= 0.0) || !(c->ca_cache_threshold >= 0.0)))
     return fail(KVR_EINVAL, "cache-aware thresholds must be >= 0");
+  if (c->cache_responses != 0 && c->cache_responses != 1) return fail(KVR_EINVAL, "cache_responses must be 0 or 1");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
   if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
@@ -134,6 +135,8 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->pad0 = 0;
   c->ca_balance_rel = 1.0001;
   c->ca_cache_threshold = 0.5;
+  c->cache_responses = 0;
+  c->pad1 = 0;
   c->update = KVR_UPD_NLMS;
   c->pending_capacity = 65536;
   c->node_capacity = 0;
@@ -215,6 +218,8 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   c->C.ca_balance_abs = cfg->ca_balance_abs;
   c->C.ca_balance_rel = cfg->ca_balance_rel;
   c->C.ca_cache_threshold = cfg->ca_cache_threshold;
+  c->C.cache_responses = cfg->cache_responses;
+  c->C.pad = 0;
   c->ws = static_cast<char*>(d_workspace);
   c->stream = static_cast<hipStream_t>(hip_stream);
   c->device = dev;

@@ -1884,6 +1884,11 @@ __device__ __forceinline__ void complete_and_decay(const Consts& C, const Ptrs& 
 
 // ---------------------------------------------------------------- routing (one thread per worker)
 
+// Output length of query k: the given one, else 4 (the paper's default).
+__device__ __forceinline__ int32_t query_out_len(const uint16_t* out_len, uint64_t k) {
+  return out_len ? (int32_t)out_len[k] : 4;
+}
+
 // LBGR score of one worker (Eq. LBGR-score with the features of Sec. 4.2
 // and the per-1k-token scaling of App. A).  *chat = estimated service time.
 __device__ double lbgr_score(const Consts& C, const WorkerHdr* w, int32_t h, int32_t L, double* chat) {

@@ -29,6 +29,10 @@
 // index floor(r * |U| / 2^64), r = word 0 of Philox4x64-10 with key
 // (seed, replica) and counter (query index, worker, draw index, 0).
 //
+// With cached responses a query is a complete token path q_j || a_j (Sec.
+// 3.2 "Cache Matching and Arrival Model"): the match, the scores and the
+// commit see the prompt q_j, the insertion takes the whole path.
+//
 // Floating point: double, left-to-right sums, built with -ffp-contract=off so
 // no multiply-add is fused; the same expressions in the same order as the
 // definition, so results are bit-identical to any IEEE implementation that
@@ -181,12 +185,14 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ double ch_sh[kMaxWorkers];
   __shared__ int32_t ell_sh[2];  // LCP(q_k, q_k+1) in slot k & 1
   __shared__ int32_t best_sh;
+  __shared__ int32_t hins_sh;  // cached length of the inserted path (>= h of the prompt)
   __shared__ uint32_t abort_sh;
   __shared__ uint32_t nev_sh;
   __shared__ uint32_t wready_sh;  // helper waves done with the draw words
   __shared__ uint32_t next_sh;    // next worker for the helpers' matches
 
   const uint32_t r = blockIdx.x;
+  const bool resp = a.C.cache_responses != 0;
   const int lane = lane_id();
   const uint32_t wave = threadIdx.x / KVR_WAVE;
   const uint32_t nwaves = blockDim.x / KVR_WAVE;
@@ -201,33 +207,37 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __syncthreads();
   if (abort_sh) return;
 
-  // query 0: stage it; completions and decay at its arrival; full matches
+  // query 0: stage its path; completions and decay at its arrival; full
+  // matches of its prompt
   {
     const uint64_t o0 = a.offsets[0];
     const int32_t L0 = (int32_t)(a.offsets[1] - o0);
+    const int32_t L0q = resp ? L0 - query_out_len(a.out_len, 0) : L0;
     for (int32_t x = (int32_t)threadIdx.x; x < L0; x += (int32_t)blockDim.x) smem[x] = a.tokens[o0 + x];
     if (wave == 0 && (uint32_t)lane < W)
       complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[0], rh->tprev);
     __syncthreads();
     for (uint32_t i = wave; i < W; i += nwaves) {
       Ptrs P = worker_ptrs(a.ws, a.L, r, i);
-      count_matched(P, match_lcp(P, P.hdr->arena_sel, smem, L0, paths.of(i)), &h_sh[0][i]);
+      count_matched(P, match_lcp(P, P.hdr->arena_sel, smem, L0q, paths.of(i)), &h_sh[0][i]);
     }
   }
   for (uint32_t k = 0; k < a.n; ++k) {
     const uint64_t o0 = a.offsets[k];
-    const int32_t Lq = (int32_t)(a.offsets[k + 1] - o0);
+    const int32_t Lp = (int32_t)(a.offsets[k + 1] - o0);  // the path inserted
     const int64_t t = a.arrival[k];
-    const int32_t olen = a.out_len ? (int32_t)a.out_len[k] : 4;
+    const int32_t olen = query_out_len(a.out_len, k);
+    const int32_t Lq = resp ? Lp - olen : Lp;  // the prompt
     const uint32_t cur = k & 1u;
     int32_t* qs = smem + cur * qstride;
     int32_t* qn = smem + (cur ^ 1u) * qstride;
     const bool has_next = k + 1 < a.n;
-    int32_t Ln = 0;
+    int32_t Ln = 0, Lnq = 0;  // path and prompt of the next query
     uint64_t n0 = 0;
     if (has_next) {
       n0 = a.offsets[k + 1];
       Ln = (int32_t)(a.offsets[k + 2] - n0);
+      Lnq = resp ? Ln - query_out_len(a.out_len, k + 1) : Ln;
     }
     __syncthreads();
 
@@ -245,8 +255,14 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       const uint32_t best = route_choice(a, r, k, W, eh, h_sh[cur], Lq, eh_sh);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       const int32_t hb = h_sh[cur][best];
+      // a cached prompt may continue into a cached response: the insertion
+      // needs the cached length of the whole path, continued from the
+      // prompt's recorded match
+      int32_t hins = hb;
+      if (resp && hb == Lq && Lp > Lq) hins = match_incremental(P, P.hdr->arena_sel, qs, Lp, Lq, Lq, paths.of(best));
       if (lane == 0) {
         best_sh = (int32_t)best;
+        hins_sh = hins;
         wready_sh = 0;
         next_sh = 0;
         const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
@@ -255,7 +271,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         if (a.hits) a.hits[orow] = hb;
         // draws this insertion will take: one per token loaded into a full cache
         const uint32_t size = P.hdr->size;
-        const uint32_t nload = (uint32_t)(Lq - hb);
+        const uint32_t nload = (uint32_t)(Lp - hins);
         const uint32_t nfree = a.L.B - size;
         nev_sh = err ? 0u : (nload > nfree ? nload - nfree : 0u);
         if (err) {
@@ -265,9 +281,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       }
       if (a.all_hits && (uint32_t)lane < W)
         a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[cur][lane];
-      if (nh == 0 && has_next) stage_next(a.tokens, n0, Ln, qn, qs, Lq, (uint32_t)lane, KVR_WAVE, &ell_sh[cur]);
+      if (nh == 0 && has_next) stage_next(a.tokens, n0, Ln, qn, qs, Lp, (uint32_t)lane, KVR_WAVE, &ell_sh[cur]);
     } else if (has_next) {
-      stage_next(a.tokens, n0, Ln, qn, qs, Lq, threadIdx.x - KVR_WAVE, blockDim.x - KVR_WAVE, &ell_sh[cur]);
+      stage_next(a.tokens, n0, Ln, qn, qs, Lp, threadIdx.x - KVR_WAVE, blockDim.x - KVR_WAVE, &ell_sh[cur]);
     }
     __syncthreads();
     if (abort_sh) break;
@@ -275,7 +291,13 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     const uint32_t nev = nev_sh;
     // draw words: RLT only
     const uint32_t rn = a.C.evict == KVR_EVICT_RLT ? (nev < a.rcap ? nev : a.rcap) : 0u;
-    const int32_t ell = ell_sh[cur];
+    const int32_t hins = hins_sh;
+    // LCP of the two paths, then of what the next match needs: the next
+    // prompt against the inserted path (routed worker) or against this
+    // prompt (every other worker, whose recorded match is of this prompt)
+    const int32_t ellp = ell_sh[cur];
+    const int32_t ell_r = ellp < Lnq ? ellp : Lnq;
+    const int32_t ell = ell_r < Lq ? ell_r : Lq;
 
     // ---- phase B.  Wave 0: the insertion, then the routed worker's h for
     // the next query.  Helpers: the insertion's draw words first, then
@@ -298,8 +320,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.ready_need = nh;
       int64_t dbg[4] = {0, 0, 0, 0};
       const uint32_t err = a.C.evict == KVR_EVICT_RLT
-                               ? rlt_insert(P, ia, qs, Lq, h_sh[cur][best], ustage, paths.of(best), dbg)
-                               : lru_insert(P, ia, qs, Lq, h_sh[cur][best], paths.of(best), dbg);
+                               ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
+                               : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
       if (lane == 0 && err) {
         if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];
@@ -313,10 +335,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         abort_sh = 1;
       }
       // the routed worker's h for the next query, from the path of the
-      // query just inserted (all of it is cached now: the old h is Lq)
+      // query just inserted (all of it is cached now: the old h is Lp)
       if (has_next && !err) {
         Ptrs Pb = worker_ptrs(a.ws, a.L, r, best);
-        count_matched(Pb, match_incremental(Pb, Pb.hdr->arena_sel, qn, Ln, Lq, ell, paths.of(best)),
+        count_matched(Pb, match_incremental(Pb, Pb.hdr->arena_sel, qn, Lnq, Lp, ell_r, paths.of(best)),
                       &h_sh[cur ^ 1u][best]);
       }
       if (nh == 0 && has_next) {
@@ -326,7 +348,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         for (uint32_t i = 0; i < W; ++i)
           if (i != best) {
             Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
+            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_sh[cur][i], ell, paths.of(i)),
                           &h_sh[cur ^ 1u][i]);
           }
       }
@@ -351,7 +373,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
           if (i >= W) break;
           if (i == best) continue;
           Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-          count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h_sh[cur][i], ell, paths.of(i)),
+          count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_sh[cur][i], ell, paths.of(i)),
                         &h_sh[cur ^ 1u][i]);
         }
       }
@@ -382,15 +404,17 @@ __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
   if (tid < RW) init_worker(worker_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
 }
 
-// Batch checks before any state changes: lengths and arrival order.
+// Batch checks before any state changes: lengths (with cached responses, a
+// prompt of at least one token before the response) and arrival order.
 __global__ void validate_kernel(char* ws, Layout L, const uint64_t* offsets, const int64_t* arrival,
-                                uint32_t n) {
+                                const uint16_t* out_len, int32_t resp, uint32_t n) {
   GlobalHdr* g = reinterpret_cast<GlobalHdr*>(ws + L.off_global);
   uint32_t bits = 0;
   for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n;
        j += (uint64_t)gridDim.x * blockDim.x) {
     const uint64_t o0 = offsets[j], o1 = offsets[j + 1];
     if (o1 <= o0 || o1 - o0 > L.maxL) bits |= KVR_DEV_BAD_LENGTH;
+    if (resp && o1 - o0 <= (uint64_t)query_out_len(out_len, j)) bits |= KVR_DEV_BAD_LENGTH;
     const int64_t prev = j == 0 ? g->last_arrival : arrival[j - 1];
     if (arrival[j] < prev) bits |= KVR_DEV_BAD_ARRIVAL;
   }
@@ -436,7 +460,7 @@ hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st)
 hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   const uint32_t blocks_v = (a.n + 255) / 256 < 1024 ? (a.n + 255) / 256 : 1024;
   hipLaunchKernelGGL(validate_kernel, dim3(blocks_v ? blocks_v : 1), dim3(256), 0, st, a.ws, a.L,
-                     a.offsets, a.arrival, a.n);
+                     a.offsets, a.arrival, a.out_len, a.C.cache_responses, a.n);
   hipLaunchKernelGGL(validate_tokens_kernel, dim3(1024), dim3(256), 0, st, a.ws, a.L, a.tokens,
                      a.offsets, a.n);
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;

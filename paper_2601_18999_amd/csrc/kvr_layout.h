@@ -123,6 +123,8 @@ struct Consts {
   int32_t router;
   int32_t ca_balance_abs;
   double ca_balance_rel, ca_cache_threshold;
+  int32_t cache_responses;  // 1: a path is prompt || response (the last out_len tokens)
+  int32_t pad;
 };
 
 // Arguments of one batch for the step kernel (device pointers).

@@ -29,6 +29,8 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   C.true_out_us = cfg->true_out_us;
   C.update = cfg->update;
   C.evict = cfg->evict;
+  C.cache_responses = cfg->cache_responses;
+  const bool resp = cfg->cache_responses != 0;
   const uint32_t W = L.W;
   // candidate list staging buffer (LDS on the device)
   const uint32_t ucap = ucap_in;
@@ -63,7 +65,9 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), arrival[0], tprev);
       for (uint32_t i = 0; i < W; ++i) {
         Ptrs P = worker_ptrs(ws, L, r, i);
-        h[0][i] = match_lcp(P, P.hdr->arena_sel, tokens + offsets[0], (int32_t)(offsets[1] - offsets[0]), path_of(i));
+        const int32_t L0 = (int32_t)(offsets[1] - offsets[0]);
+        h[0][i] = match_lcp(P, P.hdr->arena_sel, tokens + offsets[0], resp ? L0 - query_out_len(out_len, 0) : L0,
+                            path_of(i));
         P.hdr->matched_tokens += (uint64_t)h[0][i];
       }
     }
@@ -71,12 +75,15 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
     for (uint64_t j = 0; j < n; ++j) {
       const int cur = (int)(j & 1u);
       const int32_t* qs = tokens + offsets[j];
-      const int32_t Lq = (int32_t)(offsets[j + 1] - offsets[j]);
+      // path Lp (inserted) and prompt Lq (matched, scored, committed)
+      const int32_t Lp = (int32_t)(offsets[j + 1] - offsets[j]);
       const int64_t t = arrival[j];
-      const int32_t olen = out_len ? (int32_t)out_len[j] : 4;
+      const int32_t olen = query_out_len(out_len, j);
+      const int32_t Lq = resp ? Lp - olen : Lp;
       const bool has_next = j + 1 < n;
       const int32_t* qn = has_next ? tokens + offsets[j + 1] : nullptr;
       const int32_t Ln = has_next ? (int32_t)(offsets[j + 2] - offsets[j + 1]) : 0;
+      const int32_t Lnq = has_next && resp ? Ln - query_out_len(out_len, j + 1) : Ln;
       double eh[kMaxWorkers], ch[kMaxWorkers];
       if (stale >= 0) {
         Ptrs P = worker_ptrs(ws, L, r, (uint32_t)stale);
@@ -117,16 +124,22 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       if (hits) hits[r * n + j] = h[cur][best];
       if (all_hits)
         for (uint32_t i = 0; i < W; ++i) all_hits[(r * n + j) * W + i] = h[cur][i];
-      // LCP of this query and the next
-      int32_t ell = 0;
+      // LCP of this path and the next; then of the next prompt with this
+      // path (routed worker) and with this prompt (the others)
+      int32_t ellp = 0;
       if (has_next) {
-        const int32_t m = Lq < Ln ? Lq : Ln;
-        while (ell < m && qs[ell] == qn[ell]) ++ell;
+        const int32_t m = Lp < Ln ? Lp : Ln;
+        while (ellp < m && qs[ellp] == qn[ellp]) ++ellp;
       }
+      const int32_t ell_r = ellp < Lnq ? ellp : Lnq;
+      const int32_t ell = ell_r < Lq ? ell_r : Lq;
+      // the cached length of the whole path, continued from the prompt's match
+      int32_t hins = h[cur][best];
+      if (resp && hins == Lq && Lp > Lq) hins = match_incremental(P, P.hdr->arena_sel, qs, Lp, Lq, Lq, path_of(best));
       if (!err) {
         // high halves of the insertion's draw words, as the helper waves
         // compute them on the device
-        const uint32_t nload = (uint32_t)(Lq - h[cur][best]);
+        const uint32_t nload = (uint32_t)(Lp - hins);
         const uint32_t nfree = L.B - P.hdr->size;
         const uint32_t nev = nload > nfree ? nload - nfree : 0u;
         rwbuf.resize(nev ? nev : 1);
@@ -141,8 +154,8 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.rw = rwbuf.data();
         ia.ready = nullptr;
         ia.ready_need = 0;
-        err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lq, h[cur][best], ustage, path_of(best), nullptr)
-                                       : lru_insert(P, ia, qs, Lq, h[cur][best], path_of(best), nullptr);
+        err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, path_of(best), nullptr)
+                                       : lru_insert(P, ia, qs, Lp, hins, path_of(best), nullptr);
       }
       if (err) return (int)err;
       if (has_next) {
@@ -150,13 +163,13 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         for (uint32_t i = 0; i < W; ++i) {
           if (i == best) continue;
           Ptrs Pi = worker_ptrs(ws, L, r, i);
-          h[cur ^ 1][i] = match_incremental(Pi, Pi.hdr->arena_sel, qn, Ln, h[cur][i], ell, path_of(i));
+          h[cur ^ 1][i] = match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h[cur][i], ell, path_of(i));
           Pi.hdr->matched_tokens += (uint64_t)h[cur ^ 1][i];
         }
       }
       stale = (int32_t)best;
-      Lprev = Lq;
-      ell_prev = ell;
+      Lprev = Lp;
+      ell_prev = ell_r;
       tprev = t;
     }
   }

@@ -25,36 +25,42 @@ from gpu_helpers import compare_worker, note
 pytestmark = pytest.mark.gpu
 
 BATCH = 2000
-# (config, sampled replicas, prefix compared with the oracle, eviction)
+# (config, sampled replicas, prefix compared with the oracle, eviction,
+# cached responses: every turn's 4-token response is cached with its prompt
+# and is part of the next turn's prompt)
 CASES = [
-    (3, [0, 85, 170, 255], 24000, "rlt"),
-    (4, [0, 42, 127], 24000, "rlt"),
-    (5, [0, 31], 8000, "rlt"),
-    (3, [0, 255], 24000, "lru"),
-    (5, [0, 31], 8000, "lru"),
+    (3, [0, 85, 170, 255], 24000, "rlt", 0),
+    (4, [0, 42, 127], 24000, "rlt", 0),
+    (5, [0, 31], 8000, "rlt", 0),
+    (3, [0, 255], 24000, "lru", 0),
+    (5, [0, 31], 8000, "lru", 0),
+    (4, [0, 127], 24000, "rlt", 1),
 ]
 
 
-def _oracle_many(stream, W, B, replicas, n, evict):
+def _oracle_many(stream, W, B, replicas, n, evict, resp):
     with cf.ThreadPoolExecutor(max_workers=len(replicas)) as ex:
-        futs = {r: ex.submit(O.run, stream, W, B, replica=r, n=n, all_hits=True, evict=evict) for r in replicas}
+        futs = {r: ex.submit(O.run, stream, W, B, replica=r, n=n, all_hits=True, evict=evict,
+                             cache_responses=resp) for r in replicas}
         return {r: f.result() for r, f in futs.items()}
 
 
-@pytest.mark.parametrize("cfg,replicas,nprefix,evict", CASES, ids=[f"config{c[0]}-{c[3]}" for c in CASES])
-def test_full_size(cfg, replicas, nprefix, evict):
+@pytest.mark.parametrize("cfg,replicas,nprefix,evict,resp", CASES,
+                         ids=[f"config{c[0]}-{c[3]}" + ("-responses" if c[4] else "") for c in CASES])
+def test_full_size(cfg, replicas, nprefix, evict, resp):
     p = PRESETS[cfg]
     R, W, B = p["R"], p["W"], p["B"]
     t0 = time.time()
-    s = generate(p["stream"])
+    s = generate(dict(p["stream"], responses=True) if resp else p["stream"])
     note(f"config {cfg}: R={R} W={W} B={B} n={s.n} tokens={s.tokens.size} ({time.time() - t0:.1f} s)")
     assert nprefix % BATCH == 0 and nprefix < s.n
 
     # the oracle runs on host threads while the GPU works
     pool = cf.ThreadPoolExecutor(max_workers=1)
-    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix, evict)
+    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix, evict, resp)
 
-    sim = K.Simulator(R, W, B, s.max_len, evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict])
+    sim = K.Simulator(R, W, B, s.max_len, evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict],
+                      cache_responses=resp)
     try:
         ds = sim.upload(s)
         route = np.empty((R, s.n), np.int32)
@@ -103,7 +109,8 @@ def test_full_size(cfg, replicas, nprefix, evict):
         assert (route == route[0:1]).all() and (hits == hits[0:1]).all()
 
     # ---- whole stream: properties
-    lens = s.lengths.astype(np.int64)
+    paths = s.lengths.astype(np.int64)
+    lens = paths - s.out_len.astype(np.int64) if resp else paths  # the prompts
     assert ((route >= 0) & (route < W)).all()
     assert ((hits >= 0) & (hits <= lens[None, :])).all()
     for r in range(R):
@@ -119,7 +126,11 @@ def test_full_size(cfg, replicas, nprefix, evict):
         assert sum(w["prompt_tokens"] for w in ws) == int(lens.sum()), r
         per_w_prompt = np.bincount(route[r], weights=lens, minlength=W)
         assert [w["prompt_tokens"] for w in ws] == per_w_prompt.astype(np.int64).tolist(), r
-        # every routed query's missed tokens are loaded
-        miss = np.bincount(route[r], weights=lens - hits[r], minlength=W).astype(np.int64)
-        assert [w["loads"] for w in ws] == miss.tolist(), r
+        # every routed query's missed tokens are loaded (with responses, the
+        # part of the path after a wholly cached prompt may be cached too)
+        miss = np.bincount(route[r], weights=paths - hits[r], minlength=W).astype(np.int64)
+        if resp:
+            assert all(w["loads"] <= m for w, m in zip(ws, miss.tolist())), r
+        else:
+            assert [w["loads"] for w in ws] == miss.tolist(), r
     note(f"  evictions on the GPU: {sum(w['evictions'] for rr in stats for w in rr)}")

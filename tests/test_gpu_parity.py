@@ -274,3 +274,57 @@ def test_baseline_router_parity(router, evict):
         res, stats = gpu_run(s, 3, W, B, seed=case, router=ROUTER[router], ca_balance_abs=ab,
                              evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict])
         assert_parity(s, res, stats, W, B, range(3), seed=case, evict=evict, router=router, ca_balance_abs=ab)
+
+
+# ---------------------------------------------------------------- cached responses
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_cached_responses_random_parity(evict):
+    """Complete paths q || a (Sec. 3.2): the prompt is matched and scored,
+    the whole path inserted; small vocabularies make whole-prompt hits that
+    continue into cached responses common."""
+    from streams import random_response_stream
+    rng = np.random.default_rng(61 + (evict == "lru"))
+    ev = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict]
+    for case in range(4):
+        B = int(rng.integers(20, 300))
+        s = random_response_stream(rng, int(rng.integers(100, 400)), int(rng.integers(2, 6)), 40, 12, B)
+        W = int(rng.integers(1, 5))
+        upd = ["nlms", "rls", "none"][case % 3]
+        note(f"responses/{evict} case {case}: W={W} B={B} n={s.n} update={upd}")
+        res, stats = gpu_run(s, 3, W, B, update=upd, seed=case, evict=ev, cache_responses=1)
+        assert_parity(s, res, stats, W, B, range(3), update=upd, seed=case, evict=evict, cache_responses=1)
+        prompts = s.lengths - s.out_len.astype(np.int64)
+        assert (res["hits"] <= prompts[None, :]).all()
+
+
+@pytest.mark.parametrize("router", ["lbgr", "cache_aware"])
+def test_cached_responses_multiturn_parity(router):
+    """Multi-turn sessions whose responses are part of the next turn's
+    prompt, with the whole path cached, under eviction pressure; batches of
+    250 so staging crosses batch boundaries."""
+    sp = {"kind": "sessions", "n_sessions": 300, "turns": (1, 8), "start_len": 64, "ext_len": (8, 96),
+          "vocab": 32000, "responses": True, "out_len": 4, "turn_rate": 1.0, "seed": 3}
+    s = generate(sp)
+    W, B, R = 4, 3000, 4
+    note(f"responses multiturn/{router}: n={s.n} max_len={s.max_len}")
+    res, stats = gpu_run(s, R, W, B, batch=250, router=ROUTER.get(router, K.KVR_ROUTE_LBGR), cache_responses=1)
+    assert_parity(s, res, stats, W, B, range(R), router=router, cache_responses=1)
+    assert sum(w["evictions"] for w in stats[0]) > B
+
+
+def test_cached_responses_invalid_path_rejected():
+    """A path no longer than its response (an empty prompt) is rejected as a
+    whole before any state changes."""
+    s = generate(small_spec(n=50, groups=3, prefix_len=(2, 8), suffix_len=(1, 4), vocab=9))
+    s.out_len = np.full(s.n, 2, dtype=np.uint16)
+    s.out_len[17] = int(s.lengths[17])
+    sim = K.Simulator(2, 2, 100, s.max_len, cache_responses=1)
+    try:
+        ds = sim.upload(s)
+        sim.route(ds, 0, s.n)
+        st, bits = sim.check()
+        assert st == K.KVR_EINVAL and bits & 1, (st, bits)
+        assert all(w["routed"] == 0 for rr in sim.stats(check=False) for w in rr)
+    finally:
+        sim.close()

@@ -8,6 +8,7 @@ import pytest
 import emul_kernel as E
 from oracle import oracle as O
 from workload import PRESETS, generate, small_spec
+from streams import random_response_stream
 
 
 ROUTERS = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
@@ -19,7 +20,7 @@ def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", router="
     assert e["rc"] == 0
     for r in range(R):
         o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict, router=router,
-                  **{k: v for k, v in cfg.items() if k.startswith("ca_")})
+                  **{k: v for k, v in cfg.items() if k.startswith("ca_") or k == "cache_responses"})
         np.testing.assert_array_equal(e["route"][r], o["route"])
         np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
         for i in range(W):
@@ -147,3 +148,41 @@ def test_baseline_routers(router, evict):
         W = int(rng.integers(1, 6))
         B = int(max(s.max_len, rng.integers(2, 150)))
         _compare(s, 2, W, B, seed=case, evict=evict, router=router, ca_balance_abs=int(rng.integers(0, 6)))
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_cached_responses_random_paths(evict):
+    """Complete paths q || a (Sec. 3.2): matches and scores on the prompt,
+    insertion of the whole path, continued into a cached response whenever
+    the whole prompt hits."""
+    rng = np.random.default_rng(31 + (evict == "lru"))
+    full_prompt_hits = 0
+    for case in range(60):
+        B = int(rng.integers(6, 60))
+        s = random_response_stream(rng, int(rng.integers(10, 120)), int(rng.integers(2, 5)), 12, 4, B)
+        W = int(rng.integers(1, 4))
+        e = _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case, evict=evict,
+                     cache_responses=1)
+        prompts = s.lengths - s.out_len.astype(np.int64)
+        full_prompt_hits += int((e["hits"][0] == prompts).sum())
+    assert full_prompt_hits > 100
+
+
+@pytest.mark.parametrize("router", ["lbgr", "cache_aware"])
+def test_cached_responses_multiturn_sessions(router):
+    """Multi-turn sessions whose responses are part of the next turn's
+    prompt, under eviction pressure."""
+    sp = {"kind": "sessions", "n_sessions": 60, "turns": (1, 6), "start_len": 20, "ext_len": (2, 30),
+          "vocab": 50, "responses": True, "out_len": 6, "turn_rate": 2.0, "seed": 5}
+    s = generate(sp)
+    W, B = 3, 600
+    e = _compare(s, 2, W, B, router=router, cache_responses=1)
+    assert sum(w["evictions"] for w in e["workers"][0]) > 0
+
+
+def test_cached_responses_collector():
+    rng = np.random.default_rng(8)
+    s = random_response_stream(rng, 400, 3, 40, 12, 200)
+    B = 200
+    e = _compare(s, 2, 2, B, cache_responses=1, arena_words=B + 2 * s.max_len + 64)
+    assert sum(w["gc_runs"] for rr in e["workers"] for w in rr) > 10
