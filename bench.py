@@ -57,7 +57,8 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr", responses: int = 0):
+def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr", responses: int = 0,
+                 beta: int = 1):
     """The CPU oracle, single-threaded, on replica 0 of the same stream: the
     first n queries, n grown until one run takes at least budget_s (the cost
     per query grows as the caches fill, so the last steps grow by 1.4x)."""
@@ -65,7 +66,7 @@ def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str 
     n = min(1000, stream.n)
     while True:
         t0 = time.perf_counter()
-        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses)
+        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses, batch_size=beta)
         dt = time.perf_counter() - t0
         log(f"cpu oracle: {n} queries in {dt:.1f} s")
         if dt >= budget_s or n >= stream.n:
@@ -139,6 +140,9 @@ def main() -> int:
     ap.add_argument("--responses", action="store_true",
                     help="cache complete token paths q||a (each query followed by its response; in the "
                          "multi-turn workload a turn's response is part of the next prompt)")
+    ap.add_argument("--beta", type=int, default=1,
+                    help="continuous batching: the batch size beta (the last beta-1 paths routed to a "
+                         "worker are never evicted); 1 = single-query processing")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -176,7 +180,7 @@ def main() -> int:
     router = {"lbgr": K.KVR_ROUTE_LBGR, "random": K.KVR_ROUTE_RANDOM, "round_robin": K.KVR_ROUTE_ROUND_ROBIN,
               "cache_aware": K.KVR_ROUTE_CACHE_AWARE}[args.router]
     sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router,
-                      cache_responses=int(args.responses))
+                      cache_responses=int(args.responses), batch_size=args.beta)
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -223,7 +227,8 @@ def main() -> int:
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
-    traffic = load_traffic(workload) if (args.evict, args.router, args.responses) == ("rlt", "lbgr", False) else None
+    default_run = (args.evict, args.router, args.responses, args.beta) == ("rlt", "lbgr", False, 1)
+    traffic = load_traffic(workload) if default_run else None
     line = {
         "metric": "routed queries/sec",
         "value": nq / (kernel_ms * 1e-3),
@@ -238,7 +243,8 @@ def main() -> int:
         "dtype": "i32+f64",
         "data": "synthetic",
         "config": {"workload": workload + ("_responses" if args.responses else ""), "eviction": args.evict,
-                   "router": args.router, "cached_responses": bool(args.responses), "replicas": R,
+                   "router": args.router, "cached_responses": bool(args.responses), "batch_size": args.beta,
+                   "replicas": R,
                    "workers": W, "cache_tokens": B,
                    "batch_queries": args.batch, "timed_queries": q - q0,
                    "first_timed_query": q0, "stream_queries": stream.n},
@@ -265,7 +271,7 @@ def main() -> int:
         del src, dst
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router,
-                                            int(args.responses))
+                                            int(args.responses), args.beta)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 3u
+#define KVR_ABI_VERSION 4u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -126,7 +126,16 @@ typedef struct kvr_config {
    * take the whole path.  Every path must then be longer than its response
    * (a prompt of >= 1 token), and max_query_tokens bounds the path. */
   int32_t cache_responses;
-  int32_t pad1;
+  /* Continuous batching with batch size beta (Sec. 3.2, Theorem 2): the
+   * beta - 1 queries routed to a worker before the one being inserted form
+   * its running batch, and no token on their paths is evicted; a path leaves
+   * the running batch when beta - 1 later queries have been routed to that
+   * worker.  1 (default) = single-query processing, where only the
+   * insertion point is protected.  1..256, and batch_size *
+   * max_query_tokens <= cache_tokens (the paper's assumption beta * L_max <=
+   * B, so a full cache always has an evictable leaf).  Matching, routing and
+   * the observed latency do not change. */
+  int32_t batch_size;
 } kvr_config;
 
 /* Final per-(replica, worker) state and counters (kvr_stats). */

@@ -36,6 +36,11 @@
 //     (the response is not known when the query is routed);
 //   - the insertion point (the parent of the token being loaded) is never
 //     evicted while its child is loaded, so the tree stays prefix-closed;
+//   - with continuous batching of batch size beta the running batch of a
+//     worker is the beta - 1 queries routed to it before the current one:
+//     their whole paths are pinned (no token on them is evicted), and a
+//     path is released when beta - 1 later queries have been routed there;
+//     batching changes nothing else (matching, routing, observed latency);
 //   - "uniformly at random" = index floor(r * |U| / 2^64) into U sorted by
 //     root path, r = word 0 of Philox4x64-10 with key (seed, replica) and
 //     counter (global query index, worker, draw index, 0);
@@ -97,7 +102,11 @@ typedef struct orc_config {
   double ca_cache_threshold;  // cache-aware: best hit / |q| above this routes to the best hit
   // 1 = a path is q_j || a_j with |a_j| = out_len[j]; insert all of it
   int32_t cache_responses;
-  int32_t pad1;
+  // continuous batching with batch size beta (Sec. 3.2, Theorem 2): the
+  // paths of the beta - 1 queries routed to a worker before the one being
+  // inserted are in progress there and none of their tokens is evicted;
+  // 1 = single-query processing (only the insertion point is protected)
+  int32_t batch_size;
 } orc_config;
 
 typedef struct orc_worker_stats {
@@ -168,6 +177,7 @@ struct Node {
   int32_t parent = -1;
   uint32_t mark = 0;      // phase in which the token was last marked (0 = never)
   uint64_t stamp = 0;     // L-LRU access stamp
+  uint32_t pin = 0;       // number of in-progress paths through this token
   bool alive = false;
   std::map<int32_t, int32_t> kids;  // child token -> node id, ordered
 };
@@ -194,6 +204,7 @@ struct Worker {
   int64_t tl = 0;              // time of the last decay (us)
   int64_t Wb = 0;              // observed-latency backlog (us)
   std::deque<Pending> pend;
+  std::deque<std::vector<int32_t>> running;  // paths of the running batch (oldest first)
   orc_worker_stats st;
 };
 
@@ -219,6 +230,7 @@ int32_t new_node(Worker& w, int32_t tok, int32_t parent) {
   n.parent = parent;
   n.mark = 0;
   n.stamp = 0;
+  n.pin = 0;
   n.alive = true;
   n.kids.clear();
   w.nodes[parent].kids[tok] = id;
@@ -238,8 +250,9 @@ void remove_leaf(Worker& w, int32_t id) {
 bool is_leaf(const Worker& w, int32_t id) { return id != 0 && w.nodes[id].kids.empty(); }
 
 // U by definition: the leaf tokens of S that are not marked in the current
-// phase, minus the pinned insertion point, in lexicographic order of their
-// root paths (= pre-order of a depth-first walk with ordered children).
+// phase, minus the pinned insertion point and the tokens of in-progress
+// paths, in lexicographic order of their root paths (= pre-order of a
+// depth-first walk with ordered children).
 std::vector<int32_t> candidates(const Worker& w, int32_t pinned) {
   std::vector<int32_t> out, stack;
   stack.push_back(0);
@@ -248,7 +261,7 @@ std::vector<int32_t> candidates(const Worker& w, int32_t pinned) {
     stack.pop_back();
     const Node& n = w.nodes[x];
     if (x != 0 && n.kids.empty()) {
-      if (n.mark != w.phase && x != pinned) out.push_back(x);
+      if (n.mark != w.phase && x != pinned && n.pin == 0) out.push_back(x);
       continue;
     }
     for (auto it = n.kids.rbegin(); it != n.kids.rend(); ++it) stack.push_back(it->second);
@@ -352,7 +365,8 @@ void insert_rlt(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
       if (s.cfg.u_mode == 0) {
         // the parent of the evicted leaf takes its place in the ordered list
         // if it is now an unmarked, unpinned leaf; otherwise the entry goes.
-        if (par != 0 && w.nodes[par].kids.empty() && w.nodes[par].mark != w.phase && par != u)
+        if (par != 0 && w.nodes[par].kids.empty() && w.nodes[par].mark != w.phase && par != u &&
+            w.nodes[par].pin == 0)
           w.U[k] = par;
         else
           w.U.erase(w.U.begin() + (long)k);
@@ -397,12 +411,12 @@ void insert_lru(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
       if (scan) {
         for (int32_t x = 1; x < (int32_t)w.nodes.size(); ++x) {
           const Node& n = w.nodes[x];
-          if (!n.alive || !n.kids.empty() || x == u) continue;
+          if (!n.alive || !n.kids.empty() || x == u || n.pin > 0) continue;
           if (best < 0 || n.stamp < w.nodes[best].stamp) best = x;
         }
       } else {
         for (auto jt = w.lru_leaves.begin(); jt != w.lru_leaves.end(); ++jt)
-          if (jt->second != u) {
+          if (jt->second != u && w.nodes[jt->second].pin == 0) {
             best = jt->second;
             break;
           }
@@ -459,6 +473,38 @@ void online_update(Sim& s, Worker& w, const double phi[4], double e) {
 }
 
 int64_t tick(const orc_config& c, int64_t t) { return t / c.decay_interval_us; }
+
+// Add d to the in-progress count of every token of path q (all cached).
+void pin_path(Sim& s, Worker& w, const std::vector<int32_t>& q, int d) {
+  int32_t u = 0;
+  for (int32_t tok : q) {
+    auto it = w.nodes[u].kids.find(tok);
+    if (it == w.nodes[u].kids.end()) {
+      s.error |= 2;  // an in-progress token was evicted
+      return;
+    }
+    u = it->second;
+    w.nodes[u].pin = (uint32_t)((int64_t)w.nodes[u].pin + d);
+    // a released leaf that is not marked is a candidate again: the ordered
+    // list is rebuilt from its definition at the next draw
+    if (d < 0 && w.nodes[u].pin == 0 && w.nodes[u].kids.empty() && w.nodes[u].mark != w.phase)
+      w.U_valid = false;
+  }
+}
+
+// The path just inserted joins the running batch of worker i; the oldest
+// path leaves it once beta - 1 later ones are running.
+void batch_admit(Sim& s, uint32_t i, const int32_t* q, int32_t L) {
+  const uint32_t beta = s.cfg.batch_size;
+  if (beta <= 1) return;
+  Worker& w = s.w[i];
+  w.running.emplace_back(q, q + L);
+  pin_path(s, w, w.running.back(), +1);
+  if (w.running.size() > beta - 1) {
+    pin_path(s, w, w.running.front(), -1);
+    w.running.pop_front();
+  }
+}
 
 // Query jg: prompt q[0, L), inserted path q[0, Lpath) (Lpath = L unless
 // responses are cached), arrival t, output length o.
@@ -575,11 +621,13 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int32_t Lpath, int64
   if ((uint64_t)e_us > w.st.latency_max_us) w.st.latency_max_us = (uint64_t)e_us;
   if (route_out) *route_out = (int32_t)best;
   if (hit_out) *hit_out = (int32_t)hb;
-  // 6. insert the path into the routed worker's cache
+  // 6. insert the path into the routed worker's cache; it joins that
+  // worker's running batch
   if (c.evict == 0)
     insert_rlt(s, best, q, Lpath, jg);
   else
     insert_lru(s, best, q, Lpath, jg);
+  if (!s.error) batch_admit(s, best, q, Lpath);
 }
 
 // Per-token path hash H(v) = mix64(H(parent) + GOLDEN * (tok + 1)), H(root) = 0.
@@ -619,6 +667,20 @@ bool check_invariants(const Sim& s) {
     }
     if (alive != w.size) return false;
     if (s.cfg.evict == 0 && marked != w.cnt) return false;  // T is a subset of S after an insert
+    // the running batch is cached whole, and the in-progress counts are
+    // exactly the number of running paths through each token
+    std::vector<uint32_t> pins(w.nodes.size(), 0);
+    for (const auto& q : w.running) {
+      int32_t u = 0;
+      for (int32_t tok : q) {
+        auto it = w.nodes[u].kids.find(tok);
+        if (it == w.nodes[u].kids.end()) return false;
+        u = it->second;
+        pins[u] += 1;
+      }
+    }
+    for (size_t x = 1; x < w.nodes.size(); ++x)
+      if (w.nodes[x].alive && w.nodes[x].pin != pins[x]) return false;
     if (w.P < 0.0) return false;
   }
   return true;

@@ -45,7 +45,7 @@ class OrcConfig(ctypes.Structure):
         ("ca_balance_rel", ctypes.c_double),
         ("ca_cache_threshold", ctypes.c_double),
         ("cache_responses", ctypes.c_int32),
-        ("pad1", ctypes.c_int32),
+        ("batch_size", ctypes.c_int32),
     ]
 
 
@@ -96,7 +96,7 @@ DEFAULTS: Dict[str, Any] = dict(
     lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
     true_cached_us=0, true_miss_us=1000, true_out_us=10000,
     router="lbgr", ca_balance_abs=32, ca_balance_rel=1.0001, ca_cache_threshold=0.5,
-    cache_responses=0)
+    cache_responses=0, batch_size=1)
 
 ROUTER = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
 
@@ -121,6 +121,7 @@ def make_config(W: int, B: int, **kw) -> OrcConfig:
     c.ca_balance_rel = float(p["ca_balance_rel"])
     c.ca_cache_threshold = float(p["ca_cache_threshold"])
     c.cache_responses = int(p["cache_responses"])
+    c.batch_size = int(p["batch_size"])
     return c
 
 

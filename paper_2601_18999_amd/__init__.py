@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVIC
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 3
+KVR_ABI_VERSION = 4
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
@@ -57,7 +57,7 @@ class KvrConfig(ctypes.Structure):
         ("ca_balance_rel", ctypes.c_double),
         ("ca_cache_threshold", ctypes.c_double),
         ("cache_responses", ctypes.c_int32),
-        ("pad1", ctypes.c_int32),
+        ("batch_size", ctypes.c_int32),
     ]
 
 

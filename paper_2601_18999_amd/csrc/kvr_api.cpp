@@ -69,6 +69,9 @@ kvr_status validate(const kvr_config* c) {
       (c->ca_balance_abs < 0 || !(c->ca_balance_rel >= 0.0) || !(c->ca_cache_threshold >= 0.0)))
     return fail(KVR_EINVAL, "cache-aware thresholds must be >= 0");
   if (c->cache_responses != 0 && c->cache_responses != 1) return fail(KVR_EINVAL, "cache_responses must be 0 or 1");
+  if (c->batch_size < 1 || c->batch_size > 256) return fail(KVR_EINVAL, "batch_size must be in 1..256");
+  if ((uint64_t)c->batch_size * c->max_query_tokens > c->cache_tokens)
+    return fail(KVR_EINVAL, "batch_size * max_query_tokens must not exceed cache_tokens");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
   if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
@@ -136,7 +139,7 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->ca_balance_rel = 1.0001;
   c->ca_cache_threshold = 0.5;
   c->cache_responses = 0;
-  c->pad1 = 0;
+  c->batch_size = 1;
   c->update = KVR_UPD_NLMS;
   c->pending_capacity = 65536;
   c->node_capacity = 0;

@@ -113,7 +113,9 @@ struct Ptrs {
   PendRec* pend;
   uint64_t* scratch;
   int32_t* stamp0;  // L-LRU: last access of each arena word (semispace 1 at + A); null for RLT
-  uint32_t A, NC, PC;
+  int32_t* pin;     // continuous batching: running paths through each node; null otherwise
+  int32_t* run;     // continuous batching: end nodes of the running batch (ring of beta - 1)
+  uint32_t A, NC, PC, beta;
 };
 
 __device__ __forceinline__ Ptrs worker_ptrs(char* ws, const Layout& L, uint32_t r, uint32_t i) {
@@ -126,12 +128,19 @@ __device__ __forceinline__ Ptrs worker_ptrs(char* ws, const Layout& L, uint32_t 
   P.U = reinterpret_cast<int32_t*>(ws + L.off_U + w * L.leaf_stride);
   P.pend = reinterpret_cast<PendRec*>(ws + L.off_pend + w * L.pend_stride);
   P.scratch = reinterpret_cast<uint64_t*>(ws + L.off_scratch + w * L.scratch_stride);
-  P.stamp0 = L.off_stamp < L.total ? reinterpret_cast<int32_t*>(ws + L.off_stamp + w * L.arena_stride) : nullptr;
+  P.stamp0 = L.has_stamp ? reinterpret_cast<int32_t*>(ws + L.off_stamp + w * L.arena_stride) : nullptr;
+  P.pin = L.beta > 1 ? reinterpret_cast<int32_t*>(ws + L.off_pin + w * L.pin_stride) : nullptr;
+  P.run = L.beta > 1 ? reinterpret_cast<int32_t*>(ws + L.off_run + w * L.run_stride) : nullptr;
   P.A = L.A;
   P.NC = L.NC;
   P.PC = L.PC;
+  P.beta = L.beta;
   return P;
 }
+
+// Is node x on a path of the worker's running batch (continuous batching)?
+// Such a node is never evicted, and is no candidate while it is a leaf.
+__device__ __forceinline__ bool pinned(const Ptrs& P, int32_t x) { return P.pin != nullptr && P.pin[x] > 0; }
 
 // Wave-uniform copy of the cache part of a worker header.
 struct St {
@@ -642,6 +651,8 @@ __device__ __forceinline__ int32_t split_node(const Ptrs& P, St& s, int32_t x, i
   }
   node_put(P, hd, nh);
   node_put(P, x, nt);
+  // every running path through x passes through its head
+  if (P.pin != nullptr && lane_id() == 0) P.pin[hd] = P.pin[x];
   if (!child_replace(P, s, nx.parent, x, hd)) {
     KVR_FAIL_CHECK(s, 3, x, nx.parent, hd);
     return -1;
@@ -676,8 +687,9 @@ __device__ __forceinline__ void path_add(const PathRef& pr, int32_t& pc, int32_t
 
 // ---------------------------------------------------------------- RLT pieces
 
-// U := the leaves (other than `excl`) whose leaf token is unmarked, in the
-// order of the leaf list (lexicographic order of root paths).
+// U := the leaves (other than `excl` and the running batch's nodes) whose
+// leaf token is unmarked, in the order of the leaf list (lexicographic order
+// of root paths).
 __device__ __forceinline__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
   constexpr int kUnroll = 4;  // four chunks of the leaf list per round trip
   uint32_t n = 0;
@@ -689,12 +701,18 @@ __device__ __forceinline__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
       id[v] = k < s.nleaves ? P.leaf[k] : -1;
     }
     NodeRec nd[kUnroll];
-#pragma unroll
-    for (int v = 0; v < kUnroll; ++v)
-      if (id[v] > 0 && id[v] != excl) nd[v] = P.nodes[id[v]];
+    bool pn[kUnroll];
 #pragma unroll
     for (int v = 0; v < kUnroll; ++v) {
-      const bool cand = id[v] > 0 && id[v] != excl && !is_marked(s, nd[v], id[v], nd[v].len - 1);
+      pn[v] = false;
+      if (id[v] > 0 && id[v] != excl) {
+        nd[v] = P.nodes[id[v]];
+        pn[v] = pinned(P, id[v]);
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < kUnroll; ++v) {
+      const bool cand = id[v] > 0 && id[v] != excl && !pn[v] && !is_marked(s, nd[v], id[v], nd[v].len - 1);
       const uint64_t m = __ballot(cand);
       if (cand) P.U[n + (uint32_t)__popcll(m & lanemask_lt())] = id[v];
       n += (uint32_t)__popcll(m);
@@ -707,7 +725,8 @@ __device__ __forceinline__ void rebuild_U(const Ptrs& P, St& s, int32_t excl) {
 
 // The candidate at U[kk], node n with parent p, has just lost its last
 // token: drop it from the tree and the leaf list; its parent, if that became
-// an unmarked leaf, takes its place (and rank) in U, else the entry goes.
+// an unmarked leaf off the running batch, takes its place (and rank) in U,
+// else the entry goes.
 __device__ __forceinline__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk, int32_t n, int32_t p) {
   int32_t li = arr_find(P.leaf, s.nleaves, n);
   if (li < 0) {
@@ -723,7 +742,7 @@ __device__ __forceinline__ bool remove_emptied(const Ptrs& P, St& s, uint32_t kk
   if (p != 0 && np.nchild == 0) {
     if (lane_id() == 0) P.leaf[li] = p;
     wave_mem_sync();
-    if (!is_marked(s, np, p, np.len - 1)) {
+    if (!is_marked(s, np, p, np.len - 1) && !pinned(P, p)) {
       if (lane_id() == 0) P.U[kk] = p;
       wave_mem_sync();
     } else {
@@ -1092,7 +1111,7 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
       if (lane == 0) P.leaf[li] = pf;
       wave_mem_sync();
       const int32_t ptop = mark_top(s, np, pf);
-      if (ptop < np.len) {
+      if (ptop < np.len && !pinned(P, pf)) {
         if (lane == 0) {
           u.node[kkf] = pf;
           u.len[kkf] = np.len;
@@ -1469,6 +1488,144 @@ fail:
   return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
 }
 
+// ---------------------------------------------------------------- continuous batching
+
+// Lower the in-progress count of every node from x up to the root (the
+// nodes of a path leaving the running batch).  A leaf released that way
+// whose leaf token is unmarked is a candidate again: U is rebuilt from its
+// definition at the next draw.
+__device__ __forceinline__ bool unpin_chain(const Ptrs& P, St& s, int32_t x) {
+  for (uint32_t guard = 0; x > 0; ++guard) {
+    if (guard > P.NC || (uint32_t)x >= s.hwm) {
+      KVR_FAIL_CHECK(s, 21, x, guard, 0);
+      return false;
+    }
+    const NodeRec nx = P.nodes[x];
+    const int32_t c = P.pin[x] - 1;
+    if (c < 0) {
+      KVR_FAIL_CHECK(s, 22, x, c, 0);
+      return false;
+    }
+    if (lane_id() == 0) P.pin[x] = c;
+    if (c == 0 && nx.nchild == 0 && !is_marked(s, nx, x, nx.len - 1)) s.U_valid = 0;
+    x = nx.parent;
+  }
+  return true;
+}
+
+// Continuous batching (Sec. 3.2, Theorem 2): the path q[0, L) just inserted
+// joins the worker's running batch, and once beta - 1 paths run, the oldest
+// one leaves it.  A running path ends at a node boundary, so a node is
+// either wholly on it or not: a path ending inside an edge splits the edge
+// there (splits are not semantic).  The in-progress count of every node of
+// the path is raised (one lane per node of the recorded path, else up the
+// parent chain), and the leaving path's counts are lowered.  pr holds the
+// inserted path and is updated for the split.  Returns KVR_DEV_* bits.
+__device__ __forceinline__ uint32_t batch_admit(const Ptrs& P, const PathRef& pr, const int32_t* qs, int32_t L,
+                                                int64_t* dbg) {
+  St s = load_st(P.hdr);
+  const uint32_t ring = P.beta - 1u;
+  int32_t e = -1, st = 0;
+  int32_t pc = *pr.cnt;
+  const bool have_path = pc >= 1 && pc <= kPathMax && pr.start[pc - 1] < L && pr.end[pc - 1] >= L;
+  if (have_path) {
+    e = pr.node[pc - 1];
+    st = pr.start[pc - 1];
+  } else {
+    // walk down the cached path by first tokens
+    const int32_t* ar = arena_of(P, s.arena_sel);
+    int32_t x = 0, d = 0;
+    while (d < L) {
+      const int32_t c = child_find(ar, P.nodes[x], qs[d]);
+      if (c <= 0 || (uint32_t)c >= s.hwm) {
+        KVR_FAIL_CHECK(s, 20, x, d, L);
+        goto fail;
+      }
+      const int32_t len = P.nodes[c].len;
+      if (len <= 0) {
+        KVR_FAIL_CHECK(s, 20, c, d, len);
+        goto fail;
+      }
+      if (d + len >= L) {
+        e = c;
+        st = d;
+        break;
+      }
+      d += len;
+      x = c;
+    }
+  }
+  if (e <= 0) {
+    KVR_FAIL_CHECK(s, 20, e, L, 0);
+    goto fail;
+  }
+  {
+    const int32_t elen = P.nodes[e].len;
+    if (st + elen > L) {  // the path ends inside the edge of e: split it there
+      const int32_t hd = split_node(P, s, e, L - st);
+      if (hd < 0) goto fail;
+      wave_mem_sync();
+      if (have_path && lane_id() == 0) {
+        pr.node[pc - 1] = hd;
+        pr.end[pc - 1] = L;
+      }
+      e = hd;
+    }
+  }
+  // raise the counts of the new running path
+  if (have_path && (KVR_WAVE >= kPathMax || pc <= KVR_WAVE)) {
+    for (int32_t k = lane_id(); k < pc; k += KVR_WAVE) {
+      const int32_t x = (k == pc - 1) ? e : pr.node[k];
+      P.pin[x] = P.pin[x] + 1;
+    }
+  } else {
+    int32_t x = e;
+    for (uint32_t guard = 0; x > 0; ++guard) {
+      if (guard > P.NC || (uint32_t)x >= s.hwm) {
+        KVR_FAIL_CHECK(s, 21, x, guard, 1);
+        goto fail;
+      }
+      const int32_t par = P.nodes[x].parent;
+      if (lane_id() == 0) P.pin[x] = P.pin[x] + 1;
+      x = par;
+    }
+  }
+  wave_mem_sync();
+  // the ring of end nodes: push e, release the oldest once beta - 1 run
+  {
+    WorkerHdr* w = P.hdr;
+    const uint32_t head = w->run_head, cnt = w->run_count;
+    if (cnt < ring) {
+      uint32_t slot = head + cnt;
+      if (slot >= ring) slot -= ring;
+      if (lane_id() == 0) {
+        P.run[slot] = e;
+        w->run_count = cnt + 1;
+      }
+    } else {
+      const int32_t old = P.run[head];
+      if (lane_id() == 0) {
+        P.run[head] = e;
+        w->run_head = head + 1 == ring ? 0u : head + 1;
+      }
+      if (!unpin_chain(P, s, old)) goto fail;
+    }
+  }
+  store_st(P.hdr, s);
+  wave_mem_sync();
+  return 0;
+fail:
+  if (lane_id() == 0) *pr.cnt = kPathMax + 1;
+  store_st(P.hdr, s);
+  if (dbg) {
+    dbg[0] = s.dbg_check;
+    dbg[1] = s.dbg_val[0];
+    dbg[2] = s.dbg_val[1];
+    dbg[3] = s.dbg_val[2];
+  }
+  return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
+
 // ---------------------------------------------------------------- matching
 
 // ---------------------------------------------------------------- L-LRU
@@ -1482,7 +1639,7 @@ fail:
 // stamp follow it in the eviction order: they go as one segment.
 
 // Index in the leaf list of the leaf whose last token has the oldest stamp,
-// skipping node `excl`; -1 if there is none.
+// skipping node `excl` and the running batch's nodes; -1 if there is none.
 __device__ __forceinline__ int32_t lru_pick(const Ptrs& P, const St& s, const int32_t* st, int32_t excl) {
   constexpr int kUnroll = 4;
   uint64_t best = ~0ull;  // (stamp << 32) | list index
@@ -1497,7 +1654,10 @@ __device__ __forceinline__ int32_t lru_pick(const Ptrs& P, const St& s, const in
     NodeRec nd[kUnroll];
 #pragma unroll
     for (int v = 0; v < kUnroll; ++v)
-      if (id[v] > 0) nd[v] = P.nodes[id[v]];
+      if (id[v] > 0) {
+        nd[v] = P.nodes[id[v]];
+        if (pinned(P, id[v])) id[v] = -1;  // on a running path
+      }
 #pragma unroll
     for (int v = 0; v < kUnroll; ++v) {
       const uint32_t k = b + (uint32_t)(v * KVR_WAVE) + (uint32_t)lane_id();

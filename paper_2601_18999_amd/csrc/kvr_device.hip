@@ -319,9 +319,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.ready = nh && rn ? &wready_sh : nullptr;
       ia.ready_need = nh;
       int64_t dbg[4] = {0, 0, 0, 0};
-      const uint32_t err = a.C.evict == KVR_EVICT_RLT
-                               ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
-                               : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
+      uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
+                                                : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
+      // continuous batching: the path joins the worker's running batch
+      if (!err && P.beta > 1) err = batch_admit(P, paths.of(best), qs, Lp, dbg);
       if (lane == 0 && err) {
         if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
           g->err_check = (uint32_t)dbg[0];
@@ -385,6 +386,12 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     rh->tprev = a.arrival[a.n - 1];
     if (r == 0) g->last_arrival = a.arrival[a.n - 1];
   }
+}
+
+// Zero n 32-bit words (in-progress counts of continuous batching).
+__global__ void zero_words_kernel(uint32_t* p, uint64_t n) {
+  for (uint64_t x = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n; x += (uint64_t)gridDim.x * blockDim.x)
+    p[x] = 0u;
 }
 
 __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
@@ -454,6 +461,11 @@ hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st)
   const uint64_t work = (uint64_t)L.R * L.W > L.R ? (uint64_t)L.R * L.W : L.R;
   const uint32_t blocks = (uint32_t)((work + 255) / 256);
   hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, st, ws, L, rls_p0);
+  if (L.pin_stride) {
+    const uint64_t words = (uint64_t)L.R * L.W * L.pin_stride / 4u;
+    hipLaunchKernelGGL(zero_words_kernel, dim3(1024), dim3(256), 0, st, reinterpret_cast<uint32_t*>(ws + L.off_pin),
+                       words);
+  }
   return hipGetLastError();
 }
 

@@ -19,6 +19,10 @@
 //   stats out       kvr_worker_stats staging for kvr_stats
 //   stamps          (L-LRU only) last access of every edge token, laid out
 //                   like the arenas
+//   pins            (continuous batching only) per node, the number of
+//                   paths of the worker's running batch through it
+//   running rings   (continuous batching only) the end node of each path
+//                   of the running batch, oldest first
 #ifndef KVR_LAYOUT_H
 #define KVR_LAYOUT_H
 
@@ -79,11 +83,13 @@ struct WorkerHdr {
   double Pm[16];
   int64_t tl, Wb;
   uint32_t pend_head, pend_count;
+  // continuous batching: ring of the running batch's end nodes
+  uint32_t run_head, run_count;
   // counters
   uint64_t routed, prompt_tokens, hit_tokens, matched_tokens;
   uint64_t loads, evictions, forced_resets, completions, pending_max;
   uint64_t lat_sum_us, lat_max_us, gc_runs;
-  uint8_t pad[512 - 352];
+  uint8_t pad[512 - 360];
 };
 static_assert(sizeof(WorkerHdr) == 512, "worker header is 512 bytes");
 
@@ -107,10 +113,11 @@ static_assert(sizeof(GlobalHdr) == 64, "global header is 64 bytes");
 
 struct Layout {
   uint32_t R, W, B, maxL, NC, A, PC;
-  uint32_t pad0;
+  uint32_t beta;  // batch size of continuous batching (1: single-query processing)
   uint64_t off_global, off_rhdr, off_whdr, off_nodes, off_arena, off_leaf, off_U, off_pend,
-      off_scratch, off_stats, off_stamp, total;
-  uint64_t node_stride, arena_stride, leaf_stride, pend_stride, scratch_stride;
+      off_scratch, off_stats, off_stamp, off_pin, off_run, total;
+  uint64_t node_stride, arena_stride, leaf_stride, pend_stride, scratch_stride, pin_stride, run_stride;
+  uint32_t has_stamp, pad0;
 };
 
 // Constants of one run, passed by value to the kernels.
@@ -161,6 +168,7 @@ inline Layout make_layout(const kvr_config& c) {
   L.A = c.arena_words ? c.arena_words : (uint32_t)dflt_arena;
   L.A &= ~1u;  // even, so child arrays stay 8-byte aligned in both semispaces
   L.PC = c.pending_capacity;
+  L.beta = c.batch_size;
   const uint64_t RW = (uint64_t)L.R * L.W;
   uint64_t o = 0;
   L.off_global = o;
@@ -191,7 +199,15 @@ inline Layout make_layout(const kvr_config& c) {
   // L-LRU only: the last access (global query index) of every edge token,
   // at the same offsets as the tokens in both semispaces
   L.off_stamp = o;
-  if (c.evict == KVR_EVICT_LRU) o += RW * L.arena_stride;
+  L.has_stamp = c.evict == KVR_EVICT_LRU;
+  if (L.has_stamp) o += RW * L.arena_stride;
+  // continuous batching only: in-progress counts per node, running rings
+  L.pin_stride = L.beta > 1 ? align_up((uint64_t)L.NC * 4ull, 256) : 0;
+  L.off_pin = o;
+  o += RW * L.pin_stride;
+  L.run_stride = L.beta > 1 ? align_up((uint64_t)(L.beta - 1) * 4ull, 256) : 0;
+  L.off_run = o;
+  o += RW * L.run_stride;
   L.total = o;
   return L;
 }

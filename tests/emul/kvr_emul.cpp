@@ -5,6 +5,7 @@
 #include "emul_wave.h"
 #include "../../paper_2601_18999_amd/csrc/kvr_core.h"
 
+#include <cstring>
 #include <vector>
 
 using namespace kvr;
@@ -13,7 +14,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
                         const int64_t* arrival, const uint16_t* out_len, int32_t* route, int32_t* hits,
                         int32_t* all_hits, kvr_worker_stats* out, char* ws_out, uint32_t ucap_in) {
   Layout L = make_layout(*cfg);
-  std::vector<uint64_t> mem(ws_out ? 0 : (L.total + 7) / 8);
+  std::vector<uint64_t> mem(ws_out ? 0 : (L.total + 7) / 8);  // zeroed: the in-progress counts start at 0
   char* ws = ws_out ? ws_out : reinterpret_cast<char*>(mem.data());
   Consts C;
   C.seed = cfg->seed;
@@ -43,6 +44,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   ustage.cap = ucap;
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
+  if (L.pin_stride) std::memset(ws + L.off_pin, 0, (size_t)L.R * W * L.pin_stride);
   std::vector<uint32_t> rwbuf;
   // per-worker match paths (LDS on the device)
   std::vector<int32_t> pbuf((size_t)W * (3 * kPathMax + 1));
@@ -156,6 +158,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.ready_need = 0;
         err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, path_of(best), nullptr)
                                        : lru_insert(P, ia, qs, Lp, hins, path_of(best), nullptr);
+        if (!err && P.beta > 1) err = batch_admit(P, path_of(best), qs, Lp, nullptr);
       }
       if (err) return (int)err;
       if (has_next) {

@@ -6,9 +6,11 @@ path); nothing is compressed, nothing is maintained incrementally:
 * the hit count is the largest l with ``tuple(q[:l]) in S`` (Sec. 3.2,
   "Cache Matching");
 * U is recomputed at every draw by filtering S for leaves (paths with no
-  cached one-token extension) that are not in the marking set and are not
-  the insertion point, sorted with Python's tuple order, which is
-  lexicographic order of root paths (Algorithm 1);
+  cached one-token extension) that are not in the marking set, are not the
+  insertion point and are not a prefix of a path in the worker's running
+  batch (continuous batching: the last beta - 1 paths routed there), sorted
+  with Python's tuple order, which is lexicographic order of root paths
+  (Algorithm 1);
 * random words come from numpy's Philox bit generator (a library
   implementation of Philox4x64-10), not from the oracle's own code.
 
@@ -66,6 +68,7 @@ class SpecWorker:
         self.tl = 0
         self.Wb = 0
         self.pend: List[dict] = []
+        self.running: List[tuple] = []  # paths of the running batch
         self.evictions = 0
         self.loads = 0
         self.forced = 0
@@ -85,8 +88,9 @@ class SpecSim:
     def __init__(self, W: int, B: int, replica: int = 0, seed: int = 0, evict: str = "rlt",
                  update: str = "nlms", alpha_cached=0.0, alpha_miss=1.0, rho=31 / 32,
                  decay_interval_us=20000, lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
-                 true_cached_us=0, true_miss_us=1000, true_out_us=10000, cache_responses=0):
+                 true_cached_us=0, true_miss_us=1000, true_out_us=10000, cache_responses=0, batch_size=1):
         self.W, self.B, self.r, self.seed = W, B, replica, seed
+        self.beta = int(batch_size)
         self.responses = bool(cache_responses)
         self.evict, self.update = evict, update
         self.ac, self.am, self.rho, self.dt = alpha_cached, alpha_miss, rho, decay_interval_us
@@ -168,10 +172,17 @@ class SpecSim:
             self._insert_rlt(best, path, jg)
         else:
             self._insert_lru(best, path, jg)
+        if self.beta > 1:
+            w.running = (w.running + [path])[-(self.beta - 1):]
         return best, hb, h
+
+    @staticmethod
+    def _pinned(w: SpecWorker) -> set:
+        return {p[:k] for p in w.running for k in range(1, len(p) + 1)}
 
     def _insert_rlt(self, i: int, q, jg: int):
         w, B = self.w[i], self.B
+        pinned = self._pinned(w)
         d = 0
         for p in range(len(q)):
             v, u0 = q[: p + 1], q[:p]
@@ -184,13 +195,14 @@ class SpecSim:
             if v in w.S:
                 continue
             if len(w.S) == B:
-                U = sorted(x for x in _leaves(w.S) if w.mark.get(x, 0) != w.phase and x != u0)
+                U = sorted(x for x in _leaves(w.S) if w.mark.get(x, 0) != w.phase and x != u0 and x not in pinned)
                 if not U:
                     w.phase += 1
                     w.cnt = 1
                     w.mark[v] = w.phase
                     w.forced += 1
-                    U = sorted(x for x in _leaves(w.S) if w.mark.get(x, 0) != w.phase and x != u0)
+                    U = sorted(x for x in _leaves(w.S)
+                               if w.mark.get(x, 0) != w.phase and x != u0 and x not in pinned)
                     if not U:
                         raise RuntimeError("path longer than the cache")
                 r64 = philox_word0(self.seed, self.r, (jg, i, d, 0))
@@ -204,13 +216,14 @@ class SpecSim:
 
     def _insert_lru(self, i: int, q, jg: int):
         w, B, st = self.w[i], self.B, self.stamp[i]
+        pinned = self._pinned(w)
         for p in range(len(q)):
             v, u0 = q[: p + 1], q[:p]
             if v in w.S:
                 st[v] = (jg << 32) | p
                 continue
             if len(w.S) == B:
-                cands = [x for x in _leaves(w.S) if x != u0]
+                cands = [x for x in _leaves(w.S) if x != u0 and x not in pinned]
                 victim = min(cands, key=lambda x: st[x])
                 w.S.remove(victim)
                 del st[victim]
@@ -234,8 +247,9 @@ def run_spec(stream, W: int, B: int, replica: int = 0, **kw):
 # ---------------------------------------------------------------------------
 # exact expectation of RLT on one worker by enumeration of every draw
 
-def _rlt_branches(S: frozenset, T: frozenset, q, B: int):
-    """All outcomes of inserting q with probabilities: {(S', T'): Fraction}."""
+def _rlt_branches(S: frozenset, T: frozenset, q, B: int, pinned=frozenset()):
+    """All outcomes of inserting q with probabilities: {(S', T'): Fraction}.
+    ``pinned``: tokens of in-progress paths, never evicted."""
     out: Dict[Tuple[frozenset, frozenset], Fraction] = {}
 
     def rec(S, T, p, prob):
@@ -254,10 +268,10 @@ def _rlt_branches(S: frozenset, T: frozenset, q, B: int):
         if len(S) < B:
             rec(S | {v}, T, p + 1, prob)
             return
-        U = sorted(x for x in _leaves(S) if x not in T and x != u0)
+        U = sorted(x for x in _leaves(S) if x not in T and x != u0 and x not in pinned)
         if not U:
             T = frozenset({v})
-            U = sorted(x for x in _leaves(S) if x not in T and x != u0)
+            U = sorted(x for x in _leaves(S) if x not in T and x != u0 and x not in pinned)
         for x in U:
             rec((S - {x}) | {v}, T, p + 1, prob / len(U))
 
@@ -265,16 +279,21 @@ def _rlt_branches(S: frozenset, T: frozenset, q, B: int):
     return out
 
 
-def expected_hits(queries, B: int) -> List[Fraction]:
-    """E[h_j] for every query of a one-worker RLT run, exactly."""
+def expected_hits(queries, B: int, batch_size: int = 1) -> List[Fraction]:
+    """E[h_j] for every query of a one-worker RLT run, exactly; with
+    continuous batching the last batch_size - 1 paths are never evicted."""
     dist = {(frozenset(), frozenset()): Fraction(1)}
     res = []
+    running: List[tuple] = []
     for q in queries:
         q = tuple(int(x) for x in q)
         res.append(sum(p * lcp(S, q) for (S, T), p in dist.items()))
+        pinned = frozenset(p[:k] for p in running for k in range(1, len(p) + 1))
         nd: Dict[Tuple[frozenset, frozenset], Fraction] = {}
         for (S, T), p in dist.items():
-            for key, pp in _rlt_branches(S, T, q, B).items():
+            for key, pp in _rlt_branches(S, T, q, B, pinned).items():
                 nd[key] = nd.get(key, Fraction(0)) + p * pp
         dist = nd
+        if batch_size > 1:
+            running = (running + [q])[-(batch_size - 1):]
     return res

@@ -328,3 +328,44 @@ def test_cached_responses_invalid_path_rejected():
         assert all(w["routed"] == 0 for rr in sim.stats(check=False) for w in rr)
     finally:
         sim.close()
+
+
+# ---------------------------------------------------------------- continuous batching
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_batching_random_parity(evict):
+    """Continuous batching (Sec. 3.2, Theorem 2): the beta - 1 paths routed
+    to a worker before the current one are never evicted."""
+    rng = np.random.default_rng(71 + (evict == "lru"))
+    ev = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict]
+    for case in range(5):
+        beta = int(rng.integers(2, 9))
+        sp = small_spec(n=int(rng.integers(100, 400)), groups=int(rng.integers(1, 9)),
+                        prefix_len=(1, int(rng.integers(3, 40))), suffix_len=(1, int(rng.integers(2, 30))),
+                        vocab=int(rng.integers(2, 30)), seed=40 + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 6))
+        B = int(max(beta * s.max_len, rng.integers(2, 600)))
+        upd = ["nlms", "rls", "none"][case % 3]
+        note(f"batching/{evict} case {case}: beta={beta} W={W} B={B} n={s.n}")
+        res, stats = gpu_run(s, 3, W, B, update=upd, seed=case, evict=ev, batch_size=beta)
+        assert_parity(s, res, stats, W, B, range(3), update=upd, seed=case, evict=evict, batch_size=beta)
+
+
+def test_batching_multiturn_with_responses_and_collector():
+    sp = {"kind": "sessions", "n_sessions": 300, "turns": (1, 8), "start_len": 32, "ext_len": (8, 48),
+          "vocab": 32000, "responses": True, "out_len": 4, "turn_rate": 1.0, "seed": 4}
+    s = generate(sp)
+    beta = 4
+    W, B, R = 4, 4 * s.max_len, 3
+    note(f"batching multiturn: n={s.n} max_len={s.max_len} B={B}")
+    res, stats = gpu_run(s, R, W, B, batch=200, batch_size=beta, cache_responses=1,
+                         arena_words=B + 2 * s.max_len + 64)
+    assert_parity(s, res, stats, W, B, range(R), batch_size=beta, cache_responses=1)
+    assert sum(w["evictions"] for w in stats[0]) > B
+    assert sum(w["gc_runs"] for rr in stats for w in rr) > 0
+
+
+def test_batching_rejects_a_running_batch_larger_than_the_cache():
+    with pytest.raises(K.KvrError):
+        K.kvr_workspace_size(K.kvr_config_default(1, 2, 100, 30, batch_size=4))

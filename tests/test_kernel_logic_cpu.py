@@ -20,7 +20,7 @@ def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", router="
     assert e["rc"] == 0
     for r in range(R):
         o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict, router=router,
-                  **{k: v for k, v in cfg.items() if k.startswith("ca_") or k == "cache_responses"})
+                  **{k: v for k, v in cfg.items() if k.startswith("ca_") or k in ("cache_responses", "batch_size")})
         np.testing.assert_array_equal(e["route"][r], o["route"])
         np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
         for i in range(W):
@@ -186,3 +186,44 @@ def test_cached_responses_collector():
     B = 200
     e = _compare(s, 2, 2, B, cache_responses=1, arena_words=B + 2 * s.max_len + 64)
     assert sum(w["gc_runs"] for rr in e["workers"] for w in rr) > 10
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+@pytest.mark.parametrize("block", range(2))
+def test_continuous_batching_random_instances(evict, block):
+    """Continuous batching (Sec. 3.2, Theorem 2): the running batch's nodes
+    are excluded from eviction, ends of running paths split their edges, and
+    a released unmarked leaf makes U be rebuilt; against the oracle's
+    per-token pin counts."""
+    rng = np.random.default_rng(123 + block + 10 * (evict == "lru"))
+    evicted = 0
+    for case in range(40):
+        beta = int(rng.integers(2, 7))
+        sp = small_spec(n=int(rng.integers(30, 200)), groups=int(rng.integers(1, 8)),
+                        prefix_len=(1, int(rng.integers(2, 20))), suffix_len=(1, int(rng.integers(2, 12))),
+                        vocab=int(rng.integers(2, 10)), seed=500 * block + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 4))
+        B = int(max(beta * s.max_len, rng.integers(2, 150)))
+        e = _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case, evict=evict,
+                     batch_size=beta, ucap=[0, 8192][case % 2])
+        evicted += sum(w["evictions"] for w in e["workers"][0])
+    assert evicted > 1000
+
+
+def test_continuous_batching_with_responses_routers_and_collector():
+    rng = np.random.default_rng(99)
+    gc = 0
+    for case in range(20):
+        beta = int(rng.integers(2, 5))
+        B = int(rng.integers(40, 200))
+        s = random_response_stream(rng, int(rng.integers(50, 200)), int(rng.integers(2, 5)),
+                                   max(1, B // beta - 6), 6, B // beta)
+        W = int(rng.integers(1, 4))
+        router = ["lbgr", "random", "round_robin", "cache_aware"][case % 4]
+        # small vocabularies branch at almost every token: child arrays need
+        # about B more words than the edges
+        e = _compare(s, 2, W, B, seed=case, batch_size=beta, cache_responses=1, router=router,
+                     evict=["rlt", "lru"][case % 2], arena_words=2 * B + 2 * s.max_len + 64)
+        gc += sum(w["gc_runs"] for w in e["workers"][0])
+    assert gc > 20

@@ -518,3 +518,127 @@ def test_responses_match_and_contents_over_routed_history():
         assert r["workers"][i]["resident"] == len(prefixes) == r["workers"][i]["loads"]
     # a later turn's prompt contains the previous turn's response, and hits reach into it
     assert carried > 0
+
+
+# ---------------------------------------------------------------------------
+# continuous batching: the paths of a worker's running batch (the beta - 1
+# queries routed there before the current one) are never evicted
+# (Sec. 3.2, Theorem 2 and its assumption beta * L_max <= B)
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_batching_equals_bruteforce_model(evict):
+    rng = np.random.default_rng(300 + len(evict))
+    for case in range(80):
+        W = int(rng.integers(1, 4))
+        beta = int(rng.integers(2, 5))
+        B = int(rng.integers(2 * beta, 16))
+        vocab = int(rng.integers(2, 5))
+        n = int(rng.integers(5, 35))
+        s = _random_tiny_stream(rng, n, vocab, B // beta, B)
+        replica = int(rng.integers(0, 1000))
+        kw = dict(evict=evict, seed=int(rng.integers(0, 2**32)), batch_size=beta)
+        r = O.run(s, W, B, replica=replica, all_hits=True, check=1, **kw)
+        assert r["rc"] == 0
+        sim, routes, hits, allh = SM.run_spec(s, W, B, replica=replica, **kw)
+        np.testing.assert_array_equal(r["route"], routes)
+        np.testing.assert_array_equal(r["all_hits"], allh)
+        for i in range(W):
+            ws, sw = r["workers"][i], sim.w[i]
+            assert ws["evictions"] == sw.evictions and ws["loads"] == sw.loads
+            assert (ws["resident"], ws["digest_sum"], ws["digest_xor"]) == _digest_of_set(sw.S)
+            assert ws["load_est"] == sw.P and ws["theta"] == sw.theta
+            # the running batch is cached whole
+            for p in sw.running:
+                assert all(p[:k] in sw.S for k in range(1, len(p) + 1))
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_batching_candidate_list_equals_definition(evict):
+    """The maintained candidate list, rebuilt when a released path leaves an
+    unmarked leaf, gives the same run as U recomputed at every draw."""
+    rng = np.random.default_rng(17)
+    for case in range(12):
+        beta = int(rng.integers(2, 9))
+        sp = small_spec(n=int(rng.integers(100, 250)), groups=int(rng.integers(2, 8)),
+                        prefix_len=(4, 20), suffix_len=(1, 12), vocab=int(rng.integers(3, 40)), seed=case)
+        s = generate(sp)
+        W = int(rng.integers(1, 4))
+        B = int(max(beta * s.max_len, rng.integers(40, 300)))
+        a = O.run(s, W, B, replica=case, u_mode=0, all_hits=True, evict=evict, batch_size=beta, check=1)
+        b = O.run(s, W, B, replica=case, u_mode=1, all_hits=True, evict=evict, batch_size=beta)
+        assert a["rc"] == 0 and b["rc"] == 0
+        np.testing.assert_array_equal(a["route"], b["route"])
+        np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
+        assert a["workers"] == b["workers"]
+        assert sum(w["evictions"] for w in a["workers"]) > 0
+
+
+def test_batching_without_eviction_changes_nothing():
+    s = generate(small_spec(n=200, groups=5, prefix_len=(5, 25), suffix_len=(1, 15), vocab=6))
+    a = O.run(s, 3, 10**6, all_hits=True)
+    b = O.run(s, 3, 10**6, all_hits=True, batch_size=7, check=1)
+    np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
+    assert a["workers"] == b["workers"]
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_batching_protects_the_running_batch(evict):
+    """B = 4, beta = 2: (1,2) then (3,4) fill the cache; (5) starts a new
+    phase and needs one eviction.  The leaves are (1,2) and (3,4), but (3,4)
+    is in the running batch, so (1,2) goes for every random key (single-query
+    processing takes either with probability 1/2 under RLT)."""
+    s = _paths_stream([[1, 2], [3, 4], [5], [1, 2]], [0, 1, 2, 3])
+    for rep in range(40):
+        r = O.run(s, 1, 4, replica=rep, evict=evict, batch_size=2, check=1)
+        assert r["rc"] == 0
+        assert list(r["hits"]) == [0, 0, 0, 1]
+    one = [O.run(s, 1, 4, replica=rep, evict="rlt")["hits"][3] for rep in range(200)]
+    assert 0 < one.count(2) < 200 and one.count(1) + one.count(2) == 200
+
+
+BATCH_EXACT_CASES = [
+    (6, 2, [(0, 1, 2), (0, 1, 3), (0, 2, 0), (1, 2, 3), (0, 1, 2), (1, 2), (0, 1, 3), (0, 2, 1),
+            (1, 2, 3), (0, 1, 2), (2, 0, 1), (0, 1, 3)]),
+    (6, 3, [(0, 1), (0, 2), (1, 0), (0, 1), (1, 1), (0, 2), (2, 2), (0, 1), (1, 0), (0, 2), (2, 1)]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(BATCH_EXACT_CASES)))
+def test_batching_mean_hits_match_exact_enumeration(case):
+    """Mean hits over many random keys = the exact expectation, enumerated
+    over every draw with the running batch excluded from U; the expectation
+    differs from single-query processing, so the pins have an effect."""
+    B, beta, queries = BATCH_EXACT_CASES[case]
+    exact = SM.expected_hits(queries, B, batch_size=beta)
+    assert exact != SM.expected_hits(queries, B)
+    s = _paths_stream([list(q) for q in queries], list(range(len(queries))))
+    R = 20000
+    per = np.zeros((R, len(queries)))
+    for rep in range(R):
+        per[rep] = O.run(s, 1, B, replica=rep, batch_size=beta)["hits"]
+    tot = per.sum(axis=1)
+    sd = tot.std(ddof=1) / math.sqrt(R)
+    assert abs(tot.mean() - float(sum(exact))) < 4 * sd + 1e-12
+    for j, e in enumerate(exact):
+        sdj = per[:, j].std(ddof=1) / math.sqrt(R)
+        assert abs(per[:, j].mean() - float(e)) < 4.5 * sdj + 1e-12
+
+
+def test_lru_batch_lower_bound_construction():
+    """Theorem 2 lower bound: B-L+2 paths share an (L-1)-token prefix; batch
+    u is {G_1, ..., G_(beta-1), G_(u+beta-1)} for u = 1..B-L-beta+3, queried
+    in a loop.  L-LRU misses the tail of every rotating query once the
+    cache is full, while the first beta-1 paths always hit."""
+    for B, L, beta in [(12, 3, 3), (20, 4, 4), (30, 2, 2)]:
+        paths, n = _tail_paths(B, L)
+        m = B - L - beta + 3
+        order = []
+        for _ in range(5):
+            for u in range(m):
+                order += list(range(beta - 1)) + [u + beta - 1]
+        s = _paths_stream(paths, order)
+        r = O.run(s, 1, B, evict="lru", batch_size=beta, check=1)
+        assert r["rc"] == 0
+        h = r["hits"].reshape(5, m, beta)
+        assert (h[1:, :, : beta - 1] == L).all()
+        assert (h[1:, :, beta - 1] == L - 1).all()
