@@ -81,7 +81,7 @@ kvr_status validate(const kvr_config* c) {
   const uint64_t min_arena = (uint64_t)c->cache_tokens + 2ull * c->max_query_tokens + 64ull;
   if (c->arena_words != 0 && c->arena_words < min_arena)
     return fail(KVR_EINVAL, "arena_words must be 0 or >= cache_tokens + 2*max_query_tokens + 64");
-  const uint64_t dflt_arena = 4ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
+  const uint64_t dflt_arena = 8ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
   if (c->arena_words == 0 && dflt_arena >= (1ull << 32))
     return fail(KVR_EINVAL, "cache too large for 32-bit arena offsets");
   if (!finite(c->alpha_cached) || !finite(c->alpha_miss))

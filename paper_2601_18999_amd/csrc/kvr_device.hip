@@ -153,6 +153,25 @@ __device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, 
   return wave_argmin(eh, W, eh_sh);
 }
 
+// The next query's h on the workers other than `best`, taken one worker at a
+// time from an LDS counter, so a wave that drew long matches takes fewer
+// (the routing wave joins once its own work is done).  The index is
+// wave-uniform (lane 0's atomic, read back from lane 0) and the loop is
+// bounded by W.
+__device__ __forceinline__ void take_matches(const StepArgs& a, uint32_t r, uint32_t W, uint32_t best,
+                                             const int32_t* qn, int32_t Lnq, int32_t ell, const int32_t* h_cur,
+                                             int32_t* h_next, const PathArea& paths, uint32_t* next) {
+  for (uint32_t it = 0; it < W; ++it) {
+    uint32_t got = 0;
+    if (lane_id() == 0) got = atomicAdd(next, 1u);
+    const uint32_t i = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
+    if (i >= W) break;
+    if (i == best) continue;
+    Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
+    count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_cur[i], ell, paths.of(i)), &h_next[i]);
+  }
+}
+
 // One workgroup per replica walks the batch in order.  A worker's tree
 // changes only when a query is routed to it, so while wave 0 inserts query k
 // into the routed worker the other waves compute the draw words of that
@@ -341,6 +360,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         Ptrs Pb = worker_ptrs(a.ws, a.L, r, best);
         count_matched(Pb, match_incremental(Pb, Pb.hdr->arena_sel, qn, Lnq, Lp, ell_r, paths.of(best)),
                       &h_sh[cur ^ 1u][best]);
+        // then the other workers' matches that no helper has taken yet
+        if (nh > 0) take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], paths, &next_sh);
       }
       if (nh == 0 && has_next) {
         if ((uint32_t)lane < W)
@@ -364,19 +385,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
             complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
           if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
         }
-        // workers taken one at a time from an LDS counter, so a wave that
-        // drew long matches takes fewer; the index is wave-uniform (lane
-        // 0's atomic, read back from lane 0) and the loop is bounded by W
-        for (uint32_t it = 0; it < W; ++it) {
-          uint32_t got = 0;
-          if (lane == 0) got = atomicAdd(&next_sh, 1u);
-          const uint32_t i = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
-          if (i >= W) break;
-          if (i == best) continue;
-          Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-          count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_sh[cur][i], ell, paths.of(i)),
-                        &h_sh[cur ^ 1u][i]);
-        }
+        take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], paths, &next_sh);
       }
     }
     __syncthreads();
