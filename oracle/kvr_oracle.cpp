@@ -46,7 +46,13 @@
 //     counter (global query index, worker, draw index, 0);
 //   - if U is empty while the cache is full a new phase is forced
 //     (marking set reset to the current token) and U is recomputed;
-//   - the hit estimate used by the router is the exact per-worker match;
+//   - the hit estimate used by the router is the exact per-worker match, or
+//     with router_tree the match against a tree the router keeps per worker:
+//     the prompts routed there (the router never sees a response), inserted
+//     when routed, under L-LRU eviction of its own budget (App. E: a global
+//     tree that drifts from the workers' caches); the routing features and
+//     decision use that estimate, the observed latency and the hit counts use
+//     the worker's true match;
 //   - LBGR quantities are in seconds with the per-1k-token scaling of App. A
 //     (features 0.001*h, 0.001*(|q|-h), load, 1);
 //   - the residual model is updated by normalised LMS (step = the paper's
@@ -107,6 +113,12 @@ typedef struct orc_config {
   // inserted are in progress there and none of their tokens is evicted;
   // 1 = single-query processing (only the insertion point is protected)
   int32_t batch_size;
+  // approximate router tree (App. E): 1 = the router estimates h from a tree
+  // of its own per worker, holding the prompts routed there (inserted when
+  // routed) under its own L-LRU eviction with budget router_tree_tokens
+  // (0 = cache_tokens); 0 = the router sees the workers' true caches
+  int32_t router_tree;
+  uint32_t router_tree_tokens;
 } orc_config;
 
 typedef struct orc_worker_stats {
@@ -118,6 +130,9 @@ typedef struct orc_worker_stats {
   int64_t backlog_us, last_decay_us;
   double load_est;
   double theta[4];
+  // the router's tree of this worker (router_tree = 1): tokens held, digest
+  // as above, L-LRU evictions
+  uint64_t router_resident, router_digest_sum, router_digest_xor, router_evictions;
 } orc_worker_stats;
 
 }  // extern "C"
@@ -212,6 +227,7 @@ struct Sim {
   orc_config cfg;
   uint32_t replica;
   std::vector<Worker> w;
+  std::vector<Worker> rt;  // the router's tree of each worker (router_tree = 1)
   int64_t tprev = 0;
   int error = 0;
 };
@@ -393,9 +409,7 @@ void lru_set_stamp(Sim& s, Worker& w, int32_t id, uint64_t stamp) {
   n.stamp = stamp;
 }
 
-void insert_lru(Sim& s, uint32_t i, const int32_t* q, int32_t L, uint64_t jg) {
-  Worker& w = s.w[i];
-  const uint32_t B = s.cfg.cache_tokens;
+void insert_lru(Sim& s, Worker& w, uint32_t B, const int32_t* q, int32_t L, uint64_t jg) {
   const bool scan = s.cfg.u_mode == 1;
   int32_t u = 0;
   for (int32_t p = 0; p < L; ++p) {
@@ -539,10 +553,12 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int32_t Lpath, int64
     w.Wb = nb > 0 ? nb : 0;
   }
   s.tprev = t;
-  // 2. match on every worker (no state changes)
+  // 2. match on every worker (no state changes): the worker's cache, or the
+  // router's tree of it
+  const bool approx = c.router_tree != 0;
   std::vector<int32_t> h(W);
   for (uint32_t i = 0; i < W; ++i) {
-    h[i] = lcp(s.w[i], q, L);
+    h[i] = approx ? lcp(s.rt[i], q, L) : lcp(s.w[i], q, L);
     s.w[i].st.matched_tokens += (uint64_t)h[i];
     if (all_hits_row) all_hits_row[i] = h[i];
   }
@@ -597,11 +613,12 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int32_t Lpath, int64
     else
       best = small;  // low hits everywhere: the emptiest cache
   }
-  // 5. commit: load increment, observed latency, pending completion
+  // 5. commit: load increment, observed latency, pending completion; the
+  // observed latency and the hit count take the worker's true match
   Worker& w = s.w[best];
   double base_route = chat[best] + w.P;
   w.P = w.P + chat[best];
-  int64_t hb = h[best];
+  int64_t hb = approx ? lcp(w, q, L) : h[best];
   int64_t cost_us = c.true_cached_us * hb + c.true_miss_us * ((int64_t)L - hb) + c.true_out_us * (int64_t)o;
   int64_t e_us = w.Wb + cost_us;
   w.Wb = w.Wb + cost_us;
@@ -626,8 +643,11 @@ void step(Sim& s, uint64_t jg, const int32_t* q, int32_t L, int32_t Lpath, int64
   if (c.evict == 0)
     insert_rlt(s, best, q, Lpath, jg);
   else
-    insert_lru(s, best, q, Lpath, jg);
+    insert_lru(s, w, c.cache_tokens, q, Lpath, jg);
   if (!s.error) batch_admit(s, best, q, Lpath);
+  // the router adds the prompt to its tree of the routed worker
+  if (!s.error && approx)
+    insert_lru(s, s.rt[best], c.router_tree_tokens ? c.router_tree_tokens : c.cache_tokens, q, L, jg);
 }
 
 // Per-token path hash H(v) = mix64(H(parent) + GOLDEN * (tok + 1)), H(root) = 0.
@@ -681,6 +701,19 @@ bool check_invariants(const Sim& s) {
     }
     for (size_t x = 1; x < w.nodes.size(); ++x)
       if (w.nodes[x].alive && w.nodes[x].pin != pins[x]) return false;
+  }
+  // the router's trees: within their budget, prefix-closed
+  const uint64_t rb = s.cfg.router_tree_tokens ? s.cfg.router_tree_tokens : s.cfg.cache_tokens;
+  for (const Worker& w : s.rt) {
+    if (w.size > rb) return false;
+    uint64_t alive = 0;
+    for (size_t x = 1; x < w.nodes.size(); ++x) {
+      const Node& n = w.nodes[x];
+      if (!n.alive) continue;
+      alive += 1;
+      if (!w.nodes[n.parent].alive && n.parent != 0) return false;
+    }
+    if (alive != w.size) return false;
     if (w.P < 0.0) return false;
   }
   return true;
@@ -703,12 +736,18 @@ int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* 
   s.cfg = *cfg;
   s.replica = replica;
   s.w.resize(cfg->num_workers);
+  s.rt.resize(cfg->router_tree ? cfg->num_workers : 0);
   for (Worker& w : s.w) {
     w.nodes.emplace_back();
     w.nodes[0].alive = true;
     std::memset(&w.st, 0, sizeof(w.st));
     w.st.phase = 1;
     for (int a = 0; a < 16; ++a) w.Pm[a] = (a % 5 == 0) ? cfg->rls_p0 : 0.0;
+  }
+  for (Worker& w : s.rt) {
+    w.nodes.emplace_back();
+    w.nodes[0].alive = true;
+    std::memset(&w.st, 0, sizeof(w.st));
   }
   for (uint64_t j = 0; j < n; ++j) {
     const int32_t* q = tokens + offsets[j];
@@ -737,6 +776,16 @@ int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* 
     w.st.last_decay_us = w.tl;
     w.st.load_est = w.P;
     for (int a = 0; a < 4; ++a) w.st.theta[a] = w.theta[a];
+    if (cfg->router_tree) {
+      Worker& rw = s.rt[i];
+      orc_worker_stats rs;
+      std::memset(&rs, 0, sizeof(rs));
+      digest(rw, rs);
+      w.st.router_resident = rs.resident;
+      w.st.router_digest_sum = rs.digest_sum;
+      w.st.router_digest_xor = rs.digest_xor;
+      w.st.router_evictions = rw.st.evictions;
+    }
     if (wstats) wstats[i] = w.st;
   }
   return s.error;

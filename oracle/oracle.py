@@ -46,6 +46,8 @@ class OrcConfig(ctypes.Structure):
         ("ca_cache_threshold", ctypes.c_double),
         ("cache_responses", ctypes.c_int32),
         ("batch_size", ctypes.c_int32),
+        ("router_tree", ctypes.c_int32),
+        ("router_tree_tokens", ctypes.c_uint32),
     ]
 
 
@@ -55,10 +57,14 @@ _U64 = ["routed", "prompt_tokens", "hit_tokens", "matched_tokens", "loads", "evi
         "latency_sum_us", "latency_max_us"]
 
 
+_ROUTER_U64 = ["router_resident", "router_digest_sum", "router_digest_xor", "router_evictions"]
+
+
 class OrcWorkerStats(ctypes.Structure):
     _fields_ = ([(n, ctypes.c_uint64) for n in _U64]
                 + [("backlog_us", ctypes.c_int64), ("last_decay_us", ctypes.c_int64),
-                   ("load_est", ctypes.c_double), ("theta", ctypes.c_double * 4)])
+                   ("load_est", ctypes.c_double), ("theta", ctypes.c_double * 4)]
+                + [(n, ctypes.c_uint64) for n in _ROUTER_U64])
 
 
 def build(force: bool = False) -> str:
@@ -96,7 +102,7 @@ DEFAULTS: Dict[str, Any] = dict(
     lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
     true_cached_us=0, true_miss_us=1000, true_out_us=10000,
     router="lbgr", ca_balance_abs=32, ca_balance_rel=1.0001, ca_cache_threshold=0.5,
-    cache_responses=0, batch_size=1)
+    cache_responses=0, batch_size=1, router_tree=0, router_tree_tokens=0)
 
 ROUTER = {"lbgr": 0, "random": 1, "round_robin": 2, "cache_aware": 3}
 
@@ -122,6 +128,8 @@ def make_config(W: int, B: int, **kw) -> OrcConfig:
     c.ca_cache_threshold = float(p["ca_cache_threshold"])
     c.cache_responses = int(p["cache_responses"])
     c.batch_size = int(p["batch_size"])
+    c.router_tree = int(p["router_tree"])
+    c.router_tree_tokens = int(p["router_tree_tokens"])
     return c
 
 
@@ -152,6 +160,8 @@ def run(stream, W: int, B: int, replica: int = 0, n: Optional[int] = None,
         d["last_decay_us"] = int(s.last_decay_us)
         d["load_est"] = float(s.load_est)
         d["theta"] = [float(x) for x in s.theta]
+        for name in _ROUTER_U64:
+            d[name] = int(getattr(s, name))
         workers.append(d)
     return {"rc": rc, "route": route, "hits": hits, "all_hits": ah, "workers": workers}
 

@@ -88,9 +88,16 @@ class SpecSim:
     def __init__(self, W: int, B: int, replica: int = 0, seed: int = 0, evict: str = "rlt",
                  update: str = "nlms", alpha_cached=0.0, alpha_miss=1.0, rho=31 / 32,
                  decay_interval_us=20000, lr=0.992, nlms_eps=1e-9, rls_p0=100.0,
-                 true_cached_us=0, true_miss_us=1000, true_out_us=10000, cache_responses=0, batch_size=1):
+                 true_cached_us=0, true_miss_us=1000, true_out_us=10000, cache_responses=0, batch_size=1,
+                 router_tree=0, router_tree_tokens=0):
         self.W, self.B, self.r, self.seed = W, B, replica, seed
         self.beta = int(batch_size)
+        # the router's own tree per worker (App. E): routed prompts, L-LRU
+        self.approx = bool(router_tree)
+        self.RB = int(router_tree_tokens) or B
+        self.rt = [set() for _ in range(W)]
+        self.rstamp: List[Dict[tuple, int]] = [dict() for _ in range(W)]
+        self.rt_evictions = [0] * W
         self.responses = bool(cache_responses)
         self.evict, self.update = evict, update
         self.ac, self.am, self.rho, self.dt = alpha_cached, alpha_miss, rho, decay_interval_us
@@ -145,7 +152,7 @@ class SpecSim:
             w.tl = t
             w.Wb = max(0, w.Wb - (t - self.tprev))
         self.tprev = t
-        h = [lcp(w.S, q) for w in self.w]
+        h = [lcp(self.rt[i], q) if self.approx else lcp(w.S, q) for i, w in enumerate(self.w)]
         best, ehats, chats, phis = 0, [], [], []
         for i, w in enumerate(self.w):
             x = [h[i] * 0.001, (L - h[i]) * 0.001, w.P, 1.0]
@@ -162,7 +169,7 @@ class SpecSim:
         w = self.w[best]
         base = chats[best] + w.P
         w.P = w.P + chats[best]
-        hb = h[best]
+        hb = lcp(w.S, q)  # the worker's true match
         cost = self.tc * hb + self.tm * (L - hb) + self.to * o
         e_us = w.Wb + cost
         w.Wb = w.Wb + cost
@@ -171,9 +178,13 @@ class SpecSim:
         if self.evict == "rlt":
             self._insert_rlt(best, path, jg)
         else:
-            self._insert_lru(best, path, jg)
+            w.loads += sum(1 for p in range(len(path)) if path[: p + 1] not in w.S)
+            w.evictions += self._lru(w.S, self.stamp[best], B=self.B, q=path, jg=jg, pinned=self._pinned(w))
         if self.beta > 1:
             w.running = (w.running + [path])[-(self.beta - 1):]
+        if self.approx:
+            self.rt_evictions[best] += self._lru(self.rt[best], self.rstamp[best], B=self.RB, q=q, jg=jg,
+                                                 pinned=set())
         return best, hb, h
 
     @staticmethod
@@ -214,23 +225,26 @@ class SpecSim:
             w.S.add(v)
             w.loads += 1
 
-    def _insert_lru(self, i: int, q, jg: int):
-        w, B, st = self.w[i], self.B, self.stamp[i]
-        pinned = self._pinned(w)
+    @staticmethod
+    def _lru(S: set, st: Dict[tuple, int], B: int, q, jg: int, pinned: set) -> int:
+        """L-LRU insertion of q into the token set S with access stamps st;
+        returns the number of evictions.  (Counting loads is left to the
+        caller: it is the number of tokens of q not in S beforehand.)"""
+        ev = 0
         for p in range(len(q)):
             v, u0 = q[: p + 1], q[:p]
-            if v in w.S:
+            if v in S:
                 st[v] = (jg << 32) | p
                 continue
-            if len(w.S) == B:
-                cands = [x for x in _leaves(w.S) if x != u0 and x not in pinned]
+            if len(S) == B:
+                cands = [x for x in _leaves(S) if x != u0 and x not in pinned]
                 victim = min(cands, key=lambda x: st[x])
-                w.S.remove(victim)
+                S.remove(victim)
                 del st[victim]
-                w.evictions += 1
-            w.S.add(v)
+                ev += 1
+            S.add(v)
             st[v] = (jg << 32) | p
-            w.loads += 1
+        return ev
 
 
 def run_spec(stream, W: int, B: int, replica: int = 0, **kw):

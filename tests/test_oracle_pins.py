@@ -642,3 +642,109 @@ def test_lru_batch_lower_bound_construction():
         h = r["hits"].reshape(5, m, beta)
         assert (h[1:, :, : beta - 1] == L).all()
         assert (h[1:, :, beta - 1] == L - 1).all()
+
+
+# ---------------------------------------------------------------------------
+# approximate router tree (App. E): the router matches against a tree of its
+# own per worker (routed prompts, L-LRU under its own budget); the observed
+# latency and the hit counts take the worker's true match
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_router_tree_equals_bruteforce_model(evict):
+    rng = np.random.default_rng(600 + len(evict))
+    for case in range(80):
+        W = int(rng.integers(1, 4))
+        B = int(rng.integers(5, 14))
+        vocab = int(rng.integers(2, 5))
+        n = int(rng.integers(5, 35))
+        resp = case % 2
+        if resp:
+            s = _random_response_stream(rng, n, vocab, 5, 3, B)
+        else:
+            s = _random_tiny_stream(rng, n, vocab, 6, B)
+        RB = int(rng.integers(int(s.lengths.max()), 16))
+        replica = int(rng.integers(0, 1000))
+        kw = dict(evict=evict, seed=int(rng.integers(0, 2**32)), router_tree=1, router_tree_tokens=RB,
+                  cache_responses=resp)
+        r = O.run(s, W, B, replica=replica, all_hits=True, check=1, **kw)
+        assert r["rc"] == 0
+        sim, routes, hits, allh = SM.run_spec(s, W, B, replica=replica, **kw)
+        np.testing.assert_array_equal(r["route"], routes)
+        np.testing.assert_array_equal(r["hits"], hits)
+        np.testing.assert_array_equal(r["all_hits"], allh)
+        for i in range(W):
+            ws, sw = r["workers"][i], sim.w[i]
+            assert ws["evictions"] == sw.evictions and ws["loads"] == sw.loads
+            assert (ws["resident"], ws["digest_sum"], ws["digest_xor"]) == _digest_of_set(sw.S)
+            assert (ws["router_resident"], ws["router_digest_sum"], ws["router_digest_xor"]) == \
+                _digest_of_set(sim.rt[i])
+            assert ws["router_evictions"] == sim.rt_evictions[i]
+            assert ws["load_est"] == sw.P and ws["theta"] == sw.theta
+
+
+def test_router_tree_without_eviction_is_exact():
+    """Neither the caches nor the router's trees evict: the router's trees
+    hold exactly the routed prompts, as the caches do, so the estimate is
+    the true match and the run is that of the exact router."""
+    s = generate(small_spec(n=250, groups=5, prefix_len=(5, 25), suffix_len=(1, 15), vocab=6))
+    a = O.run(s, 3, 10**6, all_hits=True)
+    b = O.run(s, 3, 10**6, all_hits=True, router_tree=1, check=1)
+    np.testing.assert_array_equal(a["route"], b["route"])
+    np.testing.assert_array_equal(a["all_hits"], b["all_hits"])
+    for x, y in zip(a["workers"], b["workers"]):
+        assert {k: x[k] for k in x if not k.startswith("router_")} == {k: y[k] for k in y if not k.startswith("router_")}
+        assert y["router_resident"] == y["resident"] and y["router_digest_sum"] == y["digest_sum"]
+
+
+def _lcp_max(xs, q):
+    best = 0
+    for x in xs:
+        l = 0
+        while l < min(len(x), len(q)) and x[l] == q[l]:
+            l += 1
+        best = max(best, l)
+    return best
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_router_tree_overestimates_an_evicting_cache(evict):
+    """A router tree that never evicts: its estimate is the longest common
+    prefix with any prompt routed to the worker before (a closed form over
+    the routed history); the worker's cache evicts, so its true match, which
+    the hit counts report, is at most that."""
+    s = generate(small_spec(n=300, groups=6, prefix_len=(5, 30), suffix_len=(2, 15), vocab=7))
+    W, B = 3, 60
+    r = O.run(s, W, B, all_hits=True, evict=evict, router_tree=1, router_tree_tokens=10**6, check=1)
+    assert r["rc"] == 0 and sum(w["evictions"] for w in r["workers"]) > 0
+    assert sum(w["router_evictions"] for w in r["workers"]) == 0
+    qs = [tuple(int(x) for x in s.query(j)) for j in range(s.n)]
+    seen = [[] for _ in range(W)]
+    under = 0
+    for j in range(s.n):
+        for i in range(W):
+            assert r["all_hits"][j, i] == _lcp_max(seen[i], qs[j])
+        i = int(r["route"][j])
+        assert r["hits"][j] <= r["all_hits"][j, i]
+        under += int(r["hits"][j] < r["all_hits"][j, i])
+        seen[i].append(qs[j])
+    assert under > 0  # the estimate is off where the cache evicted
+
+
+def test_router_tree_underestimates_with_a_small_budget():
+    """A router tree with a small budget and caches that never evict: the
+    true match is the closed form over the routed history and the router's
+    estimate is at most that."""
+    s = generate(small_spec(n=300, groups=6, prefix_len=(5, 30), suffix_len=(2, 15), vocab=7))
+    W = 3
+    r = O.run(s, W, 10**6, all_hits=True, router_tree=1, router_tree_tokens=int(s.lengths.max()) + 5, check=1)
+    assert r["rc"] == 0 and sum(w["router_evictions"] for w in r["workers"]) > 0
+    qs = [tuple(int(x) for x in s.query(j)) for j in range(s.n)]
+    seen = [[] for _ in range(W)]
+    over = 0
+    for j in range(s.n):
+        i = int(r["route"][j])
+        assert r["hits"][j] == _lcp_max(seen[i], qs[j])
+        assert r["all_hits"][j, i] <= r["hits"][j]
+        over += int(r["all_hits"][j, i] < r["hits"][j])
+        seen[i].append(qs[j])
+    assert over > 0
