@@ -58,7 +58,7 @@ def log(msg: str) -> None:
 
 
 def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr", responses: int = 0,
-                 beta: int = 1):
+                 beta: int = 1, router_tree: int = 0, router_tree_tokens: int = 0):
     """The CPU oracle, single-threaded, on replica 0 of the same stream: the
     first n queries, n grown until one run takes at least budget_s (the cost
     per query grows as the caches fill, so the last steps grow by 1.4x)."""
@@ -66,7 +66,8 @@ def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str 
     n = min(1000, stream.n)
     while True:
         t0 = time.perf_counter()
-        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses, batch_size=beta)
+        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses, batch_size=beta,
+              router_tree=router_tree, router_tree_tokens=router_tree_tokens)
         dt = time.perf_counter() - t0
         log(f"cpu oracle: {n} queries in {dt:.1f} s")
         if dt >= budget_s or n >= stream.n:
@@ -143,6 +144,10 @@ def main() -> int:
     ap.add_argument("--beta", type=int, default=1,
                     help="continuous batching: the batch size beta (the last beta-1 paths routed to a "
                          "worker are never evicted); 1 = single-query processing")
+    ap.add_argument("--router-tree", action="store_true",
+                    help="approximate router: the router scores with matches on L-LRU trees of its own "
+                         "(one per worker, the routed prompts) instead of the workers' caches")
+    ap.add_argument("--router-tree-tokens", type=int, default=0, help="budget of each router tree (0 = B)")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -180,7 +185,8 @@ def main() -> int:
     router = {"lbgr": K.KVR_ROUTE_LBGR, "random": K.KVR_ROUTE_RANDOM, "round_robin": K.KVR_ROUTE_ROUND_ROBIN,
               "cache_aware": K.KVR_ROUTE_CACHE_AWARE}[args.router]
     sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router,
-                      cache_responses=int(args.responses), batch_size=args.beta)
+                      cache_responses=int(args.responses), batch_size=args.beta,
+                      router_tree=int(args.router_tree), router_tree_tokens=args.router_tree_tokens)
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -227,7 +233,8 @@ def main() -> int:
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
-    default_run = (args.evict, args.router, args.responses, args.beta) == ("rlt", "lbgr", False, 1)
+    default_run = (args.evict, args.router, args.responses, args.beta, args.router_tree) == \
+        ("rlt", "lbgr", False, 1, False)
     traffic = load_traffic(workload) if default_run else None
     line = {
         "metric": "routed queries/sec",
@@ -244,6 +251,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": workload + ("_responses" if args.responses else ""), "eviction": args.evict,
                    "router": args.router, "cached_responses": bool(args.responses), "batch_size": args.beta,
+                   "router_tree": bool(args.router_tree), "router_tree_tokens": args.router_tree_tokens or None,
                    "replicas": R,
                    "workers": W, "cache_tokens": B,
                    "batch_queries": args.batch, "timed_queries": q - q0,
@@ -271,7 +279,8 @@ def main() -> int:
         del src, dst
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router,
-                                            int(args.responses), args.beta)
+                                            int(args.responses), args.beta, int(args.router_tree),
+                                            args.router_tree_tokens)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 4u
+#define KVR_ABI_VERSION 5u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -136,6 +136,18 @@ typedef struct kvr_config {
    * B, so a full cache always has an evictable leaf).  Matching, routing and
    * the observed latency do not change. */
   int32_t batch_size;
+  /* 0 (default): the router's hit estimate is the exact match h_ij on worker
+   * i's cache.  1: the approximate router tree of App. E: the router keeps a
+   * token tree of its own per worker, holding the prompts routed there
+   * (inserted when routed; the router never sees a response) under L-LRU
+   * eviction with a budget of router_tree_tokens tokens (0 = cache_tokens,
+   * else max_query_tokens..2^30).  The scores, the routing decision, the
+   * load estimate's features and d_all_hits use the estimate from that tree;
+   * the observed latency, d_hits and the hit counters use the routed
+   * worker's true match.  At most 2^32 - 1 queries per context (its access
+   * stamps are 32-bit query indices). */
+  int32_t router_tree;
+  uint32_t router_tree_tokens;
 } kvr_config;
 
 /* Final per-(replica, worker) state and counters (kvr_stats). */
@@ -149,6 +161,9 @@ typedef struct kvr_worker_stats {
   double load_est;
   double theta[4];
   uint64_t nodes, gc_runs; /* layout-dependent, informative only */
+  /* the router's tree of this worker (router_tree = 1; else 0): tokens held,
+   * path-hash digest (as for the cache), L-LRU evictions */
+  uint64_t router_resident, router_digest_sum, router_digest_xor, router_evictions;
 } kvr_worker_stats;
 
 typedef struct kvr_ctx kvr_ctx;

@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVIC
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 4
+KVR_ABI_VERSION = 5
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
@@ -58,6 +58,8 @@ class KvrConfig(ctypes.Structure):
         ("ca_cache_threshold", ctypes.c_double),
         ("cache_responses", ctypes.c_int32),
         ("batch_size", ctypes.c_int32),
+        ("router_tree", ctypes.c_int32),
+        ("router_tree_tokens", ctypes.c_uint32),
     ]
 
 
@@ -67,11 +69,15 @@ STAT_U64 = ["routed", "prompt_tokens", "hit_tokens", "matched_tokens", "loads", 
             "latency_sum_us", "latency_max_us"]
 
 
+ROUTER_U64 = ["router_resident", "router_digest_sum", "router_digest_xor", "router_evictions"]
+
+
 class KvrWorkerStats(ctypes.Structure):
     _fields_ = ([(n, ctypes.c_uint64) for n in STAT_U64]
                 + [("backlog_us", ctypes.c_int64), ("last_decay_us", ctypes.c_int64),
                    ("load_est", ctypes.c_double), ("theta", ctypes.c_double * 4),
-                   ("nodes", ctypes.c_uint64), ("gc_runs", ctypes.c_uint64)])
+                   ("nodes", ctypes.c_uint64), ("gc_runs", ctypes.c_uint64)]
+                + [(n, ctypes.c_uint64) for n in ROUTER_U64])
 
 
 class KvrError(RuntimeError):
@@ -172,6 +178,8 @@ def _stats_dicts(arr, n: int) -> List[Dict]:
         d["theta"] = [float(x) for x in s.theta]
         d["nodes"] = int(s.nodes)
         d["gc_runs"] = int(s.gc_runs)
+        for name in ROUTER_U64:
+            d[name] = int(getattr(s, name))
         out.append(d)
     return out
 

@@ -19,7 +19,8 @@ hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st)
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st);
 hipError_t set_step_lds_limit(size_t bytes);
-size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap);
+hipError_t step_static_lds(size_t* bytes);
+size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, uint32_t path_sets);
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -72,6 +73,13 @@ kvr_status validate(const kvr_config* c) {
   if (c->batch_size < 1 || c->batch_size > 256) return fail(KVR_EINVAL, "batch_size must be in 1..256");
   if ((uint64_t)c->batch_size * c->max_query_tokens > c->cache_tokens)
     return fail(KVR_EINVAL, "batch_size * max_query_tokens must not exceed cache_tokens");
+  if (c->router_tree != 0 && c->router_tree != 1) return fail(KVR_EINVAL, "router_tree must be 0 or 1");
+  if (c->router_tree_tokens != 0 &&
+      (c->router_tree_tokens < c->max_query_tokens || c->router_tree_tokens > (1u << 30)))
+    return fail(KVR_EINVAL, "router_tree_tokens must be 0 or in max_query_tokens..2^30");
+  if (c->router_tree && 8ull * (c->router_tree_tokens ? c->router_tree_tokens : c->cache_tokens) +
+                                2ull * c->max_query_tokens + 4096ull >= (1ull << 32))
+    return fail(KVR_EINVAL, "router tree too large for 32-bit arena offsets");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
   if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
@@ -140,6 +148,8 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->ca_cache_threshold = 0.5;
   c->cache_responses = 0;
   c->batch_size = 1;
+  c->router_tree = 0;
+  c->router_tree_tokens = 0;
   c->update = KVR_UPD_NLMS;
   c->pending_capacity = 65536;
   c->node_capacity = 0;
@@ -183,8 +193,12 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   int lds_max = 0;
   e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return fail_hip(e, "hipDeviceGetAttribute(max LDS per block)");
-  const size_t static_lds = 2048;
-  const size_t qbytes = kvr::step_lds_bytes(L.maxL, L.W, 0, 0);
+  size_t static_lds = 0;
+  e = kvr::step_static_lds(&static_lds);
+  if (e != hipSuccess) return fail_hip(e, "hipFuncGetAttributes(step kernel)");
+  static_lds = (static_lds + 255u) & ~(size_t)255u;
+  const uint32_t path_sets = L.has_router ? 2u : 1u;
+  const size_t qbytes = kvr::step_lds_bytes(L.maxL, L.W, 0, 0, path_sets);
   if (qbytes + static_lds > (size_t)lds_max)
     return fail(KVR_EINVAL, "max_query_tokens does not fit in LDS (" + std::to_string(lds_max) + " bytes)");
   size_t room = (size_t)lds_max - static_lds - qbytes;
@@ -196,7 +210,7 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   size_t ucap = room / 16u;
   if (ucap > 8192) ucap = 8192;
   if (ucap < 64) ucap = 0;
-  const size_t lds = kvr::step_lds_bytes(L.maxL, L.W, (uint32_t)ucap, (uint32_t)rcap);
+  const size_t lds = kvr::step_lds_bytes(L.maxL, L.W, (uint32_t)ucap, (uint32_t)rcap, path_sets);
   if (lds > 65536) {
     e = kvr::set_step_lds_limit(lds);
     if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
@@ -247,7 +261,7 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens, co
   if (n == 0) return KVR_OK;
   if (!d_tokens || !d_offsets || !d_arrival_us) return fail(KVR_EINVAL, "tokens, offsets and arrival_us are required");
   if (n > (1u << 30)) return fail(KVR_EINVAL, "batch too large");
-  if (ctx->C.evict == KVR_EVICT_LRU && ctx->queries_done + n > 0xffffffffull)
+  if ((ctx->C.evict == KVR_EVICT_LRU || ctx->L.has_router) && ctx->queries_done + n > 0xffffffffull)
     return fail(KVR_EINVAL, "L-LRU access stamps hold 32-bit query indices: at most 2^32 - 1 queries per context");
   kvr::StepArgs a;
   a.ws = ctx->ws;

@@ -138,6 +138,30 @@ __device__ __forceinline__ Ptrs worker_ptrs(char* ws, const Layout& L, uint32_t 
   return P;
 }
 
+// The router's tree of worker i (approximate router): an L-LRU token tree
+// laid out like a cache, with its own header, budget and regions.  It has
+// no candidate list, completion ring or running batch; the digest walk
+// borrows the worker's scratch.
+__device__ __forceinline__ Ptrs router_ptrs(char* ws, const Layout& L, uint32_t r, uint32_t i) {
+  const uint64_t w = (uint64_t)r * L.W + i;
+  Ptrs P;
+  P.hdr = reinterpret_cast<WorkerHdr*>(ws + L.off_rt_hdr) + w;
+  P.nodes = reinterpret_cast<NodeRec*>(ws + L.off_rt_nodes + w * L.rt_node_stride);
+  P.arena0 = reinterpret_cast<int32_t*>(ws + L.off_rt_arena + w * L.rt_arena_stride);
+  P.leaf = reinterpret_cast<int32_t*>(ws + L.off_rt_leaf + w * L.rt_leaf_stride);
+  P.U = nullptr;
+  P.pend = nullptr;
+  P.scratch = reinterpret_cast<uint64_t*>(ws + L.off_scratch + w * L.scratch_stride);
+  P.stamp0 = reinterpret_cast<int32_t*>(ws + L.off_rt_stamp + w * L.rt_arena_stride);
+  P.pin = nullptr;
+  P.run = nullptr;
+  P.A = L.Ar;
+  P.NC = L.NCr;
+  P.PC = 0;
+  P.beta = 1;
+  return P;
+}
+
 // Is node x on a path of the worker's running batch (continuous batching)?
 // Such a node is never evicted, and is no candidate while it is a leaf.
 __device__ __forceinline__ bool pinned(const Ptrs& P, int32_t x) { return P.pin != nullptr && P.pin[x] > 0; }
@@ -2085,9 +2109,11 @@ __device__ double lbgr_score(const Consts& C, const WorkerHdr* w, int32_t h, int
 
 // Commit a query on its routed worker: add the estimated service time to the
 // load estimate (Algorithm 2), advance the observed-latency queue and queue
-// the completion record.  Returns KVR_DEV_* bits.
-__device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t L,
-                                 int64_t t, int32_t olen) {
+// the completion record.  hb = the worker's true hit (observed latency, hit
+// counter), hf = the hit the router scored with (the completion's features;
+// the same unless the router keeps its own tree).  Returns KVR_DEV_* bits.
+__device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t hf,
+                                                 int32_t L, int64_t t, int32_t olen) {
   WorkerHdr* w = P.hdr;
   const double base = chat + w->P;
   const double x3 = w->P;
@@ -2107,7 +2133,7 @@ __device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P,
     pr.chat = chat;
     pr.base = base;
     pr.x3 = x3;
-    pr.h = hb;
+    pr.h = hf;
     pr.L = L;
     P.pend[slot] = pr;
     w->pend_count += 1;
@@ -2205,6 +2231,7 @@ __device__ void worker_stats(const Ptrs& P, kvr_worker_stats* out) {
   for (int a = 0; a < 4; ++a) o.theta[a] = h->theta[a];
   o.nodes = h->nnodes;
   o.gc_runs = h->gc_runs;
+  o.router_resident = o.router_digest_sum = o.router_digest_xor = o.router_evictions = 0;
   *out = o;
 }
 

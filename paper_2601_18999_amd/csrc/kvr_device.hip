@@ -153,23 +153,85 @@ __device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, 
   return wave_argmin(eh, W, eh_sh);
 }
 
-// The next query's h on the workers other than `best`, taken one worker at a
+// Record a match length without counting it (the cache's own match when
+// the router scores with its own tree).
+__device__ __forceinline__ void store_h(int32_t h, int32_t* hslot) {
+  if (lane_id() == 0) *hslot = h;
+}
+
+// The next query's h on the workers other than `best`, taken one item at a
 // time from an LDS counter, so a wave that drew long matches takes fewer
-// (the routing wave joins once its own work is done).  The index is
-// wave-uniform (lane 0's atomic, read back from lane 0) and the loop is
-// bounded by W.
+// (the routing wave joins once its own work is done).  Items 0..W-1 are the
+// caches; with the approximate router, items W..2W-1 are the router's trees.
+// The index is wave-uniform (lane 0's atomic, read back from lane 0) and the
+// loop is bounded by the number of items.
 __device__ __forceinline__ void take_matches(const StepArgs& a, uint32_t r, uint32_t W, uint32_t best,
                                              const int32_t* qn, int32_t Lnq, int32_t ell, const int32_t* h_cur,
-                                             int32_t* h_next, const PathArea& paths, uint32_t* next) {
-  for (uint32_t it = 0; it < W; ++it) {
+                                             int32_t* h_next, const int32_t* g_cur, int32_t* g_next,
+                                             const PathArea& paths, const PathArea& rpaths, bool rtree,
+                                             uint32_t* next) {
+  const uint32_t items = rtree ? 2u * W : W;
+  for (uint32_t it = 0; it < items; ++it) {
     uint32_t got = 0;
     if (lane_id() == 0) got = atomicAdd(next, 1u);
     const uint32_t i = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
-    if (i >= W) break;
-    if (i == best) continue;
-    Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-    count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_cur[i], ell, paths.of(i)), &h_next[i]);
+    if (i >= items) break;
+    const uint32_t w = i < W ? i : i - W;
+    if (w == best) continue;
+    Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
+    if (i < W) {
+      const int32_t h = match_incremental(Pw, Pw.hdr->arena_sel, qn, Lnq, h_cur[w], ell, paths.of(w));
+      if (rtree)
+        store_h(h, &h_next[w]);
+      else
+        count_matched(Pw, h, &h_next[w]);
+    } else {
+      Ptrs Pr = router_ptrs(a.ws, a.L, r, w);
+      count_matched(Pw, match_incremental(Pr, Pr.hdr->arena_sel, qn, Lnq, g_cur[w], ell, rpaths.of(w)), &g_next[w]);
+    }
   }
+}
+
+// First device-side error of the run (check id and values for the message),
+// then the sticky status bits; the workgroup stops after the next barrier.
+__device__ __forceinline__ void report_error(GlobalHdr* g, uint32_t r, uint64_t jg, uint32_t err, const int64_t* dbg,
+                                             uint32_t* abort_flag) {
+  if (lane_id() != 0 || !err) return;
+  if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
+    g->err_check = (uint32_t)dbg[0];
+    g->err_replica = r;
+    g->err_query = jg;
+    g->err_val[0] = dbg[1];
+    g->err_val[1] = dbg[2];
+    g->err_val[2] = dbg[3];
+  }
+  atomicOr(&g->status, err);
+  *abort_flag = 1;
+}
+
+// Approximate router: the router adds prompt q[0, Lq) to its tree of the
+// routed worker (L-LRU; hr = the router's match of it), then matches the
+// next prompt there, from the path just inserted.  Returns KVR_DEV_* bits.
+__device__ __forceinline__ uint32_t router_admit(const StepArgs& a, uint32_t r, uint64_t jg, uint32_t best,
+                                                 const int32_t* qs, int32_t Lq, int32_t hr, bool has_next,
+                                                 const int32_t* qn, int32_t Lnq, int32_t ell, const PathArea& rpaths,
+                                                 int32_t* g_next, int64_t* dbg) {
+  Ptrs Pr = router_ptrs(a.ws, a.L, r, best);
+  InsertArgs ia;
+  ia.seed = a.C.seed;
+  ia.jg = jg;
+  ia.worker = best;
+  ia.replica = r;
+  ia.B = a.L.RB;
+  ia.rn = 0;
+  ia.rw = nullptr;
+  ia.ready = nullptr;
+  ia.ready_need = 0;
+  const uint32_t err = lru_insert(Pr, ia, qs, Lq, hr, rpaths.of(best), dbg);
+  if (!err && has_next)
+    count_matched(worker_ptrs(a.ws, a.L, r, best),
+                  match_incremental(Pr, Pr.hdr->arena_sel, qn, Lnq, Lq, ell, rpaths.of(best)), g_next);
+  return err;
 }
 
 // One workgroup per replica walks the batch in order.  A worker's tree
@@ -179,27 +241,35 @@ __device__ __forceinline__ void take_matches(const StepArgs& a, uint32_t r, uint
 // query's h on every other worker.  Matches are incremental: each worker
 // keeps the path of its last match, and the next query follows it up to
 // the longest common prefix of the two queries.  The routed worker's h for
-// the next query is completed from the path of the inserted query.
+// the next query is completed from the path of the inserted query.  With
+// the approximate router every worker has two trees, the cache and the
+// router's, each matched incrementally; the router's tree of the routed
+// worker is updated by a helper wave.
 __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   // dynamic LDS: two query buffers (max_query_tokens entries each), the high
-  // halves of the draw words, the match paths, then the staged candidate list
+  // halves of the draw words, the match paths (the caches', then the router
+  // trees'), then the staged candidate list
   extern __shared__ int32_t smem[];
   const uint32_t W = a.L.W;
+  const bool rtree = a.L.has_router != 0;
   const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
   uint32_t* rw = reinterpret_cast<uint32_t*>(smem + 2 * qstride);
-  PathArea paths;
+  PathArea paths, rpaths;
   paths.base = reinterpret_cast<int32_t*>(rw + a.rcap);
   paths.W = W;
+  rpaths.base = paths.base + (size_t)W * (3 * kPathMax + 1);
+  rpaths.W = W;
   UStage ustage;
   {
-    int32_t* ub = paths.base + (size_t)W * (3 * kPathMax + 1);
+    int32_t* ub = paths.base + (size_t)(rtree ? 2 : 1) * W * (3 * kPathMax + 1);
     ustage.node = ub;
     ustage.len = ub + a.ucap;
     ustage.top = ub + 2 * a.ucap;
     ustage.par = ub + 3 * a.ucap;
     ustage.cap = a.ucap;
   }
-  __shared__ int32_t h_sh[2][kMaxWorkers];  // h of the current and of the next query
+  __shared__ int32_t h_sh[2][kMaxWorkers];  // h of the current and of the next query (the caches)
+  __shared__ int32_t g_sh[2][kMaxWorkers];  // the same on the router's trees (approximate router)
   __shared__ double eh_sh[kMaxWorkers];
   __shared__ double ch_sh[kMaxWorkers];
   __shared__ int32_t ell_sh[2];  // LCP(q_k, q_k+1) in slot k & 1
@@ -208,7 +278,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ uint32_t abort_sh;
   __shared__ uint32_t nev_sh;
   __shared__ uint32_t wready_sh;  // helper waves done with the draw words
-  __shared__ uint32_t next_sh;    // next worker for the helpers' matches
+  __shared__ uint32_t next_sh;    // next item for the helpers' matches
+  // the hits the router scores with: the caches' own, or its trees'
+  int32_t(*est)[kMaxWorkers] = rtree ? g_sh : h_sh;
 
   const uint32_t r = blockIdx.x;
   const bool resp = a.C.cache_responses != 0;
@@ -238,7 +310,14 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     __syncthreads();
     for (uint32_t i = wave; i < W; i += nwaves) {
       Ptrs P = worker_ptrs(a.ws, a.L, r, i);
-      count_matched(P, match_lcp(P, P.hdr->arena_sel, smem, L0q, paths.of(i)), &h_sh[0][i]);
+      const int32_t h = match_lcp(P, P.hdr->arena_sel, smem, L0q, paths.of(i));
+      if (rtree) {
+        store_h(h, &h_sh[0][i]);
+        Ptrs Pr = router_ptrs(a.ws, a.L, r, i);
+        count_matched(P, match_lcp(Pr, Pr.hdr->arena_sel, smem, L0q, rpaths.of(i)), &g_sh[0][i]);
+      } else {
+        count_matched(P, h, &h_sh[0][i]);
+      }
     }
   }
   for (uint32_t k = 0; k < a.n; ++k) {
@@ -266,14 +345,14 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       double eh = __builtin_huge_val();
       if ((uint32_t)lane < W) {
         double ch;
-        eh = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, h_sh[cur][lane], Lq, &ch);
+        eh = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, est[cur][lane], Lq, &ch);
         ch_sh[lane] = ch;
         eh_sh[lane] = eh;
       }
       __builtin_amdgcn_wave_barrier();
-      const uint32_t best = route_choice(a, r, k, W, eh, h_sh[cur], Lq, eh_sh);
+      const uint32_t best = route_choice(a, r, k, W, eh, est[cur], Lq, eh_sh);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
-      const int32_t hb = h_sh[cur][best];
+      const int32_t hb = h_sh[cur][best];  // the worker's true hit
       // a cached prompt may continue into a cached response: the insertion
       // needs the cached length of the whole path, continued from the
       // prompt's recorded match
@@ -284,7 +363,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         hins_sh = hins;
         wready_sh = 0;
         next_sh = 0;
-        const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, Lq, t, olen);
+        const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, est[cur][best], Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
         if (a.hits) a.hits[orow] = hb;
@@ -299,7 +378,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         }
       }
       if (a.all_hits && (uint32_t)lane < W)
-        a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[cur][lane];
+        a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = est[cur][lane];
       if (nh == 0 && has_next) stage_next(a.tokens, n0, Ln, qn, qs, Lp, (uint32_t)lane, KVR_WAVE, &ell_sh[cur]);
     } else if (has_next) {
       stage_next(a.tokens, n0, Ln, qn, qs, Lp, threadIdx.x - KVR_WAVE, blockDim.x - KVR_WAVE, &ell_sh[cur]);
@@ -312,24 +391,26 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     const uint32_t rn = a.C.evict == KVR_EVICT_RLT ? (nev < a.rcap ? nev : a.rcap) : 0u;
     const int32_t hins = hins_sh;
     // LCP of the two paths, then of what the next match needs: the next
-    // prompt against the inserted path (routed worker) or against this
-    // prompt (every other worker, whose recorded match is of this prompt)
+    // prompt against the inserted path (the routed cache) or against this
+    // prompt (every other cache, whose recorded match is of this prompt, and
+    // every router tree, which holds prompts only)
     const int32_t ellp = ell_sh[cur];
     const int32_t ell_r = ellp < Lnq ? ellp : Lnq;
     const int32_t ell = ell_r < Lq ? ell_r : Lq;
+    const uint64_t jg = a.j0 + k;
 
     // ---- phase B.  Wave 0: the insertion, then the routed worker's h for
     // the next query.  Helpers: the insertion's draw words first, then
-    // completions and decay at the next arrival and the next query's h on
-    // the other workers.
+    // completions and decay at the next arrival (and the router's tree of
+    // the routed worker), and the next query's h on the other workers.
     if (wave == 0) {
       if (nh == 0)
         for (uint32_t d = (uint32_t)lane; d < rn; d += KVR_WAVE)
-          rw[d] = (uint32_t)(philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r) >> 32);
+          rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       InsertArgs ia;
       ia.seed = a.C.seed;
-      ia.jg = a.j0 + k;
+      ia.jg = jg;
       ia.worker = best;
       ia.replica = r;
       ia.B = a.L.B;
@@ -342,51 +423,58 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
                                                 : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
       // continuous batching: the path joins the worker's running batch
       if (!err && P.beta > 1) err = batch_admit(P, paths.of(best), qs, Lp, dbg);
-      if (lane == 0 && err) {
-        if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
-          g->err_check = (uint32_t)dbg[0];
-          g->err_replica = r;
-          g->err_query = a.j0 + k;
-          g->err_val[0] = dbg[1];
-          g->err_val[1] = dbg[2];
-          g->err_val[2] = dbg[3];
-        }
-        atomicOr(&g->status, err);
-        abort_sh = 1;
-      }
+      report_error(g, r, jg, err, dbg, &abort_sh);
       // the routed worker's h for the next query, from the path of the
       // query just inserted (all of it is cached now: the old h is Lp)
       if (has_next && !err) {
         Ptrs Pb = worker_ptrs(a.ws, a.L, r, best);
-        count_matched(Pb, match_incremental(Pb, Pb.hdr->arena_sel, qn, Lnq, Lp, ell_r, paths.of(best)),
-                      &h_sh[cur ^ 1u][best]);
+        const int32_t h = match_incremental(Pb, Pb.hdr->arena_sel, qn, Lnq, Lp, ell_r, paths.of(best));
+        if (rtree)
+          store_h(h, &h_sh[cur ^ 1u][best]);
+        else
+          count_matched(Pb, h, &h_sh[cur ^ 1u][best]);
         // then the other workers' matches that no helper has taken yet
-        if (nh > 0) take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], paths, &next_sh);
+        if (nh > 0)
+          take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], g_sh[cur], g_sh[cur ^ 1u], paths,
+                       rpaths, rtree, &next_sh);
       }
-      if (nh == 0 && has_next) {
-        if ((uint32_t)lane < W)
-          complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
-        if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
-        for (uint32_t i = 0; i < W; ++i)
-          if (i != best) {
-            Ptrs Pi = worker_ptrs(a.ws, a.L, r, i);
-            count_matched(Pi, match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h_sh[cur][i], ell, paths.of(i)),
-                          &h_sh[cur ^ 1u][i]);
-          }
-      }
-    } else {
-      for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
-        rw[d] = (uint32_t)(philox_word0(a.j0 + k, best, d, 0ull, a.C.seed, r) >> 32);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-      if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-      if (has_next) {
-        if (wave == 1) {
+      if (nh == 0 && !err) {
+        if (has_next) {
           if ((uint32_t)lane < W)
             complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
           if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
         }
-        take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], paths, &next_sh);
+        if (rtree) {
+          int64_t rdbg[4] = {0, 0, 0, 0};
+          const uint32_t rerr = router_admit(a, r, jg, best, qs, Lq, g_sh[cur][best], has_next, qn, Lnq, ell, rpaths,
+                                             &g_sh[cur ^ 1u][best], rdbg);
+          report_error(g, r, jg, rerr, rdbg, &abort_sh);
+        }
+        if (has_next)
+          take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], g_sh[cur], g_sh[cur ^ 1u], paths,
+                       rpaths, rtree, &next_sh);
       }
+    } else {
+      for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
+        rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (wave == 1) {
+        if (has_next) {
+          if ((uint32_t)lane < W)
+            complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
+          if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
+        }
+        if (rtree) {
+          int64_t rdbg[4] = {0, 0, 0, 0};
+          const uint32_t rerr = router_admit(a, r, jg, best, qs, Lq, g_sh[cur][best], has_next, qn, Lnq, ell, rpaths,
+                                             &g_sh[cur ^ 1u][best], rdbg);
+          report_error(g, r, jg, rerr, rdbg, &abort_sh);
+        }
+      }
+      if (has_next)
+        take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], g_sh[cur], g_sh[cur ^ 1u], paths,
+                     rpaths, rtree, &next_sh);
     }
     __syncthreads();
     if (abort_sh) break;
@@ -417,7 +505,10 @@ __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
     g->err_val[0] = g->err_val[1] = g->err_val[2] = 0;
   }
   if (tid < L.R) reinterpret_cast<ReplicaHdr*>(ws + L.off_rhdr)[tid].tprev = 0;
-  if (tid < RW) init_worker(worker_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
+  if (tid < RW) {
+    init_worker(worker_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
+    if (L.has_router) init_worker(router_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
+  }
 }
 
 // Batch checks before any state changes: lengths (with cached responses, a
@@ -454,15 +545,28 @@ __global__ void validate_tokens_kernel(char* ws, Layout L, const int32_t* tokens
 __global__ void stats_kernel(char* ws, Layout L) {
   const uint64_t widx = blockIdx.x;
   if (threadIdx.x != 0) return;
-  Ptrs P = worker_ptrs(ws, L, (uint32_t)(widx / L.W), (uint32_t)(widx % L.W));
-  worker_stats(P, reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats) + widx);
+  const uint32_t r = (uint32_t)(widx / L.W), i = (uint32_t)(widx % L.W);
+  kvr_worker_stats o;
+  worker_stats(worker_ptrs(ws, L, r, i), &o);
+  o.router_resident = o.router_digest_sum = o.router_digest_xor = o.router_evictions = 0;
+  if (L.has_router) {
+    // the router's tree of the worker: contents digest and evictions
+    Ptrs Pr = router_ptrs(ws, L, r, i);
+    kvr_worker_stats t;
+    worker_stats(Pr, &t);
+    o.router_resident = t.resident;
+    o.router_digest_sum = t.digest_sum;
+    o.router_digest_xor = t.digest_xor;
+    o.router_evictions = Pr.hdr->evictions;
+  }
+  reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats)[widx] = o;
 }
 
 // ---------------------------------------------------------------- launchers (host)
 
-size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap) {
+size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, uint32_t path_sets) {
   return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + (size_t)rcap * sizeof(uint32_t) +
-         (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
+         (size_t)path_sets * W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
 }
 
 
@@ -485,7 +589,7 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(validate_tokens_kernel, dim3(1024), dim3(256), 0, st, a.ws, a.L, a.tokens,
                      a.offsets, a.n);
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
-  const size_t lds = step_lds_bytes(a.L.maxL, a.L.W, a.ucap, a.rcap);
+  const size_t lds = step_lds_bytes(a.L.maxL, a.L.W, a.ucap, a.rcap, a.L.has_router ? 2u : 1u);
   hipLaunchKernelGGL(step_kernel, dim3(a.L.R), dim3(64 * waves), lds, st, a);
   return hipGetLastError();
 }
@@ -493,6 +597,15 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
 hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st) {
   hipLaunchKernelGGL(stats_kernel, dim3(L.R * L.W), dim3(64), 0, st, ws, L);
   return hipGetLastError();
+}
+
+// Static LDS of the step kernel (its __shared__ variables), from the
+// compiled kernel's attributes.
+hipError_t step_static_lds(size_t* bytes) {
+  hipFuncAttributes fa;
+  const hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(step_kernel));
+  if (e == hipSuccess) *bytes = fa.sharedSizeBytes;
+  return e;
 }
 
 hipError_t set_step_lds_limit(size_t bytes) {

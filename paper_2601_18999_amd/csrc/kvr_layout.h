@@ -23,6 +23,9 @@
 //                   paths of the worker's running batch through it
 //   running rings   (continuous batching only) the end node of each path
 //                   of the running batch, oldest first
+//   router trees    (approximate router only) per worker a second token
+//                   tree, the router's: header, node table, arenas, leaf
+//                   list and access stamps, sized for its own budget
 #ifndef KVR_LAYOUT_H
 #define KVR_LAYOUT_H
 
@@ -117,7 +120,13 @@ struct Layout {
   uint64_t off_global, off_rhdr, off_whdr, off_nodes, off_arena, off_leaf, off_U, off_pend,
       off_scratch, off_stats, off_stamp, off_pin, off_run, total;
   uint64_t node_stride, arena_stride, leaf_stride, pend_stride, scratch_stride, pin_stride, run_stride;
-  uint32_t has_stamp, pad0;
+  uint32_t has_stamp;
+  // the router's trees (approximate router): budget, node capacity, words per
+  // semispace; offsets and strides of their regions
+  uint32_t has_router;
+  uint32_t RB, NCr, Ar, pad1;
+  uint64_t off_rt_hdr, off_rt_nodes, off_rt_arena, off_rt_leaf, off_rt_stamp;
+  uint64_t rt_node_stride, rt_arena_stride, rt_leaf_stride;
 };
 
 // Constants of one run, passed by value to the kernels.
@@ -193,7 +202,10 @@ inline Layout make_layout(const kvr_config& c) {
   L.pend_stride = align_up((uint64_t)L.PC * sizeof(PendRec), 256);
   L.off_pend = o;
   o += RW * L.pend_stride;
-  L.scratch_stride = align_up((uint64_t)L.NC * 16ull, 256);
+  // the digest walk's stack serves the cache and the router's tree in turn
+  const uint64_t ncr = c.router_tree ? (uint64_t)(c.router_tree_tokens ? c.router_tree_tokens : c.cache_tokens) + 3ull
+                                     : 0ull;
+  L.scratch_stride = align_up((ncr > L.NC ? ncr : (uint64_t)L.NC) * 16ull, 256);
   L.off_scratch = o;
   o += RW * L.scratch_stride;
   L.off_stats = o;
@@ -210,6 +222,27 @@ inline Layout make_layout(const kvr_config& c) {
   L.run_stride = L.beta > 1 ? align_up((uint64_t)(L.beta - 1) * 4ull, 256) : 0;
   L.off_run = o;
   o += RW * L.run_stride;
+  // the router's trees: L-LRU token trees like the caches, with their own
+  // budget (prompts only, so no query exceeds it)
+  L.has_router = c.router_tree != 0;
+  L.RB = c.router_tree_tokens ? c.router_tree_tokens : c.cache_tokens;
+  L.NCr = L.RB + 3u;
+  L.Ar = (uint32_t)((8ull * L.RB + 2ull * c.max_query_tokens + 4096ull) & ~1ull);
+  L.pad1 = 0;
+  const uint64_t RWr = L.has_router ? RW : 0;
+  L.off_rt_hdr = o;
+  o = align_up(o + RWr * sizeof(WorkerHdr), 256);
+  L.rt_node_stride = align_up((uint64_t)L.NCr * sizeof(NodeRec), 256);
+  L.off_rt_nodes = o;
+  o += RWr * L.rt_node_stride;
+  L.rt_arena_stride = align_up(2ull * L.Ar * 4ull, 256);
+  L.off_rt_arena = o;
+  o += RWr * L.rt_arena_stride;
+  L.rt_leaf_stride = align_up((uint64_t)L.NCr * 4ull, 256);
+  L.off_rt_leaf = o;
+  o += RWr * L.rt_leaf_stride;
+  L.off_rt_stamp = o;
+  o += RWr * L.rt_arena_stride;
   L.total = o;
   return L;
 }

@@ -32,6 +32,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   C.evict = cfg->evict;
   C.cache_responses = cfg->cache_responses;
   const bool resp = cfg->cache_responses != 0;
+  const bool rtree = L.has_router != 0;
   const uint32_t W = L.W;
   // candidate list staging buffer (LDS on the device)
   const uint32_t ucap = ucap_in;
@@ -43,7 +44,10 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   ustage.par = ubuf.data() + 3 * ucap;
   ustage.cap = ucap;
   for (uint32_t r = 0; r < L.R; ++r)
-    for (uint32_t i = 0; i < W; ++i) init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
+    for (uint32_t i = 0; i < W; ++i) {
+      init_worker(worker_ptrs(ws, L, r, i), cfg->rls_p0);
+      if (rtree) init_worker(router_ptrs(ws, L, r, i), cfg->rls_p0);
+    }
   if (L.pin_stride) std::memset(ws + L.off_pin, 0, (size_t)L.R * W * L.pin_stride);
   std::vector<uint32_t> rwbuf;
   // per-worker match paths (LDS on the device)
@@ -56,24 +60,41 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
     p.cnt = pbuf.data() + (size_t)3 * W * kPathMax + i;
     return p;
   };
+  // the router trees' recorded matches (approximate router)
+  std::vector<int32_t> rbuf((size_t)W * (3 * kPathMax + 1));
+  auto rpath_of = [&](uint32_t i) {
+    PathRef p;
+    p.node = rbuf.data() + (size_t)i * kPathMax;
+    p.start = rbuf.data() + (size_t)(W + i) * kPathMax;
+    p.end = rbuf.data() + (size_t)(2 * W + i) * kPathMax;
+    p.cnt = rbuf.data() + (size_t)3 * W * kPathMax + i;
+    return p;
+  };
   for (uint32_t r = 0; r < L.R; ++r) {
     // the schedule of step_kernel for one replica, one batch: completions of
-    // query 0 and full matches first; then per query the stale worker's
-    // incremental match, scores, route, commit, insert, completions of the
-    // next query and incremental matches of it on the other workers
-    int32_t h[2][kMaxWorkers];
+    // query 0 and full matches first; then per query the scores, route,
+    // commit and insertion, the routed worker's match of the next query, the
+    // completions at the next arrival, the router's tree of the routed
+    // worker, and the next query's matches on the other workers.  h = the
+    // caches' matches, g = the router trees' (approximate router); the
+    // router scores with est = g or h.
+    int32_t h[2][kMaxWorkers], g[2][kMaxWorkers];
+    int32_t(*est)[kMaxWorkers] = rtree ? g : h;
     int64_t tprev = 0;
     if (n > 0) {
       for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), arrival[0], tprev);
+      const int32_t L0 = (int32_t)(offsets[1] - offsets[0]);
+      const int32_t L0q = resp ? L0 - query_out_len(out_len, 0) : L0;
       for (uint32_t i = 0; i < W; ++i) {
         Ptrs P = worker_ptrs(ws, L, r, i);
-        const int32_t L0 = (int32_t)(offsets[1] - offsets[0]);
-        h[0][i] = match_lcp(P, P.hdr->arena_sel, tokens + offsets[0], resp ? L0 - query_out_len(out_len, 0) : L0,
-                            path_of(i));
-        P.hdr->matched_tokens += (uint64_t)h[0][i];
+        h[0][i] = match_lcp(P, P.hdr->arena_sel, tokens + offsets[0], L0q, path_of(i));
+        if (rtree) {
+          Ptrs Pr = router_ptrs(ws, L, r, i);
+          g[0][i] = match_lcp(Pr, Pr.hdr->arena_sel, tokens + offsets[0], L0q, rpath_of(i));
+        }
+        P.hdr->matched_tokens += (uint64_t)est[0][i];
       }
     }
-    int32_t stale = -1, Lprev = 0, ell_prev = 0;
     for (uint64_t j = 0; j < n; ++j) {
       const int cur = (int)(j & 1u);
       const int32_t* qs = tokens + offsets[j];
@@ -87,13 +108,8 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       const int32_t Ln = has_next ? (int32_t)(offsets[j + 2] - offsets[j + 1]) : 0;
       const int32_t Lnq = has_next && resp ? Ln - query_out_len(out_len, j + 1) : Ln;
       double eh[kMaxWorkers], ch[kMaxWorkers];
-      if (stale >= 0) {
-        Ptrs P = worker_ptrs(ws, L, r, (uint32_t)stale);
-        h[cur][stale] = match_incremental(P, P.hdr->arena_sel, qs, Lq, Lprev, ell_prev, path_of((uint32_t)stale));
-        P.hdr->matched_tokens += (uint64_t)h[cur][stale];
-      }
       for (uint32_t i = 0; i < W; ++i)
-        eh[i] = lbgr_score(C, worker_ptrs(ws, L, r, i).hdr, h[cur][i], Lq, &ch[i]);
+        eh[i] = lbgr_score(C, worker_ptrs(ws, L, r, i).hdr, est[cur][i], Lq, &ch[i]);
       uint32_t best = 0;
       for (uint32_t i = 1; i < W; ++i)
         if (eh[i] < eh[best]) best = i;
@@ -109,25 +125,26 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         for (uint32_t i = 1; i < W; ++i) {
           if (load(i) < load(lo)) lo = i;
           if (load(i) > load(hi)) hi = i;
-          if (h[cur][i] > h[cur][hmax]) hmax = i;
+          if (est[cur][i] > est[cur][hmax]) hmax = i;
           if (size(i) < size(small)) small = i;
         }
         if (load(hi) - load(lo) > (uint32_t)cfg->ca_balance_abs &&
             (double)load(hi) > cfg->ca_balance_rel * (double)load(lo))
           best = lo;
-        else if ((double)h[cur][hmax] > cfg->ca_cache_threshold * (double)Lq)
+        else if ((double)est[cur][hmax] > cfg->ca_cache_threshold * (double)Lq)
           best = hmax;
         else
           best = small;
       }
       Ptrs P = worker_ptrs(ws, L, r, best);
-      uint32_t err = commit_route(C, P, ch[best], h[cur][best], Lq, t, olen);
+      uint32_t err = commit_route(C, P, ch[best], h[cur][best], est[cur][best], Lq, t, olen);
       if (route) route[r * n + j] = (int32_t)best;
       if (hits) hits[r * n + j] = h[cur][best];
       if (all_hits)
-        for (uint32_t i = 0; i < W; ++i) all_hits[(r * n + j) * W + i] = h[cur][i];
+        for (uint32_t i = 0; i < W; ++i) all_hits[(r * n + j) * W + i] = est[cur][i];
       // LCP of this path and the next; then of the next prompt with this
-      // path (routed worker) and with this prompt (the others)
+      // path (routed cache) and with this prompt (the other caches and
+      // every router tree)
       int32_t ellp = 0;
       if (has_next) {
         const int32_t m = Lp < Ln ? Lp : Ln;
@@ -162,22 +179,59 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       }
       if (err) return (int)err;
       if (has_next) {
+        h[cur ^ 1][best] = match_incremental(P, P.hdr->arena_sel, qn, Lnq, Lp, ell_r, path_of(best));
+        if (!rtree) P.hdr->matched_tokens += (uint64_t)h[cur ^ 1][best];
         for (uint32_t i = 0; i < W; ++i) complete_and_decay(C, worker_ptrs(ws, L, r, i), arrival[j + 1], t);
+      }
+      if (rtree) {
+        // the router adds the prompt to its tree of the routed worker
+        Ptrs Pr = router_ptrs(ws, L, r, best);
+        InsertArgs ia;
+        ia.seed = C.seed;
+        ia.jg = j;
+        ia.worker = best;
+        ia.replica = r;
+        ia.B = L.RB;
+        ia.rn = 0;
+        ia.rw = nullptr;
+        ia.ready = nullptr;
+        ia.ready_need = 0;
+        err = lru_insert(Pr, ia, qs, Lq, g[cur][best], rpath_of(best), nullptr);
+        if (err) return (int)err;
+        if (has_next) {
+          g[cur ^ 1][best] = match_incremental(Pr, Pr.hdr->arena_sel, qn, Lnq, Lq, ell, rpath_of(best));
+          P.hdr->matched_tokens += (uint64_t)g[cur ^ 1][best];
+        }
+      }
+      if (has_next) {
         for (uint32_t i = 0; i < W; ++i) {
           if (i == best) continue;
           Ptrs Pi = worker_ptrs(ws, L, r, i);
           h[cur ^ 1][i] = match_incremental(Pi, Pi.hdr->arena_sel, qn, Lnq, h[cur][i], ell, path_of(i));
-          Pi.hdr->matched_tokens += (uint64_t)h[cur ^ 1][i];
+          if (rtree) {
+            Ptrs Pr = router_ptrs(ws, L, r, i);
+            g[cur ^ 1][i] = match_incremental(Pr, Pr.hdr->arena_sel, qn, Lnq, g[cur][i], ell, rpath_of(i));
+          }
+          Pi.hdr->matched_tokens += (uint64_t)est[cur ^ 1][i];
         }
       }
-      stale = (int32_t)best;
-      Lprev = Lp;
-      ell_prev = ell_r;
       tprev = t;
     }
   }
   for (uint32_t r = 0; r < L.R; ++r)
-    for (uint32_t i = 0; i < W; ++i) worker_stats(worker_ptrs(ws, L, r, i), out + (uint64_t)r * W + i);
+    for (uint32_t i = 0; i < W; ++i) {
+      kvr_worker_stats* o = out + (uint64_t)r * W + i;
+      worker_stats(worker_ptrs(ws, L, r, i), o);
+      if (rtree) {
+        Ptrs Pr = router_ptrs(ws, L, r, i);
+        kvr_worker_stats t;
+        worker_stats(Pr, &t);
+        o->router_resident = t.resident;
+        o->router_digest_sum = t.digest_sum;
+        o->router_digest_xor = t.digest_xor;
+        o->router_evictions = Pr.hdr->evictions;
+      }
+    }
   return 0;
 }
 

@@ -31,7 +31,7 @@ def test_config_default_holds_paper_constants():
     assert c.abi_version == K.KVR_ABI_VERSION
     assert c.alpha_cached == 0.0 and c.alpha_miss == 1.0
     assert c.rho == 31.0 / 32.0 and c.decay_interval_us == 20000 and c.lr == 0.992
-    assert c.cache_responses == 0 and c.batch_size == 1
+    assert c.cache_responses == 0 and c.batch_size == 1 and c.router_tree == 0
 
 
 def test_continuous_batching_regions_only_when_used():
@@ -49,6 +49,7 @@ BAD = [
     dict(lr=math.inf), dict(nlms_eps=-1.0), dict(rls_p0=0.0), dict(alpha_miss=math.nan),
     dict(true_miss_us=-1), dict(num_replicas=0), dict(abi_version=1), dict(struct_size=8),
     dict(cache_responses=2), dict(batch_size=0), dict(batch_size=257), dict(batch_size=11),
+    dict(router_tree=2), dict(router_tree=1, router_tree_tokens=50),
 ]
 
 

@@ -27,44 +27,48 @@ pytestmark = pytest.mark.gpu
 BATCH = 2000
 # (config, sampled replicas, prefix compared with the oracle, eviction,
 # cached responses: every turn's 4-token response is cached with its prompt
-# and is part of the next turn's prompt, batch size of continuous batching)
+# and is part of the next turn's prompt, batch size of continuous batching,
+# approximate router tree with the cache's budget)
 CASES = [
-    (3, [0, 85, 170, 255], 24000, "rlt", 0, 1),
-    (4, [0, 42, 127], 24000, "rlt", 0, 1),
-    (5, [0, 31], 8000, "rlt", 0, 1),
-    (3, [0, 255], 24000, "lru", 0, 1),
-    (5, [0, 31], 8000, "lru", 0, 1),
-    (4, [0, 127], 24000, "rlt", 1, 1),
-    (5, [0, 31], 8000, "rlt", 0, 16),
-    (4, [0, 127], 24000, "lru", 1, 16),
+    (3, [0, 85, 170, 255], 24000, "rlt", 0, 1, 0),
+    (4, [0, 42, 127], 24000, "rlt", 0, 1, 0),
+    (5, [0, 31], 8000, "rlt", 0, 1, 0),
+    (3, [0, 255], 24000, "lru", 0, 1, 0),
+    (5, [0, 31], 8000, "lru", 0, 1, 0),
+    (4, [0, 127], 24000, "rlt", 1, 1, 0),
+    (5, [0, 31], 8000, "rlt", 0, 16, 0),
+    (4, [0, 127], 24000, "lru", 1, 16, 0),
+    (5, [0, 31], 8000, "rlt", 0, 1, 1),
+    (4, [0, 127], 24000, "rlt", 1, 1, 1),
 ]
 
 
-def _oracle_many(stream, W, B, replicas, n, evict, resp, beta):
+def _oracle_many(stream, W, B, replicas, n, evict, resp, beta, rt):
     with cf.ThreadPoolExecutor(max_workers=len(replicas)) as ex:
         futs = {r: ex.submit(O.run, stream, W, B, replica=r, n=n, all_hits=True, evict=evict,
-                             cache_responses=resp, batch_size=beta) for r in replicas}
+                             cache_responses=resp, batch_size=beta, router_tree=rt) for r in replicas}
         return {r: f.result() for r, f in futs.items()}
 
 
-@pytest.mark.parametrize("cfg,replicas,nprefix,evict,resp,beta", CASES,
+@pytest.mark.parametrize("cfg,replicas,nprefix,evict,resp,beta,rt", CASES,
                          ids=[f"config{c[0]}-{c[3]}" + ("-responses" if c[4] else "") +
-                              (f"-batch{c[5]}" if c[5] > 1 else "") for c in CASES])
-def test_full_size(cfg, replicas, nprefix, evict, resp, beta):
+                              (f"-batch{c[5]}" if c[5] > 1 else "") + ("-routertree" if c[6] else "")
+                              for c in CASES])
+def test_full_size(cfg, replicas, nprefix, evict, resp, beta, rt):
     p = PRESETS[cfg]
     R, W, B = p["R"], p["W"], p["B"]
     t0 = time.time()
     s = generate(dict(p["stream"], responses=True) if resp else p["stream"])
     note(f"config {cfg}: R={R} W={W} B={B} n={s.n} tokens={s.tokens.size} responses={resp} batch={beta} "
-         f"({time.time() - t0:.1f} s)")
+         f"router_tree={rt} ({time.time() - t0:.1f} s)")
     assert nprefix % BATCH == 0 and nprefix < s.n
 
     # the oracle runs on host threads while the GPU works
     pool = cf.ThreadPoolExecutor(max_workers=1)
-    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix, evict, resp, beta)
+    ofut = pool.submit(_oracle_many, s, W, B, replicas, nprefix, evict, resp, beta, rt)
 
     sim = K.Simulator(R, W, B, s.max_len, evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict],
-                      cache_responses=resp, batch_size=beta)
+                      cache_responses=resp, batch_size=beta, router_tree=rt)
     try:
         ds = sim.upload(s)
         route = np.empty((R, s.n), np.int32)

@@ -369,3 +369,42 @@ def test_batching_multiturn_with_responses_and_collector():
 def test_batching_rejects_a_running_batch_larger_than_the_cache():
     with pytest.raises(K.KvrError):
         K.kvr_workspace_size(K.kvr_config_default(1, 2, 100, 30, batch_size=4))
+
+
+# ---------------------------------------------------------------- approximate router tree
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_router_tree_random_parity(evict):
+    """The approximate router of App. E: the router's own L-LRU tree per
+    worker gives the estimates it scores with; the commit, the observed
+    latency and the hit counts take the cache's own match."""
+    rng = np.random.default_rng(81 + (evict == "lru"))
+    ev = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict]
+    for case in range(5):
+        sp = small_spec(n=int(rng.integers(100, 400)), groups=int(rng.integers(1, 9)),
+                        prefix_len=(1, int(rng.integers(3, 60))), suffix_len=(1, int(rng.integers(2, 40))),
+                        vocab=int(rng.integers(2, 30)), seed=60 + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 7))
+        B = int(max(s.max_len, rng.integers(2, 600)))
+        RB = int(max(s.max_len, rng.integers(2, 800)))
+        router = ["lbgr", "cache_aware"][case % 2]
+        note(f"router tree/{evict} case {case}: W={W} B={B} RB={RB} n={s.n} router={router}")
+        res, stats = gpu_run(s, 3, W, B, seed=case, evict=ev, router=ROUTER.get(router, K.KVR_ROUTE_LBGR),
+                             router_tree=1, router_tree_tokens=RB)
+        assert_parity(s, res, stats, W, B, range(3), seed=case, evict=evict, router=router, router_tree=1,
+                      router_tree_tokens=RB)
+
+
+def test_router_tree_with_responses_and_batching():
+    sp = {"kind": "sessions", "n_sessions": 300, "turns": (1, 8), "start_len": 32, "ext_len": (8, 48),
+          "vocab": 32000, "responses": True, "out_len": 4, "turn_rate": 1.0, "seed": 6}
+    s = generate(sp)
+    W, R, beta = 4, 3, 3
+    B = beta * s.max_len
+    note(f"router tree multiturn: n={s.n} max_len={s.max_len} B={B}")
+    res, stats = gpu_run(s, R, W, B, batch=300, batch_size=beta, cache_responses=1, router_tree=1,
+                         router_tree_tokens=B // 2)
+    assert_parity(s, res, stats, W, B, range(R), batch_size=beta, cache_responses=1, router_tree=1,
+                  router_tree_tokens=B // 2)
+    assert sum(w["router_evictions"] for w in stats[0]) > 0

@@ -20,7 +20,7 @@ def _compare(s, R, W, B, update="nlms", seed=0, ucap=8192, evict="rlt", router="
     assert e["rc"] == 0
     for r in range(R):
         o = O.run(s, W, B, replica=r, all_hits=True, update=update, seed=seed, evict=evict, router=router,
-                  **{k: v for k, v in cfg.items() if k.startswith("ca_") or k in ("cache_responses", "batch_size")})
+                  **{k: v for k, v in cfg.items() if k.startswith("ca_") or k in ("cache_responses", "batch_size", "router_tree", "router_tree_tokens")})
         np.testing.assert_array_equal(e["route"][r], o["route"])
         np.testing.assert_array_equal(e["all_hits"][r], o["all_hits"])
         for i in range(W):
@@ -227,3 +227,39 @@ def test_continuous_batching_with_responses_routers_and_collector():
                      evict=["rlt", "lru"][case % 2], arena_words=2 * B + 2 * s.max_len + 64)
         gc += sum(w["gc_runs"] for w in e["workers"][0])
     assert gc > 20
+
+
+@pytest.mark.parametrize("evict", ["rlt", "lru"])
+def test_router_tree_random_instances(evict):
+    """The approximate router (App. E): a second, L-LRU tree per worker holds
+    the routed prompts; the router scores with its matches, the commit and
+    the hit counts take the cache's own."""
+    rng = np.random.default_rng(808 + (evict == "lru"))
+    for case in range(40):
+        sp = small_spec(n=int(rng.integers(30, 200)), groups=int(rng.integers(1, 8)),
+                        prefix_len=(1, int(rng.integers(2, 25))), suffix_len=(1, int(rng.integers(2, 15))),
+                        vocab=int(rng.integers(2, 10)), seed=900 + case)
+        s = generate(sp)
+        W = int(rng.integers(1, 5))
+        B = int(max(s.max_len, rng.integers(2, 150)))
+        RB = int(max(s.max_len, rng.integers(2, 200)))
+        router = ["lbgr", "cache_aware"][case % 2]
+        e = _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case, evict=evict, router=router,
+                     router_tree=1, router_tree_tokens=RB, ucap=[0, 8192][case % 2])
+        assert all(w["router_resident"] <= RB for w in e["workers"][0])
+
+
+def test_router_tree_with_responses_batching_and_collector():
+    rng = np.random.default_rng(77)
+    gc = 0
+    for case in range(16):
+        beta = int(rng.integers(1, 4))
+        B = int(rng.integers(40, 200))
+        s = random_response_stream(rng, int(rng.integers(50, 200)), int(rng.integers(2, 5)),
+                                   max(1, B // beta - 6), 6, B // beta)
+        W = int(rng.integers(1, 4))
+        RB = int(max(s.max_len, rng.integers(10, 100)))
+        e = _compare(s, 2, W, B, seed=case, batch_size=beta, cache_responses=1, router_tree=1,
+                     router_tree_tokens=RB, evict=["rlt", "lru"][case % 2], arena_words=2 * B + 2 * s.max_len + 64)
+        gc += sum(w["gc_runs"] for w in e["workers"][0])
+    assert gc > 0
