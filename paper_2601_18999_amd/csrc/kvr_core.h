@@ -336,48 +336,35 @@ __device__ void arr_erase(int32_t* a, uint32_t n, uint32_t pos) {
 
 // ---------------------------------------------------------------- child arrays
 
-// Child of a node whose edge starts with `tok`, or -1.  Four chunks of 64
-// entries per round trip.
+// Child of a node whose edge starts with `tok`, or -1.  (One chunk of 64
+// entries per round trip: most child arrays are short, and measured faster
+// than several chunks in flight.)
 __device__ int32_t child_find(const int32_t* ar, const NodeRec& nd, int32_t tok) {
-  constexpr int kU = 4;
-  for (int32_t b = 0; b < nd.nchild; b += kU * KVR_WAVE) {
-    int2 e[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      e[u].x = 0;
-      e[u].y = -1;
-      if (k < nd.nchild) e[u] = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+  for (int32_t b = 0; b < nd.nchild; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    bool hit = false;
+    int32_t id = -1;
+    if (k < nd.nchild) {
+      int2 e = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+      hit = (e.x == tok);
+      id = e.y;
     }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      const uint64_t m = __ballot(k < nd.nchild && e[u].x == tok);
-      if (m) return __shfl(e[u].y, first_lane(m), KVR_WAVE);
-    }
+    uint64_t m = __ballot(hit);
+    if (m) return __shfl(id, first_lane(m), KVR_WAVE);
   }
   return -1;
 }
 
 // Child with the largest first token < tok (below) or the smallest > tok.
 __device__ int32_t child_neighbor(const int32_t* ar, const NodeRec& nd, int64_t tok, bool below) {
-  constexpr int kU = 4;
   uint64_t best = below ? 0ull : ~0ull;
-  for (int32_t b = 0; b < nd.nchild; b += kU * KVR_WAVE) {
-    int2 e[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      if (k < nd.nchild) e[u] = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      if (k < nd.nchild) {
-        const uint64_t key = ((uint64_t)(uint32_t)e[u].x << 32) | (uint32_t)e[u].y;
-        if (below && (int64_t)e[u].x < tok && key > best) best = key;
-        if (!below && (int64_t)e[u].x > tok && key < best) best = key;
-      }
+  for (int32_t b = 0; b < nd.nchild; b += KVR_WAVE) {
+    int32_t k = b + lane_id();
+    if (k < nd.nchild) {
+      int2 e = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+      uint64_t key = ((uint64_t)(uint32_t)e.x << 32) | (uint32_t)e.y;
+      if (below && (int64_t)e.x < tok && key > best) best = key;
+      if (!below && (int64_t)e.x > tok && key < best) best = key;
     }
   }
   best = below ? wave_max_u64(best) : wave_min_u64(best);

@@ -160,8 +160,8 @@ __device__ __forceinline__ void store_h(int32_t h, int32_t* hslot) {
 }
 
 // The next query's h on the workers other than `best`, taken one item at a
-// time from an LDS counter, so a wave that drew long matches takes fewer
-// (the routing wave joins once its own work is done).  Items 0..W-1 are the
+// time from an LDS counter, so a wave that drew long matches takes fewer.
+// Items 0..W-1 are the
 // caches; with the approximate router, items W..2W-1 are the router's trees.
 // The index is wave-uniform (lane 0's atomic, read back from lane 0) and the
 // loop is bounded by the number of items.
@@ -244,14 +244,17 @@ __device__ __forceinline__ uint32_t router_admit(const StepArgs& a, uint32_t r, 
 // the next query is completed from the path of the inserted query.  With
 // the approximate router every worker has two trees, the cache and the
 // router's, each matched incrementally; the router's tree of the routed
-// worker is updated by a helper wave.
+// worker is updated by a helper wave.  The approximate router (RT) and
+// continuous batching (BA) are template switches, so the kernel without
+// them carries none of their registers.
+template <bool RT, bool BA>
 __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   // dynamic LDS: two query buffers (max_query_tokens entries each), the high
   // halves of the draw words, the match paths (the caches', then the router
   // trees'), then the staged candidate list
   extern __shared__ int32_t smem[];
   const uint32_t W = a.L.W;
-  const bool rtree = a.L.has_router != 0;
+  constexpr bool rtree = RT;
   const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
   uint32_t* rw = reinterpret_cast<uint32_t*>(smem + 2 * qstride);
   PathArea paths, rpaths;
@@ -422,7 +425,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
                                                 : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
       // continuous batching: the path joins the worker's running batch
-      if (!err && P.beta > 1) err = batch_admit(P, paths.of(best), qs, Lp, dbg);
+      if (BA && !err && P.beta > 1) err = batch_admit(P, paths.of(best), qs, Lp, dbg);
       report_error(g, r, jg, err, dbg, &abort_sh);
       // the routed worker's h for the next query, from the path of the
       // query just inserted (all of it is cached now: the old h is Lp)
@@ -433,10 +436,6 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
           store_h(h, &h_sh[cur ^ 1u][best]);
         else
           count_matched(Pb, h, &h_sh[cur ^ 1u][best]);
-        // then the other workers' matches that no helper has taken yet
-        if (nh > 0)
-          take_matches(a, r, W, best, qn, Lnq, ell, h_sh[cur], h_sh[cur ^ 1u], g_sh[cur], g_sh[cur ^ 1u], paths,
-                       rpaths, rtree, &next_sh);
       }
       if (nh == 0 && !err) {
         if (has_next) {
@@ -590,7 +589,15 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
                      a.offsets, a.n);
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
   const size_t lds = step_lds_bytes(a.L.maxL, a.L.W, a.ucap, a.rcap, a.L.has_router ? 2u : 1u);
-  hipLaunchKernelGGL(step_kernel, dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  const bool rt = a.L.has_router != 0, ba = a.L.beta > 1;
+  if (rt && ba)
+    hipLaunchKernelGGL((step_kernel<true, true>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  else if (rt)
+    hipLaunchKernelGGL((step_kernel<true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  else if (ba)
+    hipLaunchKernelGGL((step_kernel<false, true>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  else
+    hipLaunchKernelGGL((step_kernel<false, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   return hipGetLastError();
 }
 
@@ -599,18 +606,30 @@ hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Static LDS of the step kernel (its __shared__ variables), from the
-// compiled kernel's attributes.
+static const void* const kStepKernels[4] = {
+    reinterpret_cast<const void*>(step_kernel<false, false>), reinterpret_cast<const void*>(step_kernel<false, true>),
+    reinterpret_cast<const void*>(step_kernel<true, false>), reinterpret_cast<const void*>(step_kernel<true, true>)};
+
+// Static LDS of the step kernels (their __shared__ variables, the largest),
+// from the compiled kernels' attributes.
 hipError_t step_static_lds(size_t* bytes) {
-  hipFuncAttributes fa;
-  const hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(step_kernel));
-  if (e == hipSuccess) *bytes = fa.sharedSizeBytes;
-  return e;
+  size_t mx = 0;
+  for (const void* f : kStepKernels) {
+    hipFuncAttributes fa;
+    const hipError_t e = hipFuncGetAttributes(&fa, f);
+    if (e != hipSuccess) return e;
+    if (fa.sharedSizeBytes > mx) mx = fa.sharedSizeBytes;
+  }
+  *bytes = mx;
+  return hipSuccess;
 }
 
 hipError_t set_step_lds_limit(size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(step_kernel),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  for (const void* f : kStepKernels) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace kvr
