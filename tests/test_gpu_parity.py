@@ -408,3 +408,19 @@ def test_router_tree_with_responses_and_batching():
     assert_parity(s, res, stats, W, B, range(R), batch_size=beta, cache_responses=1, router_tree=1,
                   router_tree_tokens=B // 2)
     assert sum(w["router_evictions"] for w in stats[0]) > 0
+
+
+# ---------------------------------------------------------------- the paper's GSP shape
+
+@pytest.mark.parametrize("cfg,evict", [(7, "rlt"), (7, "lru"), (6, "rlt")])
+def test_gsp_paper_shape_full_stream(cfg, evict):
+    """App. A's GSP (128 groups x 32 queries, lengths 512..8192, prefix ratio
+    0.5, 4 workers with 200k-token caches), in the worst-case round-robin
+    order and in random order: the whole stream against the oracle."""
+    p = PRESETS[cfg]
+    s = generate(p["stream"])
+    ev = {"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict]
+    note(f"{p['name']}/{evict}: n={s.n}")
+    res, stats = gpu_run(s, 4, p["W"], p["B"], batch=1024, evict=ev)
+    assert_parity(s, res, stats, p["W"], p["B"], [0, 3], evict=evict)
+    assert sum(w["evictions"] for w in stats[0]) > 0

@@ -13,6 +13,12 @@ workload families (Sec. 5 "Workloads"; App. A):
   of a session is the session start followed by the first k extensions.
 * ``paths``     - an explicit list of token paths queried in a given order
   (used for the constructions in the paper's proofs).
+* ``gsp``       - the paper's own GSP shape (App. A): G groups of Q queries
+  each; a group's prompt length cycles over a list of lengths across groups,
+  a fixed share of it (the prefix ratio) is the group's shared prefix and
+  the rest a fresh suffix; queries come in a random order or in the
+  worst-case round-robin order (one query per group per turn, the groups in
+  a fixed cycle).
 
 Arrivals are a Poisson process (exponential gaps) unless a recipe says
 otherwise; times are integer microseconds.  Output length is 4 tokens
@@ -242,6 +248,40 @@ def _gen_sessions(sp: Dict[str, Any], rng: np.random.Generator) -> Stream:
     return Stream(tokens, offsets, arrival, out_len, dict(sp, n=n))
 
 
+def _gen_gsp(sp: Dict[str, Any], rng: np.random.Generator) -> Stream:
+    g, per, vocab = int(sp["groups"]), int(sp["per_group"]), int(sp["vocab"])
+    lengths = [int(x) for x in sp["lengths"]]
+    glen = np.array([lengths[k % len(lengths)] for k in range(g)], dtype=np.int64)
+    plen = np.floor(glen * float(sp["prefix_ratio"])).astype(np.int64)
+    prefixes = [rng.integers(0, vocab, size=int(l), dtype=np.int32) for l in plen]
+    n = g * per
+    if sp.get("order", "random") == "round_robin":
+        group = np.tile(np.arange(g), per)  # turn t: groups 0..G-1
+    else:
+        group = rng.permutation(np.repeat(np.arange(g), per))
+    limit = sp.get("n")
+    if limit is not None:
+        group = group[: int(limit)]
+        n = group.shape[0]
+    slen = glen[group] - plen[group]
+    suffix_tokens = rng.integers(0, vocab, size=int(slen.sum()), dtype=np.int32)
+    arrival = _poisson_times_us(rng, n, float(sp.get("rate", 12.0)))
+
+    def fill(tok, off):
+        so = 0
+        for j in range(n):
+            o = int(off[j])
+            p = prefixes[group[j]]
+            tok[o:o + p.shape[0]] = p
+            s = int(slen[j])
+            tok[o + p.shape[0]:o + p.shape[0] + s] = suffix_tokens[so:so + s]
+            so += s
+
+    tokens, offsets = _assemble(glen[group], fill)
+    out_len = np.full(n, int(sp.get("out_len", 4)), dtype=np.uint16)
+    return Stream(tokens, offsets, arrival, out_len, dict(sp, n=n))
+
+
 def _gen_paths(sp: Dict[str, Any], rng: np.random.Generator) -> Stream:
     paths: List[Sequence[int]] = sp["paths"]
     order = sp.get("order")
@@ -265,7 +305,7 @@ def _gen_paths(sp: Dict[str, Any], rng: np.random.Generator) -> Stream:
 
 
 _KINDS = {"groups": _gen_groups, "two_level": _gen_two_level,
-          "sessions": _gen_sessions, "paths": _gen_paths}
+          "sessions": _gen_sessions, "paths": _gen_paths, "gsp": _gen_gsp}
 
 
 def _append_responses(st: Stream, vocab: int, rng: np.random.Generator) -> Stream:
@@ -321,6 +361,16 @@ PRESETS: Dict[int, Dict[str, Any]] = {
         "stream": {"kind": "groups", "n": 200000, "groups": 256, "prefix_len": (2048, 8192),
                    "suffix_len": (128, 1024), "zipf_s": 0.8, "vocab": 128000, "rate": 12.0,
                    "burst": {"p_on": 1.0 / 500.0, "length": 500, "rate": 120.0}}},
+    # the paper's GSP setting (App. A): 128 groups x 32 queries, prompt
+    # lengths cycling over 512..8192 across groups, prefix ratio 0.5, 4
+    # workers with about 200k cached tokens each, 12 req/s; random order and
+    # the worst-case round-robin order (context runs, not benchmark lines)
+    6: {"name": "gsp_paper_random", "R": 64, "W": 4, "B": 200000,
+        "stream": {"kind": "gsp", "groups": 128, "per_group": 32, "lengths": (512, 1024, 2048, 4096, 8192),
+                   "prefix_ratio": 0.5, "order": "random", "vocab": 32000, "rate": 12.0}},
+    7: {"name": "gsp_paper_round_robin", "R": 64, "W": 4, "B": 200000,
+        "stream": {"kind": "gsp", "groups": 128, "per_group": 32, "lengths": (512, 1024, 2048, 4096, 8192),
+                   "prefix_ratio": 0.5, "order": "round_robin", "vocab": 32000, "rate": 12.0}},
 }
 
 
