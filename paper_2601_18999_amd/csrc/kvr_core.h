@@ -394,6 +394,29 @@ __device__ __forceinline__ int32_t leaf_rank(const Ptrs& P, const St& s, const i
   return after ? pos + 1 : pos;
 }
 
+// Rank in the leaf list (lexicographic order) of the leaf that the insertion
+// of a path creates, on the tree as it is before that insertion: the path's
+// cached part ends in node `last` (0: the root) after `lastcov` of its
+// `lastlen` edge tokens, and tok is the path's first token not cached.  A
+// match ending inside the edge of last will split it there, and the new leaf
+// goes before or after every leaf below last; ending at a leaf, the new leaf
+// takes its place; else it goes next to its neighbours among last's
+// children.  -1 on an inconsistency.
+__device__ int32_t new_leaf_rank(const Ptrs& P, const St& s, const int32_t* ar, int32_t last, int32_t lastcov,
+                                 int32_t lastlen, int32_t tok) {
+  if (last != 0 && lastcov < lastlen) {
+    const int32_t tail_tok = ar[P.nodes[last].off + (uint32_t)lastcov];
+    return leaf_rank(P, s, ar, last, !(tok < tail_tok));
+  }
+  const NodeRec na = P.nodes[last];
+  if (last != 0 && na.nchild == 0) return arr_find(P.leaf, s.nleaves, last);
+  if (na.nchild == 0) return 0;  // the empty tree
+  const int32_t cb = child_neighbor(ar, na, tok, true);
+  if (cb >= 0) return leaf_rank(P, s, ar, cb, true);
+  const int32_t ca = child_neighbor(ar, na, tok, false);
+  return leaf_rank(P, s, ar, ca, false);
+}
+
 // ---------------------------------------------------------------- allocation
 
 // Wave-cooperative copy of n words (eight loads in flight per lane).
@@ -803,7 +826,24 @@ struct InsertArgs {
   // there once *ready reaches ready_need (LDS counter, workgroup scope)
   const uint32_t* ready;
   uint32_t ready_need;
+  // when non-null: another wave computes the new leaf's rank in the leaf
+  // list from the recorded match path (new_leaf_rank on the tree before the
+  // insertion) into *rank and then sets *rank_ready to 1, or to 2 when it
+  // could not or the match ends inside an edge (LDS, workgroup scope)
+  const int32_t* rank;
+  const uint32_t* rank_ready;
 };
+
+// The new leaf's rank from the other wave (bounded wait), or -1 if it could
+// not compute it or the wait ran out.
+__device__ __forceinline__ int32_t await_rank(const InsertArgs& ia) {
+  uint32_t spins = 0, rd;
+  while ((rd = __hip_atomic_load(ia.rank_ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) == 0u) {
+    if (++spins > (1u << 22)) break;
+    __builtin_amdgcn_s_sleep(2);
+  }
+  return rd == 1u ? *ia.rank : -1;
+}
 
 // Word 0 of Philox4x64-10 for draw d of this insertion: key (seed, replica),
 // counter (query index, worker, d, 0).
@@ -1311,35 +1351,21 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         ar = arena_of(P, s.arena_sel);
       }
     }
-    // ---- rank of the new leaf in the leaf list
-    int32_t pos;
-    bool replace = false;
-    {
-      NodeRec na = P.nodes[a];
-      if (a != 0 && na.nchild == 0) {
-        pos = arr_find(P.leaf, s.nleaves, a);
-        replace = true;
-      } else if (split) {
-        NodeRec nt = P.nodes[last];
-        int32_t tail_tok = ar[nt.off];
-        pos = leaf_rank(P, s, ar, last, !(qs[h] < tail_tok));
-      } else if (na.nchild == 0) {
-        pos = 0;
-      } else {
-        int32_t cb = child_neighbor(ar, na, qs[h], true);
-        if (cb >= 0) {
-          pos = leaf_rank(P, s, ar, cb, true);
-        } else {
-          int32_t ca = child_neighbor(ar, na, qs[h], false);
-          pos = leaf_rank(P, s, ar, ca, false);
-        }
-      }
-    }
-    if (pos < 0 || (uint32_t)pos > s.nleaves) {
-      KVR_FAIL_CHECK(s, 4, pos, s.nleaves, a);
-      goto fail;
-    }
+    // ---- rank of the new leaf in the leaf list: from another wave, which
+    // computes it on the tree before this insertion while this one marks
+    // (only when no edge is split: that would change what it reads), or here
+    int32_t pos = -1;
+    const bool rank_helper = ia.rank != nullptr && have_path && !split;
+    const bool replace = a != 0 && P.nodes[a].nchild == 0;
+    if (!rank_helper) pos = new_leaf_rank(P, s, ar, split ? last : a, 0, split ? 1 : 0, qs[h]);
     // ---- the new leaf node holding q[h, L)
+    bool ranked = false;
+    if (rank_helper && (uint64_t)s.arena_top + (uint32_t)nload > P.A) {
+      // a collection is coming, which moves what the other wave reads
+      pos = await_rank(ia);
+      if (pos < 0) pos = new_leaf_rank(P, s, ar, a, 0, 0, qs[h]);
+      ranked = true;
+    }
     uint32_t eoff;
     if (!arena_alloc(P, s, (uint32_t)nload, false, eoff)) goto fail;
     ar = arena_of(P, s.arena_sel);
@@ -1347,6 +1373,12 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     // except a collection, which fences first; the fence at the end of the
     // insertion orders them before the next match
     wave_copy(ar + eoff, qs + h, nload);
+    if (rank_helper && !ranked) {
+      // if the other wave could not, or takes too long, rank here (the tree
+      // is as the local ranking above would see it)
+      pos = await_rank(ia);
+      if (pos < 0) pos = new_leaf_rank(P, s, ar, a, 0, 0, qs[h]);
+    }
     l = node_alloc(P, s);
     if (l < 0) goto fail;
     {
@@ -1363,6 +1395,10 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     }
     if (!child_add(P, s, a, qs[h], l)) goto fail;
     ar = arena_of(P, s.arena_sel);
+    if (pos < 0 || (uint32_t)pos > s.nleaves) {
+      KVR_FAIL_CHECK(s, 4, pos, s.nleaves, a);
+      goto fail;
+    }
     if (replace) {
       if (lane_id() == 0) P.leaf[pos] = l;
       wave_mem_sync();
@@ -1653,6 +1689,40 @@ fail:
     dbg[3] = s.dbg_val[2];
   }
   return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
+
+// The rank in the leaf list of the leaf the insertion of q (h cached tokens,
+// h < L) creates in the routed worker's cache, for the insertion wave, on
+// the tree before the insertion: from the recorded match path of q, when
+// that match ends at a node boundary (an edge split would change what this
+// reads).  Publishes *rank and sets *ready to 1, or to 2 without a rank.
+__device__ __forceinline__ void rank_for_insertion(const Ptrs& P, const PathRef& pr, const int32_t* qs, int32_t h,
+                                                   int32_t* rank, uint32_t* ready) {
+  int32_t pos = -1;
+  const int32_t pc = *pr.cnt;
+  if (pc <= kPathMax) {
+    int32_t last = 0, cov = 0, len = 0;
+    bool ok = true;
+    if (h > 0) {
+      int32_t e = pc - 1;
+      while (e > 0 && pr.start[e] >= h) --e;
+      ok = pc > 0 && pr.start[e] < h && pr.end[e] >= h;
+      if (ok) {
+        last = pr.node[e];
+        cov = h - pr.start[e];
+        len = pr.end[e] - pr.start[e];
+      }
+    }
+    if (ok && cov == len) {
+      const St s = load_st(P.hdr);
+      pos = new_leaf_rank(P, s, arena_of(P, s.arena_sel), last, cov, len, qs[h]);
+    }
+  }
+  if (lane_id() == 0) {
+    *rank = pos;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __hip_atomic_store(ready, pos >= 0 ? 1u : 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
 }
 
 // ---------------------------------------------------------------- matching

@@ -227,6 +227,8 @@ __device__ __forceinline__ uint32_t router_admit(const StepArgs& a, uint32_t r, 
   ia.rw = nullptr;
   ia.ready = nullptr;
   ia.ready_need = 0;
+  ia.rank = nullptr;
+  ia.rank_ready = nullptr;
   const uint32_t err = lru_insert(Pr, ia, qs, Lq, hr, rpaths.of(best), dbg);
   if (!err && has_next)
     count_matched(worker_ptrs(a.ws, a.L, r, best),
@@ -282,6 +284,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ uint32_t nev_sh;
   __shared__ uint32_t wready_sh;  // helper waves done with the draw words
   __shared__ uint32_t next_sh;    // next item for the helpers' matches
+  __shared__ int32_t rank_sh;     // the new leaf's rank, from the last helper wave
+  __shared__ uint32_t rank_ready_sh;
   // the hits the router scores with: the caches' own, or its trees'
   int32_t(*est)[kMaxWorkers] = rtree ? g_sh : h_sh;
 
@@ -366,6 +370,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         hins_sh = hins;
         wready_sh = 0;
         next_sh = 0;
+        rank_ready_sh = 0;
         const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, est[cur][best], Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
@@ -421,6 +426,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.rw = rw;
       ia.ready = nh && rn ? &wready_sh : nullptr;
       ia.ready_need = nh;
+      ia.rank = nh && a.C.evict == KVR_EVICT_RLT ? &rank_sh : nullptr;
+      ia.rank_ready = &rank_ready_sh;
       int64_t dbg[4] = {0, 0, 0, 0};
       uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
                                                 : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
@@ -454,6 +461,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
                        rpaths, rtree, &next_sh);
       }
     } else {
+      // the last helper first ranks the insertion's new leaf
+      if (wave == nwaves - 1 && a.C.evict == KVR_EVICT_RLT && hins < Lp)
+        rank_for_insertion(worker_ptrs(a.ws, a.L, r, best), paths.of(best), qs, hins, &rank_sh, &rank_ready_sh);
       for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
         rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");

@@ -24,6 +24,7 @@ inline int __builtin_amdgcn_readfirstlane(int v) { return v; }
 inline void __builtin_amdgcn_s_sleep(int) {}
 #define __ATOMIC_ACQUIRE_EMUL 0
 template <typename T> inline T __hip_atomic_load(const T* p, int, int) { return *p; }
+template <typename T> inline void __hip_atomic_store(T* p, T v, int, int) { *p = v; }
 template <typename T> inline T __hip_atomic_fetch_add(T* p, T v, int, int) { T o = *p; *p += v; return o; }
 #ifndef __HIP_MEMORY_SCOPE_WORKGROUP
 #define __HIP_MEMORY_SCOPE_WORKGROUP 3

@@ -173,6 +173,17 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.rw = rwbuf.data();
         ia.ready = nullptr;
         ia.ready_need = 0;
+        // the new leaf's rank as the device's last helper wave computes it,
+        // from the recorded match path on the tree before the insertion
+        int32_t rank = -1;
+        uint32_t rank_ready = 0;
+        ia.rank = nullptr;
+        ia.rank_ready = nullptr;
+        if (C.evict == KVR_EVICT_RLT && hins < Lp) {
+          rank_for_insertion(P, path_of(best), qs, hins, &rank, &rank_ready);
+          ia.rank = &rank;
+          ia.rank_ready = &rank_ready;
+        }
         err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, path_of(best), nullptr)
                                        : lru_insert(P, ia, qs, Lp, hins, path_of(best), nullptr);
         if (!err && P.beta > 1) err = batch_admit(P, path_of(best), qs, Lp, nullptr);
@@ -196,6 +207,8 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.rw = nullptr;
         ia.ready = nullptr;
         ia.ready_need = 0;
+        ia.rank = nullptr;
+        ia.rank_ready = nullptr;
         err = lru_insert(Pr, ia, qs, Lq, g[cur][best], rpath_of(best), nullptr);
         if (err) return (int)err;
         if (has_next) {
