@@ -406,6 +406,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     const int32_t ell_r = ellp < Lnq ? ellp : Lnq;
     const int32_t ell = ell_r < Lq ? ell_r : Lq;
     const uint64_t jg = a.j0 + k;
+    // with two or more helpers, the last one ranks the new leaf of an RLT
+    // insertion while the others compute its draw words
+    const bool ranker = nh >= 2 && a.C.evict == KVR_EVICT_RLT && hins < Lp;
 
     // ---- phase B.  Wave 0: the insertion, then the routed worker's h for
     // the next query.  Helpers: the insertion's draw words first, then
@@ -425,8 +428,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.rn = rn;
       ia.rw = rw;
       ia.ready = nh && rn ? &wready_sh : nullptr;
-      ia.ready_need = nh;
-      ia.rank = nh && a.C.evict == KVR_EVICT_RLT ? &rank_sh : nullptr;
+      ia.ready_need = ranker ? nh - 1u : nh;
+      ia.rank = ranker ? &rank_sh : nullptr;
       ia.rank_ready = &rank_ready_sh;
       int64_t dbg[4] = {0, 0, 0, 0};
       uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
@@ -461,13 +464,17 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
                        rpaths, rtree, &next_sh);
       }
     } else {
-      // the last helper first ranks the insertion's new leaf
-      if (wave == nwaves - 1 && a.C.evict == KVR_EVICT_RLT && hins < Lp)
+      if (ranker && wave == nwaves - 1) {
+        // the last helper ranks the insertion's new leaf
         rank_for_insertion(worker_ptrs(a.ws, a.L, r, best), paths.of(best), qs, hins, &rank_sh, &rank_ready_sh);
-      for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += blockDim.x - KVR_WAVE)
-        rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-      if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      } else {
+        // the others compute the draw words
+        const uint32_t nd = blockDim.x - (ranker ? 2u : 1u) * KVR_WAVE;
+        for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += nd)
+          rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
       if (wave == 1) {
         if (has_next) {
           if ((uint32_t)lane < W)
