@@ -2148,41 +2148,68 @@ __device__ __forceinline__ int32_t query_out_len(const uint16_t* out_len, uint64
   return out_len ? (int32_t)out_len[k] : 4;
 }
 
-// LBGR score of one worker (Eq. LBGR-score with the features of Sec. 4.2
-// and the per-1k-token scaling of App. A).  *chat = estimated service time.
-__device__ double lbgr_score(const Consts& C, const WorkerHdr* w, int32_t h, int32_t L, double* chat) {
-  double x1 = (double)h * 0.001;
-  double x2 = (double)(L - h) * 0.001;
-  double x3 = w->P;
-  double x4 = 1.0;
-  double ch = C.alpha_cached * x1 + C.alpha_miss * x2;
-  double res = w->theta[0] * x1;
-  res = res + w->theta[1] * x2;
-  res = res + w->theta[2] * x3;
-  res = res + w->theta[3] * x4;
-  *chat = ch;
-  return (ch + w->P) + res;
+// The fields of a worker header that scoring and the commit read, loaded
+// together by the worker's lane (one round trip for all of them).
+struct RouteView {
+  double P, theta[4];
+  int64_t Wb;
+  uint32_t pend_head, pend_count, pending_max, size;
+  uint64_t routed, prompt_tokens, hit_tokens, lat_sum_us, lat_max_us;
+};
+
+__device__ __forceinline__ RouteView load_view(const WorkerHdr* w) {
+  RouteView v;
+  v.P = w->P;
+  for (int a = 0; a < 4; ++a) v.theta[a] = w->theta[a];
+  v.Wb = w->Wb;
+  v.pend_head = w->pend_head;
+  v.pend_count = w->pend_count;
+  v.pending_max = (uint32_t)w->pending_max;
+  v.size = w->size;
+  v.routed = w->routed;
+  v.prompt_tokens = w->prompt_tokens;
+  v.hit_tokens = w->hit_tokens;
+  v.lat_sum_us = w->lat_sum_us;
+  v.lat_max_us = w->lat_max_us;
+  return v;
 }
 
-// Commit a query on its routed worker: add the estimated service time to the
-// load estimate (Algorithm 2), advance the observed-latency queue and queue
-// the completion record.  hb = the worker's true hit (observed latency, hit
-// counter), hf = the hit the router scored with (the completion's features;
-// the same unless the router keeps its own tree).  Returns KVR_DEV_* bits.
-__device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P, double chat, int32_t hb, int32_t hf,
-                                                 int32_t L, int64_t t, int32_t olen) {
+// LBGR score of one worker (Eq. LBGR-score with the features of Sec. 4.2
+// and the per-1k-token scaling of App. A).  *chat = estimated service time.
+__device__ double lbgr_score(const Consts& C, const RouteView& w, int32_t h, int32_t L, double* chat) {
+  double x1 = (double)h * 0.001;
+  double x2 = (double)(L - h) * 0.001;
+  double x3 = w.P;
+  double x4 = 1.0;
+  double ch = C.alpha_cached * x1 + C.alpha_miss * x2;
+  double res = w.theta[0] * x1;
+  res = res + w.theta[1] * x2;
+  res = res + w.theta[2] * x3;
+  res = res + w.theta[3] * x4;
+  *chat = ch;
+  return (ch + w.P) + res;
+}
+
+// Commit a query on its routed worker, whose header fields v holds: add the
+// estimated service time to the load estimate (Algorithm 2), advance the
+// observed-latency queue and queue the completion record.  hb = the worker's
+// true hit (observed latency, hit counter), hf = the hit the router scored
+// with (the completion's features; the same unless the router keeps its own
+// tree).  Returns KVR_DEV_* bits.
+__device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P, const RouteView& v, double chat,
+                                                 int32_t hb, int32_t hf, int32_t L, int64_t t, int32_t olen) {
   WorkerHdr* w = P.hdr;
-  const double base = chat + w->P;
-  const double x3 = w->P;
-  w->P = w->P + chat;
+  const double base = chat + v.P;
+  const double x3 = v.P;
+  w->P = v.P + chat;
   const int64_t cost = C.true_cached_us * hb + C.true_miss_us * (int64_t)(L - hb) + C.true_out_us * (int64_t)olen;
-  const int64_t e_us = w->Wb + cost;
-  w->Wb = w->Wb + cost;
+  const int64_t e_us = v.Wb + cost;
+  w->Wb = v.Wb + cost;
   uint32_t err = 0;
-  if (w->pend_count >= P.PC) {
+  if (v.pend_count >= P.PC) {
     err |= KVR_DEV_PENDING_FULL;
   } else {
-    uint32_t slot = w->pend_head + w->pend_count;
+    uint32_t slot = v.pend_head + v.pend_count;
     if (slot >= P.PC) slot -= P.PC;
     PendRec pr;
     pr.t_route = t;
@@ -2193,14 +2220,15 @@ __device__ __forceinline__ uint32_t commit_route(const Consts& C, const Ptrs& P,
     pr.h = hf;
     pr.L = L;
     P.pend[slot] = pr;
-    w->pend_count += 1;
-    if (w->pend_count > w->pending_max) w->pending_max = w->pend_count;
+    const uint32_t cnt = v.pend_count + 1u;
+    w->pend_count = cnt;
+    if (cnt > v.pending_max) w->pending_max = cnt;
   }
-  w->routed += 1;
-  w->prompt_tokens += (uint64_t)L;
-  w->hit_tokens += (uint64_t)hb;
-  w->lat_sum_us += (uint64_t)e_us;
-  if ((uint64_t)e_us > w->lat_max_us) w->lat_max_us = (uint64_t)e_us;
+  w->routed = v.routed + 1u;
+  w->prompt_tokens = v.prompt_tokens + (uint64_t)L;
+  w->hit_tokens = v.hit_tokens + (uint64_t)hb;
+  w->lat_sum_us = v.lat_sum_us + (uint64_t)e_us;
+  if ((uint64_t)e_us > v.lat_max_us) w->lat_max_us = (uint64_t)e_us;
   return err;
 }
 

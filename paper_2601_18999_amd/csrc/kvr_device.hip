@@ -126,7 +126,8 @@ __device__ __forceinline__ uint32_t wave_argmin_u32(uint32_t v, uint32_t W) {
 // The routed worker of query k (global index j0 + k): the LBGR argmin, or
 // one of the baseline routers of Sec. 5.  Wave-uniform; one lane per worker.
 __device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, uint32_t k, uint32_t W, double eh,
-                                                 const int32_t* hrow, int32_t Lq, const double* eh_sh) {
+                                                 const int32_t* hrow, int32_t Lq, const double* eh_sh,
+                                                 const RouteView& v) {
   const uint64_t jg = a.j0 + k;
   if (a.C.router == KVR_ROUTE_RANDOM)
     return (uint32_t)__umul64hi(philox_word0(jg, 0ull, 0ull, 1ull, a.C.seed, r), (uint64_t)W);
@@ -134,9 +135,8 @@ __device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, 
   if (a.C.router == KVR_ROUTE_CACHE_AWARE) {
     uint32_t load = 0, size = 0, h = 0;
     if ((uint32_t)lane_id() < W) {
-      const WorkerHdr* w = worker_ptrs(a.ws, a.L, r, (uint32_t)lane_id()).hdr;
-      load = w->pend_count;
-      size = w->size;
+      load = v.pend_count;
+      size = v.size;
       h = (uint32_t)hrow[lane_id()];
     }
     const uint32_t lo = wave_argmin_u32(load, W);
@@ -276,7 +276,6 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ int32_t h_sh[2][kMaxWorkers];  // h of the current and of the next query (the caches)
   __shared__ int32_t g_sh[2][kMaxWorkers];  // the same on the router's trees (approximate router)
   __shared__ double eh_sh[kMaxWorkers];
-  __shared__ double ch_sh[kMaxWorkers];
   __shared__ int32_t ell_sh[2];  // LCP(q_k, q_k+1) in slot k & 1
   __shared__ int32_t best_sh;
   __shared__ int32_t hins_sh;  // cached length of the inserted path (>= h of the prompt)
@@ -349,15 +348,15 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     // ---- phase A.  Wave 0: scores, argmin, commit.  Helpers: stage the
     // next query.
     if (wave == 0) {
-      double eh = __builtin_huge_val();
+      double eh = __builtin_huge_val(), ch = 0.0;
+      RouteView v{};
       if ((uint32_t)lane < W) {
-        double ch;
-        eh = lbgr_score(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr, est[cur][lane], Lq, &ch);
-        ch_sh[lane] = ch;
+        v = load_view(worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr);
+        eh = lbgr_score(a.C, v, est[cur][lane], Lq, &ch);
         eh_sh[lane] = eh;
       }
       __builtin_amdgcn_wave_barrier();
-      const uint32_t best = route_choice(a, r, k, W, eh, est[cur], Lq, eh_sh);
+      const uint32_t best = route_choice(a, r, k, W, eh, est[cur], Lq, eh_sh, v);
       Ptrs P = worker_ptrs(a.ws, a.L, r, best);
       const int32_t hb = h_sh[cur][best];  // the worker's true hit
       // a cached prompt may continue into a cached response: the insertion
@@ -365,18 +364,21 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       // prompt's recorded match
       int32_t hins = hb;
       if (resp && hb == Lq && Lp > Lq) hins = match_incremental(P, P.hdr->arena_sel, qs, Lp, Lq, Lq, paths.of(best));
+      // the routed worker's lane commits from the header fields it holds
+      uint32_t cerr = 0;
+      if ((uint32_t)lane == best) cerr = commit_route(a.C, P, v, ch, hb, est[cur][best], Lq, t, olen);
+      const uint32_t err = (uint32_t)__builtin_amdgcn_readlane((int)cerr, (int)best);
+      const uint32_t size = (uint32_t)__builtin_amdgcn_readlane((int)v.size, (int)best);
       if (lane == 0) {
         best_sh = (int32_t)best;
         hins_sh = hins;
         wready_sh = 0;
         next_sh = 0;
         rank_ready_sh = 0;
-        const uint32_t err = commit_route(a.C, P, ch_sh[best], hb, est[cur][best], Lq, t, olen);
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
         if (a.hits) a.hits[orow] = hb;
         // draws this insertion will take: one per token loaded into a full cache
-        const uint32_t size = P.hdr->size;
         const uint32_t nload = (uint32_t)(Lp - hins);
         const uint32_t nfree = a.L.B - size;
         nev_sh = err ? 0u : (nload > nfree ? nload - nfree : 0u);

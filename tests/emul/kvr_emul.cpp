@@ -108,8 +108,11 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
       const int32_t Ln = has_next ? (int32_t)(offsets[j + 2] - offsets[j + 1]) : 0;
       const int32_t Lnq = has_next && resp ? Ln - query_out_len(out_len, j + 1) : Ln;
       double eh[kMaxWorkers], ch[kMaxWorkers];
-      for (uint32_t i = 0; i < W; ++i)
-        eh[i] = lbgr_score(C, worker_ptrs(ws, L, r, i).hdr, est[cur][i], Lq, &ch[i]);
+      RouteView view[kMaxWorkers];
+      for (uint32_t i = 0; i < W; ++i) {
+        view[i] = load_view(worker_ptrs(ws, L, r, i).hdr);
+        eh[i] = lbgr_score(C, view[i], est[cur][i], Lq, &ch[i]);
+      }
       uint32_t best = 0;
       for (uint32_t i = 1; i < W; ++i)
         if (eh[i] < eh[best]) best = i;
@@ -137,7 +140,7 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
           best = small;
       }
       Ptrs P = worker_ptrs(ws, L, r, best);
-      uint32_t err = commit_route(C, P, ch[best], h[cur][best], est[cur][best], Lq, t, olen);
+      uint32_t err = commit_route(C, P, view[best], ch[best], h[cur][best], est[cur][best], Lq, t, olen);
       if (route) route[r * n + j] = (int32_t)best;
       if (hits) hits[r * n + j] = h[cur][best];
       if (all_hits)
