@@ -1970,26 +1970,44 @@ fail:
   return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
 }
 
-// First index k < n with e[k] != q[k], or n.  KVR_MATCH_UNROLL wave-wide
-// loads are in flight per iteration (64 tokens each on a 64-lane wave).
+// First index k < n with e[k] != q[k] (e in global memory, q in LDS), or
+// n.  The edge is read in aligned 16-byte blocks of four tokens, one block
+// per lane and KVR_MATCH_UNROLL blocks per lane in flight (up to 2,048
+// tokens per round trip on a 64-lane wave).  The first block may start up
+// to three tokens before e and the last end up to three after e + n, always
+// inside the same aligned 16 bytes; those tokens are not compared.
 #ifndef KVR_MATCH_UNROLL
 #define KVR_MATCH_UNROLL 8
 #endif
 __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n) {
   constexpr int kUnroll = KVR_MATCH_UNROLL;
-  for (int32_t b = 0; b < n; b += kUnroll * KVR_WAVE) {
-    int32_t ev[kUnroll], qv[kUnroll];
+  const uintptr_t ea = reinterpret_cast<uintptr_t>(e);
+  const int32_t lead = (int32_t)((ea & 15u) >> 2);
+  const int4* base = reinterpret_cast<const int4*>(ea - (uintptr_t)lead * 4u);
+  const int32_t nb = (lead + n + 3) >> 2;  // blocks covering e[-lead, n)
+  for (int32_t b = 0; b < nb; b += kUnroll * KVR_WAVE) {
+    int4 v[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      ev[u] = k < n ? e[k] : 0;
-      qv[u] = k < n ? q[k] : 0;
+      const int32_t blk = b + u * KVR_WAVE + lane_id();
+      v[u].x = v[u].y = v[u].z = v[u].w = 0;
+      if (blk < nb) v[u] = base[blk];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int32_t k = b + u * KVR_WAVE + lane_id();
-      const uint64_t m = __ballot(k < n && ev[u] != qv[u]);
-      if (m) return b + u * KVR_WAVE + first_lane(m);
+      const int32_t blk = b + u * KVR_WAVE + lane_id();
+      const int32_t x0 = blk * 4 - lead;  // index into e of v[u].x
+      int32_t mm = n;
+      if (blk < nb) {
+        const int32_t t4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+        for (int c = 3; c >= 0; --c) {
+          const int32_t x = x0 + c;
+          if (x >= 0 && x < n && t4[c] != q[x]) mm = x;
+        }
+      }
+      const uint64_t m = __ballot(mm < n);
+      if (m) return __shfl(mm, first_lane(m), KVR_WAVE);
     }
   }
   return n;

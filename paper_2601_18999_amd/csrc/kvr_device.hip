@@ -70,25 +70,41 @@ __device__ __forceinline__ void count_matched(const Ptrs& P, int32_t h, int32_t*
 
 // Stage q_next[0, Ln) (threads t0, t0 + stride, ...) and fold each thread's
 // first position where it differs from q_cur into *ell (LDS minimum), so
-// that after the next barrier *ell = LCP(q_cur, q_next).
+// that after the next barrier *ell = LCP(q_cur, q_next).  The stream is read
+// in aligned 16-byte blocks of four tokens, four blocks per thread in flight;
+// the first and last block may reach up to three tokens outside the query,
+// inside the same aligned 16 bytes, and those are not staged.
 __device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, int32_t Ln, int32_t* qn,
                                            const int32_t* qc, int32_t Lc, uint32_t t0, uint32_t stride,
                                            int32_t* ell) {
-  constexpr int kUnroll = 8;  // loads in flight per thread
+  constexpr int kUnroll = 4;  // blocks in flight per thread
+  const uintptr_t sa = reinterpret_cast<uintptr_t>(tokens + n0);
+  const int32_t lead = (int32_t)((sa & 15u) >> 2);
+  const int4* base = reinterpret_cast<const int4*>(sa - (uintptr_t)lead * 4u);
+  const uint32_t nb = (uint32_t)((lead + Ln + 3) >> 2);
   int32_t m = Lc < Ln ? Lc : Ln;
-  for (uint32_t b = t0; b < (uint32_t)Ln; b += kUnroll * stride) {
-    int32_t v[kUnroll];
+  for (uint32_t b = t0; b < nb; b += kUnroll * stride) {
+    int4 v[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t x = b + (uint32_t)u * stride;
-      v[u] = x < (uint32_t)Ln ? tokens[n0 + x] : 0;
+      const uint32_t blk = b + (uint32_t)u * stride;
+      v[u].x = v[u].y = v[u].z = v[u].w = 0;
+      if (blk < nb) v[u] = base[blk];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t x = b + (uint32_t)u * stride;
-      if (x < (uint32_t)Ln) {
-        qn[x] = v[u];
-        if ((int32_t)x < m && qc[x] != v[u]) m = (int32_t)x;
+      const uint32_t blk = b + (uint32_t)u * stride;
+      if (blk < nb) {
+        const int32_t t4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+        const int32_t x0 = (int32_t)blk * 4 - lead;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int32_t x = x0 + c;
+          if (x >= 0 && x < Ln) {
+            qn[x] = t4[c];
+            if (x < m && qc[x] != t4[c]) m = x;
+          }
+        }
       }
     }
   }

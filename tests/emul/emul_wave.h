@@ -16,6 +16,7 @@
 struct kvr_emul_dim3 { unsigned x, y, z; };
 static const kvr_emul_dim3 threadIdx = {0, 0, 0};
 struct int2 { int x, y; };
+struct alignas(16) int4 { int x, y, z, w; };
 
 inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
 inline int __shfl(int v, int, int) { return v; }
