@@ -71,13 +71,13 @@ __device__ __forceinline__ void count_matched(const Ptrs& P, int32_t h, int32_t*
 // Stage q_next[0, Ln) (threads t0, t0 + stride, ...) and fold each thread's
 // first position where it differs from q_cur into *ell (LDS minimum), so
 // that after the next barrier *ell = LCP(q_cur, q_next).  The stream is read
-// in aligned 16-byte blocks of four tokens, four blocks per thread in flight;
+// in aligned 16-byte blocks of four tokens, eight blocks per thread in flight;
 // the first and last block may reach up to three tokens outside the query,
 // inside the same aligned 16 bytes, and those are not staged.
 __device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, int32_t Ln, int32_t* qn,
                                            const int32_t* qc, int32_t Lc, uint32_t t0, uint32_t stride,
                                            int32_t* ell) {
-  constexpr int kUnroll = 4;  // blocks in flight per thread
+  constexpr int kUnroll = 8;  // blocks in flight per thread
   const uintptr_t sa = reinterpret_cast<uintptr_t>(tokens + n0);
   const int32_t lead = (int32_t)((sa & 15u) >> 2);
   const int4* base = reinterpret_cast<const int4*>(sa - (uintptr_t)lead * 4u);
