@@ -424,3 +424,53 @@ def test_gsp_paper_shape_full_stream(cfg, evict):
     res, stats = gpu_run(s, 4, p["W"], p["B"], batch=1024, evict=ev)
     assert_parity(s, res, stats, p["W"], p["B"], [0, 3], evict=evict)
     assert sum(w["evictions"] for w in stats[0]) > 0
+
+
+# ---------------------------------------------------------------- extreme shapes
+
+def test_largest_worker_count_and_query_length():
+    """W = 64 workers (the most a replica holds) and queries up to the largest
+    max_query_tokens (16,384): the query buffers leave little LDS, so the
+    candidate list stays in global memory and most draw words are computed
+    by the inserting wave itself."""
+    rng = np.random.default_rng(5)
+    groups = [[int(x) for x in rng.integers(0, 1000, size=int(rng.integers(2000, 12000)))] for _ in range(6)]
+    paths, order = [], []
+    for j in range(40):
+        g = groups[int(rng.integers(0, 6))]
+        paths.append(g + [int(x) for x in rng.integers(0, 1000, size=int(rng.integers(1, 16384 - len(g) + 1)))])
+        order.append(j)
+    s = generate({"kind": "paths", "paths": paths, "order": order})
+    assert s.max_len <= 16384
+    W, B = 64, 40000
+    note(f"W={W} B={B} max_len={s.max_len} n={s.n}")
+    res, stats = gpu_run(s, 2, W, B, max_len=16384)
+    assert_parity(s, res, stats, W, B, range(2))
+    s2 = generate({"kind": "paths", "paths": paths[:20], "order": list(range(20)) * 3})
+    res, stats = gpu_run(s2, 2, 3, 16384, max_len=16384)
+    assert_parity(s2, res, stats, 3, 16384, range(2))
+    assert sum(w["evictions"] for w in stats[0]) > 16384
+
+
+def test_single_token_queries_in_a_one_token_cache():
+    """B = 1: every miss evicts the only cached token (the degenerate case of
+    Algorithm 1: the marking set resets at every new token)."""
+    rng = np.random.default_rng(9)
+    paths = [[int(rng.integers(0, 3))] for _ in range(200)]
+    s = generate({"kind": "paths", "paths": paths, "order": list(range(200))})
+    for evict in ("rlt", "lru"):
+        res, stats = gpu_run(s, 3, 2, 1, evict={"rlt": K.KVR_EVICT_RLT, "lru": K.KVR_EVICT_LRU}[evict])
+        assert_parity(s, res, stats, 2, 1, range(3), evict=evict)
+        assert all(w["resident"] <= 1 for rr in stats for w in rr)
+
+
+def test_one_query_repeated():
+    """The same query over and over: everything after the first is a full
+    hit on the worker it went to, and nothing is ever evicted."""
+    q = list(range(100, 400))
+    s = generate({"kind": "paths", "paths": [q], "order": [0] * 300})
+    res, stats = gpu_run(s, 2, 4, 1000, batch=7)
+    assert_parity(s, res, stats, 4, 1000, range(2))
+    for r in range(2):
+        assert (res["all_hits"][r][1:].max(axis=1) == len(q)).all()
+        assert sum(w["evictions"] for w in stats[r]) == 0
