@@ -983,7 +983,9 @@ __device__ __forceinline__ bool stage_in(const Ptrs& P, St& s, const UStage& u) 
   return true;
 }
 
-__device__ __forceinline__ void stage_out(const Ptrs& P, const St& s, const UStage& u) {
+// Write the staged list back.  fence = false when the caller's own fence
+// follows before anything reads U or the node lengths again.
+__device__ __forceinline__ void stage_out(const Ptrs& P, const St& s, const UStage& u, bool fence = true) {
   for (uint32_t b = 0; b < s.nU; b += KVR_WAVE) {
     const uint32_t k = b + (uint32_t)lane_id();
     if (k < s.nU) {
@@ -992,7 +994,7 @@ __device__ __forceinline__ void stage_out(const Ptrs& P, const St& s, const USta
       P.nodes[n].len = u.len[k];
     }
   }
-  wave_mem_sync();
+  if (fence) wave_mem_sync();
 }
 
 // remove entry pos of the staged list (n entries); LDS only, so the wave's
@@ -1494,7 +1496,9 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         k += done;
       }
     }
-    if (staged) stage_out(P, s, ustage);
+    // no fence: the insertion's last fence orders these stores before any
+    // later read
+    if (staged) stage_out(P, s, ustage, false);
     if (reset_at >= 0 && !applied) {
       s.phase += 1;
       s.U_valid = 0;
