@@ -3,22 +3,24 @@
 //
 // One workgroup owns one replica for a whole batch and walks the batch's
 // queries in order (the simulation is sequential within a replica, Sec. 3.1:
-// the state after query j-1 decides query j).  Per query:
-//   * all waves: stage the query tokens in LDS;
-//   * wave 0: completions and load decay for every worker, one lane per
-//     worker (Algorithm 2, update and decay threads; Sec. 4.2);
-//   * every wave takes workers in turn and computes h_ij, the longest
-//     cached prefix of the query, walking the worker's compressed radix tree
-//     and comparing 64 tokens per wave instruction (Sec. 3.2 "Cache
-//     Matching");
-//   * wave 0: the LBGR score of every worker, the argmin (lowest index on
-//     ties) and the commit on the routed worker (Algorithm 2 routing thread,
-//     Eq. LBGR-score, Eq. 2 with the estimate);
-//   * wave 0: RLT insertion into the routed worker's cache (Algorithm 1):
-//     marks along the path, phase resets, a uniform draw over the unmarked
-//     leaf tokens U for every token loaded into a full cache (Eq. 3: no other
-//     cache changes).
-//
+// the state after query j-1 decides query j).  Per query, in two phases
+// separated by workgroup barriers:
+//   * phase A, wave 0: the LBGR score of every worker from its load,
+//     residual model and h_ij, the longest cached prefix of the query (Sec.
+//     3.2 "Cache Matching"); the argmin (lowest index on ties) and the commit
+//     on the routed worker (Algorithm 2 routing thread, Eq. LBGR-score, Eq. 2
+//     with the estimate), or a baseline router of Sec. 5.  The other waves
+//     stage the next query in LDS.
+//   * phase B, wave 0: the insertion into the routed worker's cache with RLT
+//     (Algorithm 1: marks along the path, phase resets, a uniform draw over
+//     the unmarked leaf tokens U for every token loaded into a full cache;
+//     Eq. 3: no other cache changes) or L-LRU, then that worker's h for the
+//     next query.  The other waves: the draw words of the insertion and the
+//     new leaf's rank; completions and load decay at the next arrival, one
+//     lane per worker (Algorithm 2, update and decay threads; Sec. 4.2); the
+//     next query's h on every other worker, walking each compressed radix
+//     tree from the point where the previous match on it can be resumed.
+
 // The cache of a worker is a compressed radix tree: a node holds an edge of
 // `len` tokens; its leaf token (when it has no children) is the last one.
 // U is kept as an ordered list of candidate leaf nodes in lexicographic
