@@ -748,3 +748,51 @@ def test_router_tree_underestimates_with_a_small_budget():
         over += int(r["all_hits"][j, i] < r["hits"][j])
         seen[i].append(qs[j])
     assert over > 0
+
+
+# ---------------------------------------------------------------------------
+# Theorem 3's phase bound: in a phase with c clean tokens RLT misses at most
+# c + c(H_n - H_c) tokens in expectation, n = min(B - L + c, B)
+
+def _harmonic(k):
+    return sum(Fraction(1, i) for i in range(1, k + 1))
+
+
+@pytest.mark.parametrize("c", [1, 4, 8])
+def test_rlt_phase_miss_bound_on_the_proofs_adversary(c):
+    """Paths share an (L-1)-token prefix and differ in the last token, so a
+    phase of the marking algorithm covers B-L+1 distinct tails.  Every phase
+    first asks for c tails never seen (clean), then for B-L+1-c tails of the
+    previous phase (stale): the order the proof calls the worst.  The mean
+    misses per phase over many random keys stay within the bound, and at
+    least the c clean misses happen."""
+    B, L = 20, 4
+    k = B - L + 1  # tails per phase
+    prefix = [500, 501, 502]
+    nxt = 0
+    phases = [list(range(k))]
+    nxt = k
+    for p in range(12):
+        clean = list(range(nxt, nxt + c))
+        nxt += c
+        phases.append(clean + phases[-1][: k - c])
+    tails = [t for ph in phases for t in ph]
+    paths = {t: prefix + [10000 + t] for t in set(tails)}
+    ids = sorted(paths)
+    s = _paths_stream([paths[t] for t in ids], [ids.index(t) for t in tails])
+    reps = 600
+    per_phase = np.zeros((reps, len(phases) - 1))
+    for rep in range(reps):
+        r = O.run(s, 1, B, replica=rep, check=1)
+        assert r["rc"] == 0
+        miss = L - r["hits"]
+        for p in range(1, len(phases)):
+            per_phase[rep, p - 1] = miss[p * k:(p + 1) * k].sum()
+    n = min(B - L + c, B)
+    bound = float(c + c * (_harmonic(n) - _harmonic(c)))
+    m = per_phase[:, 1:].mean()  # phase 1 follows the fill, start from the next
+    sd = per_phase[:, 1:].mean(axis=1).std(ddof=1) / math.sqrt(reps)
+    assert per_phase.min() >= c
+    assert m <= bound + 4 * sd, (m, bound)
+    # the stale requests do miss sometimes: the bound is not vacuous here
+    assert m > c
