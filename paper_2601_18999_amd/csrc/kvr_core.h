@@ -2023,28 +2023,27 @@ __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n)
 __device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L, int32_t x, int32_t off,
                               int32_t d, const PathRef& pr, int32_t& pc) {
   const int32_t* ar = arena_of(P, sel);
-  if (x != 0 && d < L) {
-    const NodeRec nx = P.nodes[x];
-    if (off < nx.len) {  // the rest of this edge first
-      const int32_t rest = nx.len - off;
-      const int32_t n = rest < L - d ? rest : L - d;
-      const int32_t k = first_mismatch(ar + nx.off + off, qs + d, n);
-      d += k;
-      if (k < rest) return d;
-    }
+  if (d >= L) return d;
+  // the record of the current node is loaded once and carried down
+  NodeRec nx = P.nodes[x];
+  if (x != 0 && off < nx.len) {  // the rest of this edge first
+    const int32_t rest = nx.len - off;
+    const int32_t n = rest < L - d ? rest : L - d;
+    const int32_t k = first_mismatch(ar + nx.off + off, qs + d, n);
+    d += k;
+    if (k < rest) return d;
   }
   while (d < L) {
-    NodeRec nx = P.nodes[x];
-    int32_t c = child_find(ar, nx, qs[d]);
+    const int32_t c = child_find(ar, nx, qs[d]);
     if (c < 0) break;
-    NodeRec nc = P.nodes[c];
+    const NodeRec nc = P.nodes[c];
     if (nc.len <= 0) break;  // never true for a consistent tree
     path_add(pr, pc, c, d, d + nc.len);
-    int32_t n = nc.len < L - d ? nc.len : L - d;
-    int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + d + 1, n - 1);
+    const int32_t n = nc.len < L - d ? nc.len : L - d;
+    const int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + d + 1, n - 1);
     d += k;
     if (k < nc.len) break;
-    x = c;
+    nx = nc;
   }
   return d;
 }
