@@ -210,9 +210,13 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   size_t ucap = room / 16u;
   if (ucap > 8192) ucap = 8192;
   if (ucap < 64) ucap = 0;
+  // The dynamic-LDS limit is an attribute of the kernel functions, shared
+  // by every context in the process: raise it to all the device allows, so
+  // that a context with a smaller query buffer never lowers it under one
+  // with a larger buffer.
   const size_t lds = kvr::step_lds_bytes(L.maxL, L.W, (uint32_t)ucap, (uint32_t)rcap, path_sets);
   if (lds > 65536) {
-    e = kvr::set_step_lds_limit(lds);
+    e = kvr::set_step_lds_limit((size_t)lds_max - static_lds);
     if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
   }
   kvr_ctx* c = new (std::nothrow) kvr_ctx;

@@ -474,3 +474,43 @@ def test_one_query_repeated():
     for r in range(2):
         assert (res["all_hits"][r][1:].max(axis=1) == len(q)).all()
         assert sum(w["evictions"] for w in stats[r]) == 0
+
+
+def test_two_live_contexts_with_different_lds_needs():
+    """Two contexts alive at once, the second created with a much shorter
+    query buffer (so a smaller LDS footprint) than the first: batches of the
+    two interleave, and each context still matches the oracle."""
+    rng = np.random.default_rng(13)
+    base = [int(x) for x in rng.integers(0, 500, size=6000)]
+    long_paths = [base[:int(rng.integers(100, 6000))] + [int(x) for x in rng.integers(0, 500, size=int(
+        rng.integers(1, 6000)))] for _ in range(30)]
+    s1 = generate({"kind": "paths", "paths": long_paths, "order": [int(x) for x in rng.integers(0, 30, size=60)]})
+    s2 = generate({"kind": "paths", "paths": [[int(x) for x in rng.integers(0, 5, size=int(rng.integers(1, 40)))]
+                                              for _ in range(50)],
+                   "order": [int(x) for x in rng.integers(0, 50, size=300)]})
+    W1, B1, W2, B2 = 4, 20000, 3, 120
+    note(f"long: max_len={s1.max_len} n={s1.n}; short: max_len={s2.max_len} n={s2.n}")
+    a = K.Simulator(2, W1, B1, s1.max_len)
+    b = K.Simulator(2, W2, B2, s2.max_len)
+    try:
+        da, db = a.upload(s1), b.upload(s2)
+        outs_a, outs_b = [], []
+        for k in range(6):
+            outs_a.append(a.route(da, 10 * k, 10, all_hits=True))
+            outs_b.append(b.route(db, 50 * k, 50, all_hits=True))
+        res = {}
+        for sim, outs, key in ((a, outs_a, "a"), (b, outs_b, "b")):
+            sim.stream.synchronize()
+            st, bits = sim.check()
+            res[key] = {"route": np.concatenate([o["route"].cpu().numpy() for o in outs], 1),
+                        "hits": np.concatenate([o["hits"].cpu().numpy() for o in outs], 1),
+                        "all_hits": np.concatenate([o["all_hits"].cpu().numpy() for o in outs], 1),
+                        "status": st, "bits": bits}
+            res[key + "_stats"] = sim.stats(check=False)
+    finally:
+        a.close()
+        b.close()
+    assert_parity(s1, res["a"], res["a_stats"], W1, B1, range(2))
+    assert_parity(s2, res["b"], res["b_stats"], W2, B2, range(2))
+    assert sum(w["evictions"] for w in res["a_stats"][0]) > 0
+    assert sum(w["evictions"] for w in res["b_stats"][0]) > 0
