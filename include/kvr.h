@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 5u
+#define KVR_ABI_VERSION 6u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -199,9 +199,10 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens,
                            int32_t* d_all_hits);
 
 /* Synchronise the stream and copy the state of every (replica, worker) into
- * h_out[r*W + i] (R*W entries, host memory).  Returns the device status as
- * kvr_check does. */
-kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out);
+ * h_out[r*W + i], host memory with room for h_count entries: KVR_EINVAL,
+ * with nothing written, when h_count < R*W.  Returns the device status as
+ * kvr_check does (the entries are written also when it is an error). */
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out, size_t h_count);
 
 /* Synchronise the stream and return the sticky device status as a
  * kvr_status; *h_bits (optional) receives the raw KVR_DEV_* bits. */

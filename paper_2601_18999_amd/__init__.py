@@ -21,7 +21,7 @@ STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVIC
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 5
+KVR_ABI_VERSION = 6
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
@@ -112,7 +112,7 @@ def load_library() -> ctypes.CDLL:
     lib.kvr_route_batch.restype = ctypes.c_int
     lib.kvr_route_batch.argtypes = [vp, u32, vp, vp, vp, vp, vp, vp, vp]
     lib.kvr_stats.restype = ctypes.c_int
-    lib.kvr_stats.argtypes = [vp, ctypes.POINTER(KvrWorkerStats)]
+    lib.kvr_stats.argtypes = [vp, ctypes.POINTER(KvrWorkerStats), ctypes.c_size_t]
     lib.kvr_check.restype = ctypes.c_int
     lib.kvr_check.argtypes = [vp, ctypes.POINTER(u32)]
     lib.kvr_queries_done.restype = u64
@@ -186,7 +186,7 @@ def _stats_dicts(arr, n: int) -> List[Dict]:
 
 def kvr_stats(ctx: int, R: int, W: int, check: bool = True) -> List[List[Dict]]:
     arr = (KvrWorkerStats * (R * W))()
-    st = load_library().kvr_stats(ctypes.c_void_p(ctx), arr)
+    st = load_library().kvr_stats(ctypes.c_void_p(ctx), arr, R * W)
     if check:
         _check(st, "kvr_stats")
     flat = _stats_dicts(arr, R * W)

@@ -310,9 +310,12 @@ kvr_status kvr_check(kvr_ctx* ctx, uint32_t* h_bits) {
   return KVR_OK;
 }
 
-kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out) {
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out, size_t h_count) {
   if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
   if (!h_out) return fail(KVR_EINVAL, "h_out is NULL");
+  if (h_count < (size_t)ctx->L.R * ctx->L.W)
+    return fail(KVR_EINVAL, "h_out holds " + std::to_string(h_count) + " entries, the context has " +
+                                std::to_string((size_t)ctx->L.R * ctx->L.W));
   uint32_t bits = 0;
   kvr_status st = kvr_check(ctx, &bits);
   hipError_t e = kvr::launch_stats(ctx->ws, ctx->L, ctx->stream);

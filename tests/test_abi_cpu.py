@@ -75,7 +75,7 @@ def test_workspace_size_grows_with_every_dimension():
 def test_null_context_and_arguments():
     lib = K.load_library()
     assert lib.kvr_route_batch(None, 1, None, None, None, None, None, None, None) == K.KVR_EINVAL
-    assert lib.kvr_stats(None, None) == K.KVR_EINVAL
+    assert lib.kvr_stats(None, None, 0) == K.KVR_EINVAL
     assert lib.kvr_check(None, None) == K.KVR_EINVAL
     assert lib.kvr_queries_done(None) == 0
     lib.kvr_destroy(None)
@@ -89,3 +89,30 @@ def test_init_without_device_or_workspace():
     with pytest.raises(K.KvrError) as ei:
         K.kvr_init_replicas(c, 256, 16)  # too small
     assert ei.value.status == K.KVR_ENOMEM
+
+
+def test_binding_structs_match_the_header(tmp_path):
+    """Every field of kvr_config and kvr_worker_stats sits at the same offset
+    in the ctypes binding as in the C header (compiled here with gcc)."""
+    import ctypes
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "kvr.h"', "int main(void) {"]
+    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats)):
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats)):
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)

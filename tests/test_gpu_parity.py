@@ -6,6 +6,7 @@ residual model to 1e-9 relative.  Sizes are ones the oracle finishes in
 seconds but that still cover many 64-token tiles, ragged tails, phase
 resets, forced resets and collector runs.
 """
+import ctypes
 import math
 
 import numpy as np
@@ -174,6 +175,10 @@ def test_invalid_batches_are_rejected_before_any_state_change():
         sim.route(dbad, 0, bad.n)
         st, bits = sim.check()
         assert st == K.KVR_EINVAL, (kind, st, bits)
+        # a stats buffer one entry short is refused before anything is written
+        short = (K.KvrWorkerStats * (sim.R * sim.W))()
+        assert K.load_library().kvr_stats(ctypes.c_void_p(sim.ctx), short, sim.R * sim.W - 1) == K.KVR_EINVAL
+        assert all(short[i].routed == 0 for i in range(sim.R * sim.W))
         after = sim.stats(check=False)
         assert before == after, kind
         with pytest.raises(K.KvrError) as ei:
