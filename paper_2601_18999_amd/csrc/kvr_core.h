@@ -822,10 +822,13 @@ struct InsertArgs {
   uint32_t B;
   uint32_t rn;        // the high halves of draw words 0..rn-1 are precomputed in rw
   const uint32_t* rw;
-  // when non-null: the words are being written by other waves, and are all
-  // there once *ready reaches ready_need (LDS counter, workgroup scope)
-  const uint32_t* ready;
-  uint32_t ready_need;
+  // when non-null: the words are being written by nprog other waves in
+  // rounds of `round` words (words [k*round, (k+1)*round) in round k), and
+  // prog[w] (LDS, workgroup scope) counts the rounds drawing wave w has
+  // completed
+  const uint32_t* prog;
+  uint32_t nprog;
+  uint32_t round;
   // when non-null: another wave computes the new leaf's rank in the leaf
   // list from the recorded match path (new_leaf_rank on the tree before the
   // insertion) into *rank and then sets *rank_ready to 1, or to 2 when it
@@ -843,6 +846,31 @@ __device__ __forceinline__ int32_t await_rank(const InsertArgs& ia) {
     __builtin_amdgcn_s_sleep(2);
   }
   return rd == 1u ? *ia.rank : -1;
+}
+
+
+// An insertion whose draw words take at most this many rounds waits for all
+// of them at once (measured faster than starting on the first rounds).
+constexpr uint32_t kAwaitAllRounds = 4;
+
+// Wait (bounded) until draw words [0, need) of rw are written (need <= rn).
+// Returns the count of words known to be there, at least need, or 0 if the
+// wait ran out (the caller then computes every word itself).
+__device__ __forceinline__ uint32_t await_words(const InsertArgs& ia, uint32_t need) {
+  if (ia.rn <= kAwaitAllRounds * ia.round) need = ia.rn;
+  const uint32_t want = (need + ia.round - 1u) / ia.round;  // rounds
+  uint32_t spins = 0;
+  for (;;) {
+    bool late = false;
+    if ((uint32_t)lane_id() < ia.nprog)
+      late = __hip_atomic_load(ia.prog + lane_id(), __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < want;
+    if (!__ballot(late)) {
+      const uint64_t have = (uint64_t)want * ia.round;
+      return have < ia.rn ? (uint32_t)have : ia.rn;
+    }
+    if (++spins > (1u << 22)) return 0u;
+    __builtin_amdgcn_s_sleep(2);
+  }
 }
 
 // Word 0 of Philox4x64-10 for draw d of this insertion: key (seed, replica),
@@ -1044,7 +1072,7 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
 #pragma unroll
     for (int r = 0; r < kDraws; ++r) {
       uint64_t d = dctr + (uint64_t)(r * KVR_WAVE + lane);
-      if (d >= ia.rn) d = ia.rn - 1u;
+      if (d >= dctr + cnt) d = dctr + cnt - 1u;
       wv[r] = ia.rw[d];
     }
 #pragma unroll
@@ -1419,17 +1447,10 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     uint32_t k = 0;
     bool staged = false;
     InsertArgs iq = ia;
-    if (nev > 0 && iq.ready) {
-      // bounded wait; past it the words are computed here instead
-      uint32_t spins = 0;
-      while (__hip_atomic_load(iq.ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < iq.ready_need) {
-        if (++spins > (1u << 22)) {
-          iq.rn = 0;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(2);
-      }
-    }
+    // draw words [0, have) are known to be written; before a block reads
+    // words past that, wait for the drawing waves' rounds to cover them
+    // (bounded: past it the words are computed here instead)
+    uint32_t have = iq.prog ? 0u : iq.rn;
     while (k < nev) {
       const int32_t p = h + (int32_t)nfree + (int32_t)k;
       if (reset_at >= 0 && !applied && p >= reset_at) {
@@ -1476,6 +1497,11 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         while (ku < limu) {
           constexpr uint32_t kSpan = (uint32_t)kEvictDraws * KVR_WAVE;
           const uint32_t cnt = limu - ku < kSpan ? limu - ku : kSpan;
+          if (du + cnt > have && have < iq.rn) {
+            const uint32_t need = du + cnt < iq.rn ? du + cnt : iq.rn;
+            have = await_words(iq, need);
+            if (have == 0u) iq.rn = 0;
+          }
           uint32_t done = 0;
           bool changed = false;
           ok = evict_block_staged<kEvictDraws>(P, s, iq, ustage, (uint64_t)du, cnt, done, changed);
@@ -1490,6 +1516,11 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
         if (!ok) goto fail;
       } else {
         const uint32_t cnt = lim - k < (uint32_t)KVR_WAVE ? lim - k : (uint32_t)KVR_WAVE;
+        if (dctr + cnt > have && have < iq.rn) {
+          const uint32_t need = (uint32_t)dctr + cnt < iq.rn ? (uint32_t)dctr + cnt : iq.rn;
+          have = await_words(iq, need);
+          if (have == 0u) iq.rn = 0;
+        }
         uint32_t done = 0;
         if (!evict_block(P, s, iq, dctr, cnt, done)) goto fail;
         dctr += done;

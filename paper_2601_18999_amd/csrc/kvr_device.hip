@@ -243,8 +243,9 @@ __device__ __forceinline__ uint32_t router_admit(const StepArgs& a, uint32_t r, 
   ia.B = a.L.RB;
   ia.rn = 0;
   ia.rw = nullptr;
-  ia.ready = nullptr;
-  ia.ready_need = 0;
+  ia.prog = nullptr;
+  ia.nprog = 0;
+  ia.round = 1;
   ia.rank = nullptr;
   ia.rank_ready = nullptr;
   const uint32_t err = lru_insert(Pr, ia, qs, Lq, hr, rpaths.of(best), dbg);
@@ -299,7 +300,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   __shared__ int32_t hins_sh;  // cached length of the inserted path (>= h of the prompt)
   __shared__ uint32_t abort_sh;
   __shared__ uint32_t nev_sh;
-  __shared__ uint32_t wready_sh;  // helper waves done with the draw words
+  __shared__ uint32_t prog_sh[16];  // rounds of draw words each drawing wave has written
   __shared__ uint32_t next_sh;    // next item for the helpers' matches
   __shared__ int32_t rank_sh;     // the new leaf's rank, from the last helper wave
   __shared__ uint32_t rank_ready_sh;
@@ -387,10 +388,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       if ((uint32_t)lane == best) cerr = commit_route(a.C, P, v, ch, hb, est[cur][best], Lq, t, olen);
       const uint32_t err = (uint32_t)__builtin_amdgcn_readlane((int)cerr, (int)best);
       const uint32_t size = (uint32_t)__builtin_amdgcn_readlane((int)v.size, (int)best);
+      if ((uint32_t)lane < 16u) prog_sh[lane] = 0u;
       if (lane == 0) {
         best_sh = (int32_t)best;
         hins_sh = hins;
-        wready_sh = 0;
         next_sh = 0;
         rank_ready_sh = 0;
         const uint64_t orow = (uint64_t)r * a.n + k;
@@ -447,8 +448,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.B = a.L.B;
       ia.rn = rn;
       ia.rw = rw;
-      ia.ready = nh && rn ? &wready_sh : nullptr;
-      ia.ready_need = ranker ? nh - 1u : nh;
+      ia.prog = nh && rn ? prog_sh : nullptr;
+      ia.nprog = ranker ? nh - 1u : nh;
+      ia.round = 2u * (blockDim.x - (ranker ? 2u : 1u) * KVR_WAVE);
       ia.rank = ranker ? &rank_sh : nullptr;
       ia.rank_ready = &rank_ready_sh;
       int64_t dbg[4] = {0, 0, 0, 0};
@@ -488,12 +490,22 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         // the last helper ranks the insertion's new leaf
         rank_for_insertion(worker_ptrs(a.ws, a.L, r, best), paths.of(best), qs, hins, &rank_sh, &rank_ready_sh);
       } else {
-        // the others compute the draw words
+        // the others compute the draw words, a round of 2*nd words at a
+        // time (two independent words per lane), and publish each round
+        // they complete
         const uint32_t nd = blockDim.x - (ranker ? 2u : 1u) * KVR_WAVE;
-        for (uint32_t d = threadIdx.x - KVR_WAVE; d < rn; d += nd)
-          rw[d] = (uint32_t)(philox_word0(jg, best, d, 0ull, a.C.seed, r) >> 32);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        if (lane == 0) __hip_atomic_fetch_add(&wready_sh, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        uint32_t rounds = 0;
+        for (uint32_t base = 0; base < rn; base += 2u * nd) {
+          const uint32_t d0 = base + threadIdx.x - KVR_WAVE, d1 = d0 + nd;
+          const uint64_t w0 = philox_word0(jg, best, d0, 0ull, a.C.seed, r);
+          const uint64_t w1 = philox_word0(jg, best, d1, 0ull, a.C.seed, r);
+          if (d0 < rn) rw[d0] = (uint32_t)(w0 >> 32);
+          if (d1 < rn) rw[d1] = (uint32_t)(w1 >> 32);
+          ++rounds;
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          if (lane == 0)
+            __hip_atomic_store(&prog_sh[wave - 1u], rounds, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
       }
       if (wave == 1) {
         if (has_next) {

@@ -174,8 +174,9 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.B = L.B;
         ia.rn = nev;
         ia.rw = rwbuf.data();
-        ia.ready = nullptr;
-        ia.ready_need = 0;
+        ia.prog = nullptr;
+        ia.nprog = 0;
+        ia.round = 1;
         // the new leaf's rank as the device's last helper wave computes it,
         // from the recorded match path on the tree before the insertion
         int32_t rank = -1;
@@ -208,8 +209,9 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
         ia.B = L.RB;
         ia.rn = 0;
         ia.rw = nullptr;
-        ia.ready = nullptr;
-        ia.ready_need = 0;
+        ia.prog = nullptr;
+        ia.nprog = 0;
+        ia.round = 1;
         ia.rank = nullptr;
         ia.rank_ready = nullptr;
         err = lru_insert(Pr, ia, qs, Lq, g[cur][best], rpath_of(best), nullptr);
