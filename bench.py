@@ -66,24 +66,46 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(stream, W, B, budget_s: float, evict: str = "rlt", router: str = "lbgr", responses: int = 0,
-                 beta: int = 1, router_tree: int = 0, router_tree_tokens: int = 0):
-    """The CPU oracle, single-threaded, on replica 0 of the same stream: the
-    first n queries, n grown until one run takes at least budget_s (the cost
-    per query grows as the caches fill, so the last steps grow by 1.4x)."""
+def host_cores() -> int:
+    """Cores for the CPU leg: this process's CPU affinity, at most 16 (one
+    GPU's share of its host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(stream, W, B, budget_s: float, replicas: int, evict: str = "rlt", router: str = "lbgr",
+                 responses: int = 0, beta: int = 1, router_tree: int = 0, router_tree_tokens: int = 0):
+    """The CPU oracle on the host's cores: one single-threaded oracle run per
+    replica, as many replicas at once as there are cores (its C entry point
+    releases the GIL), each over the first n queries of the same stream; n
+    grown until one round takes at least budget_s (the cost per query grows
+    as the caches fill, so the last steps grow by 1.4x)."""
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import oracle as O
+    O.lib()  # built and loaded once, before the threads
+    threads = max(1, min(replicas, host_cores()))
     n = min(1000, stream.n)
-    while True:
-        t0 = time.perf_counter()
-        O.run(stream, W, B, replica=0, n=n, evict=evict, router=router, cache_responses=responses, batch_size=beta,
-              router_tree=router_tree, router_tree_tokens=router_tree_tokens)
-        dt = time.perf_counter() - t0
-        log(f"cpu oracle: {n} queries in {dt:.1f} s")
-        if dt >= budget_s or n >= stream.n:
-            break
-        n = min(stream.n, int(n * (2.0 if dt < budget_s / 3 else 1.4)))
-    return {"value": n / dt, "unit": "queries/s", "cores": 1, "kind": "oracle",
-            "sample": f"replica 0, queries 0..{n} of the same stream, one thread, {dt:.1f} s"}
+
+    def one(r: int) -> None:
+        o = O.run(stream, W, B, replica=r, n=n, evict=evict, router=router, cache_responses=responses,
+                  batch_size=beta, router_tree=router_tree, router_tree_tokens=router_tree_tokens)
+        assert o["rc"] == 0, (r, o["rc"])
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        while True:
+            t0 = time.perf_counter()
+            list(ex.map(one, range(threads)))
+            dt = time.perf_counter() - t0
+            log(f"cpu oracle: {threads} replicas x {n} queries in {dt:.1f} s")
+            if dt >= budget_s or n >= stream.n:
+                break
+            n = min(stream.n, int(n * (2.0 if dt < budget_s / 3 else 1.4)))
+    return {"value": threads * n / dt, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"replicas 0..{threads - 1}, queries 0..{n} of the same stream, one thread per replica, "
+                      f"{dt:.1f} s"}
 
 
 def _pmc_rows(path: str, counter: str):
@@ -287,7 +309,7 @@ def main() -> int:
         line["copy_probe_bytes"] = src.numel()
         del src, dst
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, args.evict, args.router,
+        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, R, args.evict, args.router,
                                             int(args.responses), args.beta, int(args.router_tree),
                                             args.router_tree_tokens)
     print(json.dumps(line), flush=True)
