@@ -39,27 +39,46 @@ __device__ __forceinline__ void wave_mem_sync() { __builtin_amdgcn_fence(__ATOMI
 
 __device__ __forceinline__ int first_lane(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
-  uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, KVR_WAVE);
-  uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, KVR_WAVE);
+// Wave reductions with DPP lane moves (no LDS round trip): shifts by 1, 2,
+// 4 and 8 lanes within each row of 16 leave the row's result in its lane 15,
+// then the broadcasts of lanes 15 and 31 to the following rows leave the
+// wave's result in lane 63, which is returned to every lane.  A lane whose
+// DPP source lies outside its row keeps its own value.  Call with the whole
+// wave active.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, kCtrl, kRowMask, 0xf, false);
+}
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  const uint32_t lo = dpp_u32<kCtrl, kRowMask>((uint32_t)v);
+  const uint32_t hi = dpp_u32<kCtrl, kRowMask>((uint32_t)(v >> 32));
   return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
-    uint64_t w = shfl_xor_u64(v, o);
-    v = w < v ? w : v;
+template <bool kMax>
+__device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t v) {
+#define KVR_RED_STEP(ctrl, rows)                  \
+  {                                               \
+    const uint64_t w = dpp_u64<ctrl, rows>(v);    \
+    v = kMax ? (w > v ? w : v) : (w < v ? w : v); \
   }
-  return v;
+  KVR_RED_STEP(0x111, 0xf)  // row_shr:1
+  KVR_RED_STEP(0x112, 0xf)  // row_shr:2
+  KVR_RED_STEP(0x114, 0xf)  // row_shr:4
+  KVR_RED_STEP(0x118, 0xf)  // row_shr:8
+  KVR_RED_STEP(0x142, 0xa)  // row_bcast:15 into rows 1 and 3
+  KVR_RED_STEP(0x143, 0xc)  // row_bcast:31 into rows 2 and 3
+#undef KVR_RED_STEP
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, KVR_WAVE - 1);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), KVR_WAVE - 1);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
-    uint64_t w = shfl_xor_u64(v, o);
-    v = w > v ? w : v;
-  }
-  return v;
-}
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) { return wave_reduce_u64<false>(v); }
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) { return wave_reduce_u64<true>(v); }
 
 // ---------------------------------------------------------------- Philox4x64-10
 // Salmon et al., SC'11: ten rounds, two 64x64->128 products per round, key
@@ -350,7 +369,7 @@ __device__ int32_t child_find(const int32_t* ar, const NodeRec& nd, int32_t tok)
       id = e.y;
     }
     uint64_t m = __ballot(hit);
-    if (m) return __shfl(id, first_lane(m), KVR_WAVE);
+    if (m) return __builtin_amdgcn_readlane(id, first_lane(m));
   }
   return -1;
 }
@@ -930,7 +949,7 @@ __device__ __forceinline__ bool evict_block(const Ptrs& P, St& s, const InsertAr
   int32_t c = 0;
   while (todo) {
     const int ld = first_lane(todo);
-    const uint32_t v = (uint32_t)__shfl((int)kk, ld, KVR_WAVE);
+    const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)kk, ld);
     const bool same = act && kk == v;
     const uint64_t m = __ballot(same);
     if (same) {
@@ -949,10 +968,10 @@ __device__ __forceinline__ bool evict_block(const Ptrs& P, St& s, const InsertAr
   wave_mem_sync();
   done = (uint32_t)f + 1u;
   if (exm) {
-    const uint32_t kkf = (uint32_t)__shfl((int)kk, f, KVR_WAVE);
-    const int32_t nf = __shfl(n, f, KVR_WAVE);
-    const int32_t pf = __shfl(nd.parent, f, KVR_WAVE);
-    const int32_t left = __shfl(top, f, KVR_WAVE);
+    const uint32_t kkf = (uint32_t)__builtin_amdgcn_readlane((int)kk, f);
+    const int32_t nf = __builtin_amdgcn_readlane(n, f);
+    const int32_t pf = __builtin_amdgcn_readlane(nd.parent, f);
+    const int32_t left = __builtin_amdgcn_readlane(top, f);
     if (left > 0) {  // the next token is marked: no longer a candidate
       arr_erase(P.U, s.nU, kkf);
       s.nU -= 1;
@@ -2042,7 +2061,7 @@ __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n)
         }
       }
       const uint64_t m = __ballot(mm < n);
-      if (m) return __shfl(mm, first_lane(m), KVR_WAVE);
+      if (m) return __builtin_amdgcn_readlane(mm, first_lane(m));
     }
   }
   return n;

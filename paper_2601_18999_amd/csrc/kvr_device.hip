@@ -110,11 +110,8 @@ __device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, i
       }
     }
   }
-  // minimum over the wave, then one LDS atomic per wave
-  for (int o = KVR_WAVE / 2; o > 0; o >>= 1) {
-    const int32_t y = __shfl_xor(m, o, KVR_WAVE);
-    m = y < m ? y : m;
-  }
+  // minimum over the wave (m >= 0), then one LDS atomic per wave
+  m = (int32_t)wave_min_u64((uint64_t)(uint32_t)m);
   if (lane_id() == 0) atomicMin(ell, m);
 }
 

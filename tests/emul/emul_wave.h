@@ -21,6 +21,8 @@ struct alignas(16) int4 { int x, y, z, w; };
 inline uint64_t __ballot(bool p) { return p ? 1ull : 0ull; }
 inline int __shfl(int v, int, int) { return v; }
 inline int __builtin_amdgcn_readlane(int v, int) { return v; }
+// one lane: every DPP source lies outside the row, so the lane keeps its value
+inline int __builtin_amdgcn_update_dpp(int old, int, int, int, int, bool) { return old; }
 inline int __builtin_amdgcn_readfirstlane(int v) { return v; }
 inline void __builtin_amdgcn_s_sleep(int) {}
 #define __ATOMIC_ACQUIRE_EMUL 0
