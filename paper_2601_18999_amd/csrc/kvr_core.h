@@ -625,17 +625,34 @@ __device__ int32_t child_slot(const int32_t* ar, const NodeRec& na, int32_t c) {
 }
 
 // Remove child c of node a, whose record (as read by the caller) is na; na
-// is updated to the new child count.
+// is updated to the new child count.  The last entry, which moves into the
+// removed one's slot, is taken from the chunk just read when it is there
+// (every array of up to 64 children).
 __device__ __forceinline__ bool child_remove_rec(const Ptrs& P, const St& s, int32_t a, NodeRec& na, int32_t c) {
   int32_t* ar = arena_of(P, s.arena_sel);
-  int32_t pos = child_slot(ar, na, c);
-  if (pos < 0) return false;
-  int32_t last = na.nchild - 1;
-  if (lane_id() == 0) {
-    if (pos != last) {
-      ar[na.coff + 2 * pos] = ar[na.coff + 2 * last];
-      ar[na.coff + 2 * pos + 1] = ar[na.coff + 2 * last + 1];
+  const int32_t last = na.nchild - 1;
+  int32_t pos = -1;
+  int2 lst = {0, 0};
+  bool have_last = false;
+  for (int32_t b = 0; b < na.nchild; b += KVR_WAVE) {
+    const int32_t k = b + lane_id();
+    int2 e = {0, -1};
+    if (k < na.nchild) e = *reinterpret_cast<const int2*>(ar + na.coff + 2 * k);
+    if (last >= b && last < b + KVR_WAVE) {
+      lst.x = __builtin_amdgcn_readlane(e.x, last - b);
+      lst.y = __builtin_amdgcn_readlane(e.y, last - b);
+      have_last = true;
     }
+    const uint64_t m = __ballot(k < na.nchild && e.y == c);
+    if (m) {
+      pos = b + first_lane(m);
+      break;
+    }
+  }
+  if (pos < 0) return false;
+  if (pos != last && !have_last) lst = *reinterpret_cast<const int2*>(ar + na.coff + 2 * last);
+  if (lane_id() == 0) {
+    if (pos != last) *reinterpret_cast<int2*>(ar + na.coff + 2 * pos) = lst;
     P.nodes[a].nchild = last;
   }
   wave_mem_sync();
@@ -1218,12 +1235,18 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
       KVR_FAIL_CHECK(s, 12, nf, s.nleaves, kkf);
       return false;
     }
+    // unless the parent takes the leaf-list entry over, the entry goes: the
+    // first chunk of that shift is read together with the child array
+    const bool takeover = pf != 0 && np.nchild == 1;
+    int32_t shift0 = 0;
+    const uint32_t k0 = (uint32_t)li + (uint32_t)lane_id();
+    if (!takeover && k0 + 1u < s.nleaves) shift0 = P.leaf[k0 + 1u];
     if (!child_remove_rec(P, s, pf, np, nf)) {
       KVR_FAIL_CHECK(s, 13, nf, pf, 0);
       return false;
     }
     node_free(P, s, nf);
-    if (pf != 0 && np.nchild == 0) {
+    if (takeover) {
       if (lane == 0) P.leaf[li] = pf;
       wave_mem_sync();
       const int32_t ptop = mark_top(s, np, pf);
@@ -1239,7 +1262,10 @@ __device__ __forceinline__ bool evict_block_staged(const Ptrs& P, St& s, const I
         s.nU -= 1;
       }
     } else {
-      arr_erase(P.leaf, s.nleaves, (uint32_t)li);
+      if (k0 + 1u < s.nleaves) P.leaf[k0] = shift0;
+      wave_mem_sync();
+      if ((uint32_t)li + (uint32_t)KVR_WAVE + 1u < s.nleaves)
+        arr_erase(P.leaf, s.nleaves, (uint32_t)li + (uint32_t)KVR_WAVE);
       s.nleaves -= 1;
       stage_erase(u, s.nU, kkf);
       s.nU -= 1;
