@@ -589,8 +589,19 @@ __device__ __forceinline__ void node_free(const Ptrs& P, St& s, int32_t id) {
   s.nnodes -= 1;
 }
 
-__device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c) {
-  NodeRec na = P.nodes[a];
+// Add child c (first token tok) to node a.  When the caller has read a's
+// child count, capacity and array offset (in semispace sel_read), they are
+// used unless a collection has switched semispaces since.
+__device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c,
+                                          const int32_t* known = nullptr, uint32_t sel_read = 0) {
+  NodeRec na;
+  if (known != nullptr && s.arena_sel == sel_read) {
+    na.nchild = known[0];
+    na.ccap = known[1];
+    na.coff = (uint32_t)known[2];
+  } else {
+    na = P.nodes[a];
+  }
   if (na.nchild == na.ccap) {
     int32_t ncap = na.ccap ? 2 * na.ccap : 2;
     uint32_t off;
@@ -1431,7 +1442,16 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     // (only when no edge is split: that would change what it reads), or here
     int32_t pos = -1;
     const bool rank_helper = ia.rank != nullptr && have_path && !split;
-    const bool replace = a != 0 && P.nodes[a].nchild == 0;
+    // a's child count, capacity and array offset, for the child added below
+    int32_t a_known[3];
+    {
+      const NodeRec na = P.nodes[a];
+      a_known[0] = na.nchild;
+      a_known[1] = na.ccap;
+      a_known[2] = (int32_t)na.coff;
+    }
+    const uint32_t a_sel = s.arena_sel;
+    const bool replace = a != 0 && a_known[0] == 0;
     if (!rank_helper) pos = new_leaf_rank(P, s, ar, split ? last : a, 0, split ? 1 : 0, qs[h]);
     // ---- the new leaf node holding q[h, L)
     bool ranked = false;
@@ -1468,7 +1488,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
       nl.ma = 0;
       node_put(P, l, nl);
     }
-    if (!child_add(P, s, a, qs[h], l)) goto fail;
+    if (!child_add(P, s, a, qs[h], l, a_known, a_sel)) goto fail;
     ar = arena_of(P, s.arena_sel);
     if (pos < 0 || (uint32_t)pos > s.nleaves) {
       KVR_FAIL_CHECK(s, 4, pos, s.nleaves, a);
