@@ -71,6 +71,7 @@
 // -ffp-contract=off so no multiply-add is fused.
 #include <cstdint>
 #include <cstring>
+#include <ctime>
 #include <deque>
 #include <map>
 #include <set>
@@ -134,6 +135,17 @@ typedef struct orc_worker_stats {
   // as above, L-LRU evictions
   uint64_t router_resident, router_digest_sum, router_digest_xor, router_evictions;
 } orc_worker_stats;
+
+// Options of orc_run_ex (all optional; zero-initialise).
+typedef struct orc_run_opts {
+  uint64_t snap_every;       // > 0: snapshot the per-worker state every snap_every queries
+  orc_worker_stats* snaps;   // [ceil(n / snap_every) * W] snapshots
+  uint64_t time_from;        // first query of the timed window
+  double time_budget_s;      // > 0: stop once the window has taken this much thread CPU time
+  double window_cpu_s;       // out: thread CPU seconds of the window
+  double window_wall_s;      // out: wall seconds of the window
+  uint64_t done;             // out: queries processed
+} orc_run_opts;
 
 }  // extern "C"
 
@@ -676,7 +688,8 @@ void digest(const Worker& w, orc_worker_stats& st) {
 
 bool check_invariants(const Sim& s) {
   for (const Worker& w : s.w) {
-    if (w.size > s.cfg.cache_tokens) return false;
+    if (w.size > s.cfg.cache_tokens) return false;  // |S_i| <= B_i (Sec. 3.1)
+    if (!(w.P >= 0.0)) return false;                // the load estimate never goes negative
     uint64_t alive = 0, marked = 0;
     for (size_t x = 1; x < w.nodes.size(); ++x) {
       const Node& n = w.nodes[x];
@@ -687,6 +700,7 @@ bool check_invariants(const Sim& s) {
     }
     if (alive != w.size) return false;
     if (s.cfg.evict == 0 && marked != w.cnt) return false;  // T is a subset of S after an insert
+    if (w.cnt > s.cfg.cache_tokens) return false;
     // the running batch is cached whole, and the in-progress counts are
     // exactly the number of running paths through each token
     std::vector<uint32_t> pins(w.nodes.size(), 0);
@@ -714,9 +728,66 @@ bool check_invariants(const Sim& s) {
       if (!w.nodes[n.parent].alive && n.parent != 0) return false;
     }
     if (alive != w.size) return false;
-    if (w.P < 0.0) return false;
   }
   return true;
+}
+
+// Signature of everything a cache holds: its tokens, marks, marking phase
+// and count, access stamps and in-progress counts.  A step may change only
+// the routed worker's (Eq. 3); the check compares these before and after.
+uint64_t cache_sig(const Worker& w) {
+  uint64_t h = mix64(w.size + 1);
+  h = mix64(h ^ w.phase);
+  h = mix64(h ^ w.cnt);
+  for (size_t x = 0; x < w.nodes.size(); ++x) {
+    const Node& n = w.nodes[x];
+    if (!n.alive) continue;
+    h = mix64(h + x);
+    h = mix64(h ^ (uint64_t)(uint32_t)n.tok);
+    h = mix64(h ^ (uint64_t)(uint32_t)n.parent);
+    h = mix64(h ^ n.mark);
+    h = mix64(h ^ n.stamp);
+    h = mix64(h ^ n.pin);
+    h = mix64(h ^ n.kids.size());
+  }
+  return h;
+}
+
+// The per-worker statistics of the current state (the counters plus the
+// path-hash digest of the cache and, with router_tree, of the router's tree).
+void snapshot(const Sim& s, uint32_t i, orc_worker_stats& out) {
+  const Worker& w = s.w[i];
+  out = w.st;
+  digest(w, out);
+  out.phase = w.phase;
+  out.cnt = w.cnt;
+  out.pending_depth = w.pend.size();
+  out.backlog_us = w.Wb;
+  out.last_decay_us = w.tl;
+  out.load_est = w.P;
+  for (int a = 0; a < 4; ++a) out.theta[a] = w.theta[a];
+  if (s.cfg.router_tree) {
+    const Worker& rw = s.rt[i];
+    orc_worker_stats rs;
+    std::memset(&rs, 0, sizeof(rs));
+    digest(rw, rs);
+    out.router_resident = rs.resident;
+    out.router_digest_sum = rs.digest_sum;
+    out.router_digest_xor = rs.digest_xor;
+    out.router_evictions = rw.st.evictions;
+  }
+}
+
+double thread_cpu_seconds() {
+  timespec ts;
+  clock_gettime(CLOCK_THREAD_CPUTIME_ID, &ts);
+  return (double)ts.tv_sec + 1e-9 * (double)ts.tv_nsec;
+}
+
+double wall_seconds() {
+  timespec ts;
+  clock_gettime(CLOCK_MONOTONIC, &ts);
+  return (double)ts.tv_sec + 1e-9 * (double)ts.tv_nsec;
 }
 
 }  // namespace
@@ -724,19 +795,26 @@ bool check_invariants(const Sim& s) {
 extern "C" {
 
 // Run replica `replica` over queries [0, n) of the stream from the initial
-// state (empty caches, zero loads, phase 1).  Outputs: route[j], hits[j] and,
-// if all_hits != NULL, all_hits[j*W + i].  wstats[W] receives the final
-// per-worker state.  Returns 0, or a bit set: 1 = bad argument,
-// 2 = invariant violated, 4 = a path longer than the cache.
-int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* tokens,
-            const uint64_t* offsets, const int64_t* arrival_us, const uint16_t* out_len,
-            int32_t* route, int32_t* hits, int32_t* all_hits, orc_worker_stats* wstats) {
+// state (empty caches, zero loads, phase 1; Sec. 3.1, Table 1).  Outputs:
+// route[j], hits[j] and, if all_hits != NULL, all_hits[j*W + i].  wstats[W]
+// receives the final per-worker state.  opts (optional) asks for snapshots of
+// the per-worker state every snap_every queries (snapshot k, after query
+// (k+1)*snap_every - 1 or the last one, in snaps[k*W + i]) and times the
+// queries from time_from on (thread CPU and wall seconds), stopping once
+// they have taken time_budget_s of CPU time when that is positive.
+// Returns 0, or a bit set: 1 = bad argument, 2 = invariant violated (with
+// check = 1), 4 = a path longer than the cache.
+int orc_run_ex(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* tokens,
+               const uint64_t* offsets, const int64_t* arrival_us, const uint16_t* out_len,
+               int32_t* route, int32_t* hits, int32_t* all_hits, orc_worker_stats* wstats,
+               orc_run_opts* opts) {
   if (!cfg || cfg->num_workers == 0 || cfg->cache_tokens == 0 || cfg->decay_interval_us <= 0) return 1;
+  const uint32_t W = cfg->num_workers;
   Sim s;
   s.cfg = *cfg;
   s.replica = replica;
-  s.w.resize(cfg->num_workers);
-  s.rt.resize(cfg->router_tree ? cfg->num_workers : 0);
+  s.w.resize(W);
+  s.rt.resize(cfg->router_tree ? W : 0);
   for (Worker& w : s.w) {
     w.nodes.emplace_back();
     w.nodes[0].alive = true;
@@ -749,7 +827,19 @@ int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* 
     w.nodes[0].alive = true;
     std::memset(&w.st, 0, sizeof(w.st));
   }
-  for (uint64_t j = 0; j < n; ++j) {
+  const uint64_t snap_every = opts ? opts->snap_every : 0;
+  const uint64_t time_from = opts ? opts->time_from : n;
+  double cpu0 = 0.0, wall0 = 0.0;
+  std::vector<uint64_t> sig_w, sig_rt;
+  uint64_t j = 0;
+  for (; j < n; ++j) {
+    if (j == time_from) {
+      cpu0 = thread_cpu_seconds();
+      wall0 = wall_seconds();
+    } else if (j > time_from && opts && opts->time_budget_s > 0.0 &&
+               thread_cpu_seconds() - cpu0 >= opts->time_budget_s) {
+      break;
+    }
     const int32_t* q = tokens + offsets[j];
     const int32_t Lpath = (int32_t)(offsets[j + 1] - offsets[j]);
     int32_t o = out_len ? (int32_t)out_len[j] : 4;
@@ -758,37 +848,108 @@ int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* 
       s.error |= 1;
       break;
     }
-    step(s, j, q, L, Lpath, arrival_us[j], o, route ? route + j : nullptr, hits ? hits + j : nullptr,
-         all_hits ? all_hits + j * cfg->num_workers : nullptr);
+    if (cfg->check) {
+      sig_w.resize(W);
+      sig_rt.resize(s.rt.size());
+      for (uint32_t i = 0; i < W; ++i) sig_w[i] = cache_sig(s.w[i]);
+      for (size_t i = 0; i < s.rt.size(); ++i) sig_rt[i] = cache_sig(s.rt[i]);
+    }
+    int32_t routed = -1;
+    step(s, j, q, L, Lpath, arrival_us[j], o, &routed, hits ? hits + j : nullptr,
+         all_hits ? all_hits + j * W : nullptr);
+    if (route) route[j] = routed;
     if (s.error) break;
-    if (cfg->check && !check_invariants(s)) {
-      s.error |= 2;
-      break;
+    if (cfg->check) {
+      if (!check_invariants(s)) s.error |= 2;
+      // Eq. 3: no cache but the routed worker's changed (nor its router tree)
+      for (uint32_t i = 0; i < W; ++i)
+        if ((int32_t)i != routed && cache_sig(s.w[i]) != sig_w[i]) s.error |= 2;
+      for (size_t i = 0; i < s.rt.size(); ++i)
+        if ((int32_t)i != routed && cache_sig(s.rt[i]) != sig_rt[i]) s.error |= 2;
+      if (s.error) {
+        ++j;
+        break;
+      }
+    }
+    if (snap_every && opts->snaps && ((j + 1) % snap_every == 0 || j + 1 == n)) {
+      const uint64_t k = j / snap_every;
+      for (uint32_t i = 0; i < W; ++i) snapshot(s, i, opts->snaps[k * W + i]);
     }
   }
-  for (uint32_t i = 0; i < cfg->num_workers; ++i) {
-    Worker& w = s.w[i];
-    digest(w, w.st);
-    w.st.phase = w.phase;
-    w.st.cnt = w.cnt;
-    w.st.pending_depth = w.pend.size();
-    w.st.backlog_us = w.Wb;
-    w.st.last_decay_us = w.tl;
-    w.st.load_est = w.P;
-    for (int a = 0; a < 4; ++a) w.st.theta[a] = w.theta[a];
-    if (cfg->router_tree) {
-      Worker& rw = s.rt[i];
-      orc_worker_stats rs;
-      std::memset(&rs, 0, sizeof(rs));
-      digest(rw, rs);
-      w.st.router_resident = rs.resident;
-      w.st.router_digest_sum = rs.digest_sum;
-      w.st.router_digest_xor = rs.digest_xor;
-      w.st.router_evictions = rw.st.evictions;
+  if (opts) {
+    opts->done = j;
+    if (j > time_from) {
+      opts->window_cpu_s = thread_cpu_seconds() - cpu0;
+      opts->window_wall_s = wall_seconds() - wall0;
+    } else {
+      opts->window_cpu_s = opts->window_wall_s = 0.0;
     }
-    if (wstats) wstats[i] = w.st;
   }
+  if (wstats)
+    for (uint32_t i = 0; i < W; ++i) snapshot(s, i, wstats[i]);
   return s.error;
+}
+
+int orc_run(const orc_config* cfg, uint32_t replica, uint64_t n, const int32_t* tokens,
+            const uint64_t* offsets, const int64_t* arrival_us, const uint16_t* out_len,
+            int32_t* route, int32_t* hits, int32_t* all_hits, orc_worker_stats* wstats) {
+  return orc_run_ex(cfg, replica, n, tokens, offsets, arrival_us, out_len, route, hits, all_hits, wstats,
+                    nullptr);
+}
+
+// Self-test of the invariant checks: build a two-worker state, plant one
+// violation (1 = a negative load estimate on a worker, 2 = a changed mark on
+// a worker the step did not route to, 3 = a token whose parent is gone) and
+// return 1 when the checks report it, 0 when they miss it.
+int orc_check_selftest(int which) {
+  Sim s;
+  s.replica = 0;
+  std::memset(&s.cfg, 0, sizeof(s.cfg));
+  s.cfg.num_workers = 2;
+  s.cfg.cache_tokens = 64;
+  s.cfg.decay_interval_us = 20000;
+  s.cfg.rho = 1.0;
+  s.cfg.lr = 0.992;
+  s.cfg.alpha_miss = 1.0;
+  s.cfg.true_miss_us = 1000;
+  s.cfg.batch_size = 1;
+  s.w.resize(2);
+  for (Worker& w : s.w) {
+    w.nodes.emplace_back();
+    w.nodes[0].alive = true;
+    std::memset(&w.st, 0, sizeof(w.st));
+  }
+  const int32_t qa[4] = {1, 2, 3, 4}, qb[3] = {7, 8, 9};
+  int32_t r0 = -1, r1 = -1;
+  step(s, 0, qa, 4, 4, 0, 4, &r0, nullptr, nullptr);
+  step(s, 1, qb, 3, 3, 1000, 4, &r1, nullptr, nullptr);
+  if (!check_invariants(s)) return 0;  // the clean state must pass
+  const uint64_t sig1 = cache_sig(s.w[1]);
+  if (which == 1) {
+    s.w[1].P = -1e-3;
+    return check_invariants(s) ? 0 : 1;
+  }
+  if (which == 2) {
+    // worker 1 holds qb (routed away from the loaded worker 0); re-mark one
+    // of its tokens as if a step routed to worker 0 had touched it
+    for (size_t x = 1; x < s.w[1].nodes.size(); ++x)
+      if (s.w[1].nodes[x].alive) {
+        s.w[1].nodes[x].mark += 1;
+        break;
+      }
+    return cache_sig(s.w[1]) != sig1 ? 1 : 0;
+  }
+  if (which == 3) {
+    Worker& w = s.w[r1];
+    for (size_t x = 1; x < w.nodes.size(); ++x)
+      if (w.nodes[x].alive && w.nodes[x].parent == 0) {
+        w.nodes[x].alive = false;  // an internal token gone: its child dangles
+        w.size -= 1;
+        break;
+      }
+    return check_invariants(s) ? 0 : 1;
+  }
+  return 0;
 }
 
 // Philox4x64-10 block for (counter, key); exported for the known-answer test.

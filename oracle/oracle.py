@@ -67,6 +67,18 @@ class OrcWorkerStats(ctypes.Structure):
                 + [(n, ctypes.c_uint64) for n in _ROUTER_U64])
 
 
+class OrcRunOpts(ctypes.Structure):
+    _fields_ = [
+        ("snap_every", ctypes.c_uint64),
+        ("snaps", ctypes.c_void_p),
+        ("time_from", ctypes.c_uint64),
+        ("time_budget_s", ctypes.c_double),
+        ("window_cpu_s", ctypes.c_double),
+        ("window_wall_s", ctypes.c_double),
+        ("done", ctypes.c_uint64),
+    ]
+
+
 def build(force: bool = False) -> str:
     """Compile the oracle with g++ (plain C++17, no FMA contraction)."""
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
@@ -89,6 +101,10 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.POINTER(OrcWorkerStats)]
+        _lib.orc_run_ex.restype = ctypes.c_int
+        _lib.orc_run_ex.argtypes = list(_lib.orc_run.argtypes) + [ctypes.POINTER(OrcRunOpts)]
+        _lib.orc_check_selftest.restype = ctypes.c_int
+        _lib.orc_check_selftest.argtypes = [ctypes.c_int]
         _lib.orc_philox4x64_10.restype = None
         _lib.orc_philox4x64_10.argtypes = [ctypes.c_void_p] * 3
         _lib.orc_pow_int.restype = ctypes.c_double
@@ -137,9 +153,27 @@ def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data
 
 
+def _worker_dict(s) -> Dict[str, Any]:
+    d = {name: int(getattr(s, name)) for name in _U64}
+    d["backlog_us"] = int(s.backlog_us)
+    d["last_decay_us"] = int(s.last_decay_us)
+    d["load_est"] = float(s.load_est)
+    d["theta"] = [float(x) for x in s.theta]
+    for name in _ROUTER_U64:
+        d[name] = int(getattr(s, name))
+    return d
+
+
 def run(stream, W: int, B: int, replica: int = 0, n: Optional[int] = None,
-        all_hits: bool = False, **kw) -> Dict[str, Any]:
-    """Run one replica of the simulation over the first ``n`` queries."""
+        all_hits: bool = False, snap_every: int = 0, time_from: Optional[int] = None,
+        time_budget_s: float = 0.0, **kw) -> Dict[str, Any]:
+    """Run one replica of the simulation over the first ``n`` queries.
+
+    ``snap_every`` > 0 adds ``snaps``: the per-worker state after every
+    ``snap_every`` queries (and after the last).  ``time_from`` times the
+    queries from that index on (``window_cpu_s``, ``window_wall_s``; with
+    ``time_budget_s`` > 0 the run stops once they took that much CPU time,
+    and ``done`` says how many queries ran)."""
     cfg = make_config(W, B, **kw)
     n = stream.n if n is None else min(int(n), stream.n)
     tokens = np.ascontiguousarray(stream.tokens, dtype=np.int32)
@@ -150,20 +184,31 @@ def run(stream, W: int, B: int, replica: int = 0, n: Optional[int] = None,
     hits = np.zeros(n, dtype=np.int32)
     ah = np.zeros((n, W), dtype=np.int32) if all_hits else None
     ws = (OrcWorkerStats * W)()
-    rc = lib().orc_run(ctypes.byref(cfg), replica, n, _ptr(tokens), _ptr(offsets), _ptr(arrival),
-                       _ptr(out_len), _ptr(route), _ptr(hits), _ptr(ah), ws)
-    workers = []
-    for i in range(W):
-        s = ws[i]
-        d = {name: int(getattr(s, name)) for name in _U64}
-        d["backlog_us"] = int(s.backlog_us)
-        d["last_decay_us"] = int(s.last_decay_us)
-        d["load_est"] = float(s.load_est)
-        d["theta"] = [float(x) for x in s.theta]
-        for name in _ROUTER_U64:
-            d[name] = int(getattr(s, name))
-        workers.append(d)
-    return {"rc": rc, "route": route, "hits": hits, "all_hits": ah, "workers": workers}
+    opts = OrcRunOpts()
+    nsnap = (n + snap_every - 1) // snap_every if snap_every > 0 else 0
+    snaps = (OrcWorkerStats * max(1, nsnap * W))()
+    opts.snap_every = int(snap_every)
+    opts.snaps = ctypes.cast(snaps, ctypes.c_void_p) if nsnap else None
+    opts.time_from = n if time_from is None else int(time_from)
+    opts.time_budget_s = float(time_budget_s)
+    rc = lib().orc_run_ex(ctypes.byref(cfg), replica, n, _ptr(tokens), _ptr(offsets), _ptr(arrival),
+                          _ptr(out_len), _ptr(route), _ptr(hits), _ptr(ah), ws, ctypes.byref(opts))
+    done = int(opts.done)
+    out = {"rc": rc, "route": route[:done], "hits": hits[:done],
+           "all_hits": None if ah is None else ah[:done],
+           "workers": [_worker_dict(ws[i]) for i in range(W)], "done": done,
+           "window_cpu_s": float(opts.window_cpu_s), "window_wall_s": float(opts.window_wall_s)}
+    if nsnap:
+        out["snaps"] = [[_worker_dict(snaps[k * W + i]) for i in range(W)]
+                        for k in range((done + snap_every - 1) // snap_every)]
+    return out
+
+
+def check_selftest(which: int) -> bool:
+    """True when the oracle's invariant checks catch planted violation
+    ``which`` (1: negative load estimate, 2: a non-routed cache changed,
+    3: a token whose parent is gone)."""
+    return bool(lib().orc_check_selftest(int(which)))
 
 
 def philox4x64_10(counter, key) -> np.ndarray:

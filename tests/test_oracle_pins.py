@@ -320,6 +320,63 @@ def test_nlms_single_step_closed_form():
     np.testing.assert_allclose(r["workers"][0]["theta"], theta, rtol=1e-13, atol=1e-18)
 
 
+def _nlms_step(theta, phi, e, mu=0.992, eps=1e-9):
+    """One normalised-LMS step, every sum left to right (Sec. 4.2 update)."""
+    ss = phi[0] * phi[0]
+    ss = ss + phi[1] * phi[1]
+    ss = ss + phi[2] * phi[2]
+    ss = ss + phi[3] * phi[3]
+    g = (mu * e) / (eps + ss)
+    return [theta[a] + g * phi[a] for a in range(4)]
+
+
+def _dot4(theta, phi):
+    acc = theta[0] * phi[0]
+    acc = acc + theta[1] * phi[1]
+    acc = acc + theta[2] * phi[2]
+    return acc + theta[3] * phi[3]
+
+
+def test_nlms_error_uses_current_model_when_completions_lag_routing():
+    """Algorithm 2's update thread minimises the squared loss of Sec. 4.2 at
+    the current parameters: the error fed to the update is the observed
+    latency minus the current model's prediction on the features stored at
+    routing.  Two queries are routed to one worker before the first
+    completes, so the second update differs from one that feeds the
+    prediction made at routing time (when theta was still 0): the pin tells
+    the two readings apart."""
+    L1, L2, shared, o = 30, 50, 10, 4
+    q1 = list(range(L1))
+    q2 = list(range(shared)) + list(range(500, 500 + L2 - shared))
+    s = _paths_stream([q1, q2, [900]], [0, 1, 2], out_len=o)
+    s.arrival_us = np.array([0, 1000, 10**9], np.int64)  # q2 routed before q1 completes
+    r = O.run(s, 1, 1000, update="nlms")
+    assert list(r["hits"]) == [0, shared, 0]
+    # query 1 at t = 0: empty cache, zero load
+    x2_1 = float(L1 - 0) * 0.001
+    phi1 = [0.0, x2_1, 0.0, 1.0]
+    chat1 = 0.0 * 0.0 + 1.0 * x2_1
+    base1 = chat1 + 0.0
+    cost1 = 1000 * L1 + 10000 * o
+    E1 = cost1 * 1e-6
+    # query 2 at t = 1 ms (same decay tick): load = chat1, backlog = cost1 - 1 ms
+    P2 = 0.0 + chat1
+    x1_2, x2_2 = float(shared) * 0.001, float(L2 - shared) * 0.001
+    phi2 = [x1_2, x2_2, P2, 1.0]
+    chat2 = 0.0 * x1_2 + 1.0 * x2_2
+    base2 = chat2 + P2
+    E2 = ((cost1 - 1000) + (1000 * (L2 - shared) + 10000 * o)) * 1e-6
+    # both complete before query 3: updates in FIFO order
+    theta1 = _nlms_step([0.0] * 4, phi1, E1 - (base1 + _dot4([0.0] * 4, phi1)))
+    theta_now = _nlms_step(theta1, phi2, E2 - (base2 + _dot4(theta1, phi2)))
+    theta_routing = _nlms_step(theta1, phi2, E2 - (base2 + _dot4([0.0] * 4, phi2)))
+    got = r["workers"][0]["theta"]
+    np.testing.assert_allclose(got, theta_now, rtol=1e-15, atol=0.0)
+    # the readings differ by far more than rounding on this stream
+    diff = np.abs(np.array(theta_now) - np.array(theta_routing))
+    assert diff.max() > 1e-3 * np.abs(theta_now).max(), (theta_now, theta_routing)
+
+
 def test_rls_equals_weighted_ridge_least_squares():
     """RLS with forgetting factor lam and P0 = p0*I minimises
     sum_t lam^(n-t) (y_t - theta.phi_t)^2 + lam^n |theta|^2 / p0."""
@@ -369,6 +426,33 @@ def test_invariants_hold(seed):
         assert w["resident"] == w["loads"] - w["evictions"]
         assert w["marked_count"] == w["cnt"] <= B
         assert w["load_est"] >= 0.0
+
+
+@pytest.mark.parametrize("which", [1, 2, 3])
+def test_invariant_checks_catch_planted_violations(which):
+    """The oracle's own checks fire on a planted violation (on the CPU):
+    1 = a negative load estimate on a worker, 2 = a change to a worker the
+    step did not route to (Eq. 3), 3 = a token whose parent is gone."""
+    assert O.check_selftest(which)
+
+
+@pytest.mark.parametrize("mode", ["rlt", "lru", "responses", "batch", "router_tree", "cache_aware"])
+def test_invariants_and_eq3_hold_every_step(mode):
+    """check = 1: after every step capacity, prefix closure, marks, running
+    batch counts and P >= 0 hold, and only the routed worker's cache (and
+    router tree) changed (Sec. 3.1, Eq. 3)."""
+    s = generate(small_spec(n=300, groups=6, prefix_len=(8, 40), suffix_len=(4, 24), vocab=12, seed=7))
+    kw = {"rlt": {}, "lru": {"evict": "lru"}, "responses": {"cache_responses": 1},
+          "batch": {"batch_size": 3}, "router_tree": {"router_tree": 1, "router_tree_tokens": 90},
+          "cache_aware": {"router": "cache_aware", "ca_balance_abs": 2}}[mode]
+    if mode == "responses":
+        s = generate(dict(small_spec(n=300, groups=6, prefix_len=(8, 40), suffix_len=(4, 24), vocab=12,
+                                     seed=7), responses=True))
+    B = 3 * s.max_len if mode == "batch" else 160  # batching assumes beta * L_max <= B
+    r = O.run(s, 3, B, replica=1, check=1, **kw)
+    assert r["rc"] == 0
+    assert sum(w["evictions"] for w in r["workers"]) > 0
+    assert len(set(r["route"].tolist())) > 1
 
 
 # ---------------------------------------------------------------------------
