@@ -4,9 +4,12 @@
 A step is one kvr_route_batch call: one batch of `--batch` queries of the
 synthetic stream, routed for every replica (completions and decay, the match
 on every worker, LBGR score/argmin/commit, RLT insertion).  The first
-`--warmup` batches fill the caches untimed; the next `--steps` batches are
-timed with events on the library's stream, with the stream and workspace
-already resident in HBM.  Prints one JSON line.
+`--warmup` batches fill the caches; the next `--steps` batches are the timed
+window (events on the library's stream, with the stream and workspace
+already resident in HBM).  The rest of the stream is then routed too, so the
+line also reports the whole stream's rate.  The CPU oracle is timed on the
+same window of the same stream (run untimed up to its first query).  Prints
+one JSON line.
 
 Default workload: the largest configuration (32 replicas x 32 workers,
 262,144-token caches, prompts of 2,176-9,216 tokens from 256 Zipf groups in
@@ -44,15 +47,18 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
+def load_traffic(workload: str, batch: int, warmup: int, steps: int):
     """HBM bytes per step-kernel launch measured by rocprofv3 counters, if
-    they were taken on the current kernel sources."""
+    they were taken on the current kernel sources over the same window
+    (batch size, warm-up and timed batches)."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
     if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    if (t.get("batch"), t.get("warmup"), t.get("steps")) != (batch, warmup, steps):
         return None
     return t
 
@@ -76,36 +82,55 @@ def host_cores() -> int:
     return max(1, min(16, n))
 
 
-def cpu_baseline(stream, W, B, budget_s: float, replicas: int, evict: str = "rlt", router: str = "lbgr",
-                 responses: int = 0, beta: int = 1, router_tree: int = 0, router_tree_tokens: int = 0):
-    """The CPU oracle on the host's cores: one single-threaded oracle run per
-    replica, as many replicas at once as there are cores (its C entry point
-    releases the GIL), each over the first n queries of the same stream; n
-    grown until one round takes at least budget_s (the cost per query grows
-    as the caches fill, so the last steps grow by 1.4x)."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(stream, W, B, q0: int, q1: int, budget_s: float, replicas: int, evict: str = "rlt",
+                 router: str = "lbgr", responses: int = 0, beta: int = 1, router_tree: int = 0,
+                 router_tree_tokens: int = 0):
+    """The CPU oracle on the host's cores, on the GPU's timed window: one
+    single-threaded oracle run per replica, as many replicas at once as there
+    are cores (its C entry point releases the GIL).  Each run goes untimed
+    through queries [0, q0), then times queries q0, q0+1, ... (thread CPU
+    time and wall time) until the window [q0, q1) ends or the timed part has
+    taken budget_s of CPU time.  1-core rate = timed queries / timed CPU
+    seconds, summed over the threads; all-core rate = the sum of the
+    threads' timed queries / wall seconds (they run concurrently)."""
     from concurrent.futures import ThreadPoolExecutor
     from oracle import oracle as O
     O.lib()  # built and loaded once, before the threads
     threads = max(1, min(replicas, host_cores()))
-    n = min(1000, stream.n)
 
-    def one(r: int) -> None:
-        o = O.run(stream, W, B, replica=r, n=n, evict=evict, router=router, cache_responses=responses,
-                  batch_size=beta, router_tree=router_tree, router_tree_tokens=router_tree_tokens)
+    def one(r: int):
+        o = O.run(stream, W, B, replica=r, n=q1, time_from=q0, time_budget_s=budget_s, evict=evict,
+                  router=router, cache_responses=responses, batch_size=beta, router_tree=router_tree,
+                  router_tree_tokens=router_tree_tokens)
         assert o["rc"] == 0, (r, o["rc"])
+        return o["done"] - q0, o["window_cpu_s"], o["window_wall_s"]
 
+    t0 = time.perf_counter()
     with ThreadPoolExecutor(max_workers=threads) as ex:
-        while True:
-            t0 = time.perf_counter()
-            list(ex.map(one, range(threads)))
-            dt = time.perf_counter() - t0
-            log(f"cpu oracle: {threads} replicas x {n} queries in {dt:.1f} s")
-            if dt >= budget_s or n >= stream.n:
-                break
-            n = min(stream.n, int(n * (2.0 if dt < budget_s / 3 else 1.4)))
-    return {"value": threads * n / dt, "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": f"replicas 0..{threads - 1}, queries 0..{n} of the same stream, one thread per replica, "
-                      f"{dt:.1f} s"}
+        res = list(ex.map(one, range(threads)))
+    dt = time.perf_counter() - t0
+    nq = sum(r[0] for r in res)
+    cpu = sum(r[1] for r in res)
+    agg = sum(r[0] / r[2] for r in res if r[2] > 0)
+    qmin, qmax = min(r[0] for r in res), max(r[0] for r in res)
+    log(f"cpu oracle: {threads} replicas, queries {q0}..{q0 + qmin}-{q0 + qmax} timed "
+        f"({cpu:.1f} CPU s), {dt:.1f} s in all")
+    return {"value": agg, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "per_core": nq / cpu if cpu > 0 else None, "cpu_model": cpu_model(),
+            "sample": f"replicas 0..{threads - 1}, one thread each; queries [0, {q0}) untimed, then "
+                      f"{qmin}..{qmax} queries of the GPU's timed window from query {q0} on, "
+                      f"{cpu:.1f} CPU s timed in all"}
 
 
 def _pmc_rows(path: str, counter: str):
@@ -130,17 +155,17 @@ def traffic_from(args) -> int:
     if probe <= 0:
         print("--traffic-from needs the --copy-probe-mib of the profiled runs", file=sys.stderr)
         return 2
-    out = {"kernel_source_hash": kernel_source_hash(), "workload": workload, "steps": args.steps,
-           "warmup": args.warmup, "copy_probe_bytes": probe}
+    out = {"kernel_source_hash": kernel_source_hash(), "workload": workload, "batch": args.batch,
+           "steps": args.steps, "warmup": args.warmup, "copy_probe_bytes": probe}
     per = {}
     for path, counter in zip(args.traffic_from, ("FETCH_SIZE", "WRITE_SIZE")):
         rows = _pmc_rows(path, counter)
         step = [v for _, name, v in rows if "step_kernel" in name]
-        if len(step) != args.warmup + args.steps:
-            print(f"{path}: {len(step)} step-kernel dispatches, expected {args.warmup + args.steps}",
+        if len(step) < args.warmup + args.steps:
+            print(f"{path}: {len(step)} step-kernel dispatches, expected at least {args.warmup + args.steps}",
                   file=sys.stderr)
             return 1
-        timed = step[args.warmup:]
+        timed = step[args.warmup:args.warmup + args.steps]
         # the probe: the last other dispatch whose count is near the probe size
         cand = [v for _, name, v in rows if "kvr::" not in name and 0.5 * probe <= v * 1024 <= 2 * probe]
         if not cand:
@@ -161,8 +186,8 @@ def traffic_from(args) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=6)
-    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batch", type=int, default=2000)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--evict", choices=["rlt", "lru"], default="rlt",
@@ -179,8 +204,11 @@ def main() -> int:
                     help="approximate router: the router scores with matches on L-LRU trees of its own "
                          "(one per worker, the routed prompts) instead of the workers' caches")
     ap.add_argument("--router-tree-tokens", type=int, default=0, help="budget of each router tree (0 = B)")
-    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--cpu-budget", type=float, default=10.0,
+                    help="CPU seconds per oracle thread on the timed window")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-whole", action="store_true",
+                    help="stop after the timed window instead of routing the rest of the stream")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, copy this many MiB device to device with a plain "
                          "copy kernel (the calibration run for rocprofv3 byte counters)")
@@ -223,25 +251,32 @@ def main() -> int:
     torch.cuda.synchronize()
 
     log(f"workspace {sim.nbytes / 1e9:.1f} GB, stream resident")
-    q = 0
+    nb = (stream.n + args.batch - 1) // args.batch  # batches in the whole stream
+    # every batch is timed with events on the library's stream; the metric
+    # is the window [warmup, warmup + steps), the rest of the stream follows
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nb)]
+
+    def run_batch(k: int) -> None:
+        b0 = k * args.batch
+        m = min(args.batch, stream.n - b0)
+        ev[k][0].record(sim.stream)
+        sim.route(ds, b0, m, out=out if m == args.batch else None)
+        ev[k][1].record(sim.stream)
+
     for k in range(args.warmup):
-        sim.route(ds, q, args.batch, out=out)
+        run_batch(k)
         torch.cuda.synchronize()
-        q += args.batch
         log(f"warmup batch {k + 1}/{args.warmup} done")
     before = totals(sim.stats())
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    q0 = q
+    q0 = args.warmup * args.batch
+    q = q0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
-        ev[k][0].record(sim.stream)
-        sim.route(ds, q, args.batch, out=out)
-        ev[k][1].record(sim.stream)
+    for k in range(args.warmup, args.warmup + args.steps):
+        run_batch(k)
         q += args.batch
         ev[k][1].synchronize()
-        log(f"timed batch {k + 1}/{args.steps}: {ev[k][0].elapsed_time(ev[k][1]):.1f} ms")
+        log(f"timed batch {k + 1 - args.warmup}/{args.steps}: {ev[k][0].elapsed_time(ev[k][1]):.1f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st, bits = sim.check()
@@ -250,23 +285,24 @@ def main() -> int:
         return 1
     after = totals(sim.stats())
     d = {k: after[k] - before[k] for k in after}
-    kernel_ms = sum(a.elapsed_time(b) for a, b in ev)
+    kernel_ms = sum(ev[k][0].elapsed_time(ev[k][1]) for k in range(args.warmup, args.warmup + args.steps))
     nq = R * (q - q0)
     paths = stream.lengths[q0:q].astype("int64")
     path_tokens = int(paths.sum()) * R
     prompt = path_tokens - (int(stream.out_len[q0:q].astype("int64").sum()) * R if args.responses else 0)
     assert prompt == d["prompt_tokens"]
     # algorithmic bytes of the timed launches: query (path) staging, edge
-    # tokens compared on every worker, edge tokens written for loaded tokens,
-    # one candidate/node read-modify-write per eviction, LBGR + completion
-    # record
+    # tokens compared on every worker (every h_ij, as a full walk reads
+    # them), edge tokens written for loaded tokens, one candidate/node
+    # read-modify-write per eviction, LBGR + completion record
     alg_bytes = (4 * path_tokens + 4 * d["matched_tokens"] + 4 * d["loads"] + 32 * d["evictions"]
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
     default_run = (args.evict, args.router, args.responses, args.beta, args.router_tree) == \
         ("rlt", "lbgr", False, 1, False)
-    traffic = load_traffic(workload) if default_run else None
+    traffic = load_traffic(workload, args.batch, args.warmup, args.steps) if default_run else None
+    launch_s = kernel_ms * 1e-3 / args.steps
     line = {
         "metric": "routed queries/sec",
         "value": nq / (kernel_ms * 1e-3),
@@ -295,8 +331,26 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic["bytes_per_launch"] if traffic else None,
-                     "alg_bytes_per_launch": alg_bytes / args.steps},
+                     "alg_bytes_per_launch": alg_bytes / args.steps,
+                     # the counted HBM bytes of the same launches over their duration
+                     "measured_gbs": traffic["bytes_per_launch"] / launch_s / 1e9 if traffic else None,
+                     "measured_frac": traffic["bytes_per_launch"] / launch_s / 1e9 / HBM_PEAK_GBS
+                     if traffic else None},
     }
+    if not args.no_whole:
+        for k in range(args.warmup + args.steps, nb):
+            run_batch(k)
+            if (k + 1) % 10 == 0 or k + 1 == nb:
+                ev[k][1].synchronize()
+                log(f"rest of the stream: batch {k + 1}/{nb}")
+        torch.cuda.synchronize()
+        st, bits = sim.check()
+        if st != K.KVR_OK:
+            print(f"device status {st} bits {bits}: {K.kvr_last_error()}", file=sys.stderr)
+            return 1
+        whole_ms = sum(a.elapsed_time(b) for a, b in ev)
+        line["whole_stream"] = {"value": R * stream.n / (whole_ms * 1e-3), "unit": "queries/s",
+                                "ms": whole_ms, "batches": nb, "queries": stream.n}
     sim.close()
     del ds, out
     torch.cuda.empty_cache()
@@ -309,7 +363,7 @@ def main() -> int:
         line["copy_probe_bytes"] = src.numel()
         del src, dst
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(stream, W, B, args.cpu_budget, R, args.evict, args.router,
+        line["cpu_baseline"] = cpu_baseline(stream, W, B, q0, q, args.cpu_budget, R, args.evict, args.router,
                                             int(args.responses), args.beta, int(args.router_tree),
                                             args.router_tree_tokens)
     print(json.dumps(line), flush=True)

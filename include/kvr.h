@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 6u
+#define KVR_ABI_VERSION 7u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -148,6 +148,12 @@ typedef struct kvr_config {
    * stamps are 32-bit query indices). */
   int32_t router_tree;
   uint32_t router_tree_tokens;
+  /* 1: the step kernel also accumulates, per replica, real-time counter
+   * ticks (100 MHz) spent by its routing wave in each part of a step
+   * (kvr_replica_stats.phase_ticks); only with evict = KVR_EVICT_RLT,
+   * router_tree = 0 and batch_size = 1.  0 (default): no timing. */
+  int32_t phase_timers;
+  uint32_t pad1;
 } kvr_config;
 
 /* Final per-(replica, worker) state and counters (kvr_stats). */
@@ -166,6 +172,39 @@ typedef struct kvr_worker_stats {
   uint64_t router_resident, router_digest_sum, router_digest_xor, router_evictions;
 } kvr_worker_stats;
 
+/* Parts of a step timed with phase_timers = 1 (kvr_replica_stats.phase_ticks). */
+enum {
+  KVR_PHASE_ROUTE = 0,      /* scores, argmin and commit (Algorithm 2 routing thread) */
+  KVR_PHASE_STAGE_WAIT = 1, /* waiting for the next query's staging                  */
+  KVR_PHASE_MARK = 2,       /* RLT insertion: marking walk over the cached part      */
+  KVR_PHASE_LOAD = 3,       /* split, new leaf's rank, edge copy, tree and list edits */
+  KVR_PHASE_EVICT = 4,      /* evictions of the loaded tokens (Algorithm 1)          */
+  KVR_PHASE_FINISH = 5,     /* marks of the loaded tokens, header, recorded path     */
+  KVR_PHASE_MATCH = 6,      /* the routed worker's h of the next query               */
+  KVR_PHASE_JOIN = 7,       /* waiting for the other workers' h of the next query    */
+  KVR_PHASES = 8
+};
+
+/* Per-replica state and counters (kvr_stats): the Sec. 5 metrics summed over
+ * the replica's workers, and a digest of its routing decisions.
+ * route_digest is the hash chain D_0 = 0,
+ *   D_(j+1) = mix64(mix64(D_j + G*(j+1)) + ((route_j << 32) | hit_j)),
+ * over the replica's queries j = 0, 1, ... in stream order, where route_j is
+ * the routed worker, hit_j = h of the routed worker (as uint32), G =
+ * 0x9E3779B97F4A7C15 and mix64 the SplitMix64 finaliser (z ^= z >> 30;
+ * z *= 0xBF58476D1CE4E5B9; z ^= z >> 27; z *= 0x94D049BB133111EB;
+ * z ^= z >> 31), all modulo 2^64: two runs route identically exactly when
+ * the chains agree (up to hash collisions). */
+typedef struct kvr_replica_stats {
+  uint64_t queries;       /* queries routed for this replica                         */
+  uint64_t route_digest;  /* D_queries                                               */
+  uint64_t prompt_tokens, hit_tokens, matched_tokens; /* sums over the workers      */
+  uint64_t loads, evictions, completions;
+  uint64_t latency_sum_us, latency_max_us; /* observed-latency model (sum, maximum) */
+  int64_t last_arrival_us;               /* arrival time of the last query routed   */
+  uint64_t phase_ticks[KVR_PHASES];      /* phase_timers = 1: ticks per part, else 0 */
+} kvr_replica_stats;
+
 typedef struct kvr_ctx kvr_ctx;
 
 /* Fill *cfg with the paper's constants (App. A) and the defaults above for
@@ -179,8 +218,11 @@ kvr_status kvr_workspace_size(const kvr_config* cfg, size_t* bytes);
 
 /* Lay the replicas out in d_workspace (>= kvr_workspace_size bytes, caller
  * owned, any content) and initialise them on hip_stream (a hipStream_t, or
- * NULL): empty caches, phase 1, zero loads and models.  On success *out is a
- * new context (free with kvr_destroy).  Asynchronous. */
+ * NULL) in the initial state of Sec. 3.1 (Table 1): every cache S_i empty,
+ * every load P_i = 0; for RLT the marking set of Algorithm 1 empty (T = {},
+ * phase 1); for LBGR (Algorithm 2) the load estimate and residual model at
+ * 0 and no pending completion.  On success *out is a new context (free with
+ * kvr_destroy).  Asynchronous. */
 kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t bytes,
                              void* hip_stream, kvr_ctx** out);
 
@@ -198,11 +240,17 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens,
                            const uint16_t* d_out_len, int32_t* d_route, int32_t* d_hits,
                            int32_t* d_all_hits);
 
-/* Synchronise the stream and copy the state of every (replica, worker) into
- * h_out[r*W + i], host memory with room for h_count entries: KVR_EINVAL,
- * with nothing written, when h_count < R*W.  Returns the device status as
- * kvr_check does (the entries are written also when it is an error). */
-kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out, size_t h_count);
+/* Synchronise the stream and report the metrics of Sec. 5 (hit tokens,
+ * prompt tokens, observed latency, evictions, loads) with the state they
+ * come from: h_replicas[r] (host memory, room for replica_count entries)
+ * receives replica r's kvr_replica_stats, h_workers[r*W + i] (room for
+ * worker_count entries) worker i's kvr_worker_stats, including the
+ * path-hash digest of its cache.  Either pointer may be NULL (that part is
+ * skipped).  KVR_EINVAL, with nothing written, when a non-NULL buffer holds
+ * fewer than R (resp. R*W) entries.  Returns the device status as kvr_check
+ * does (the entries are written also when it is an error). */
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica_count,
+                     kvr_worker_stats* h_workers, size_t worker_count);
 
 /* Synchronise the stream and return the sticky device status as a
  * kvr_status; *h_bits (optional) receives the raw KVR_DEV_* bits. */

@@ -21,7 +21,9 @@ STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVIC
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 6
+KVR_ABI_VERSION = 7
+KVR_PHASES = 8
+PHASE_NAMES = ["route", "stage_wait", "mark", "load", "evict", "finish", "match", "join"]
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
@@ -60,6 +62,8 @@ class KvrConfig(ctypes.Structure):
         ("batch_size", ctypes.c_int32),
         ("router_tree", ctypes.c_int32),
         ("router_tree_tokens", ctypes.c_uint32),
+        ("phase_timers", ctypes.c_int32),
+        ("pad1", ctypes.c_uint32),
     ]
 
 
@@ -78,6 +82,15 @@ class KvrWorkerStats(ctypes.Structure):
                    ("load_est", ctypes.c_double), ("theta", ctypes.c_double * 4),
                    ("nodes", ctypes.c_uint64), ("gc_runs", ctypes.c_uint64)]
                 + [(n, ctypes.c_uint64) for n in ROUTER_U64])
+
+
+REPLICA_U64 = ["queries", "route_digest", "prompt_tokens", "hit_tokens", "matched_tokens", "loads",
+               "evictions", "completions", "latency_sum_us", "latency_max_us"]
+
+
+class KvrReplicaStats(ctypes.Structure):
+    _fields_ = ([(n, ctypes.c_uint64) for n in REPLICA_U64]
+                + [("last_arrival_us", ctypes.c_int64), ("phase_ticks", ctypes.c_uint64 * KVR_PHASES)])
 
 
 class KvrError(RuntimeError):
@@ -112,7 +125,8 @@ def load_library() -> ctypes.CDLL:
     lib.kvr_route_batch.restype = ctypes.c_int
     lib.kvr_route_batch.argtypes = [vp, u32, vp, vp, vp, vp, vp, vp, vp]
     lib.kvr_stats.restype = ctypes.c_int
-    lib.kvr_stats.argtypes = [vp, ctypes.POINTER(KvrWorkerStats), ctypes.c_size_t]
+    lib.kvr_stats.argtypes = [vp, ctypes.POINTER(KvrReplicaStats), ctypes.c_size_t,
+                              ctypes.POINTER(KvrWorkerStats), ctypes.c_size_t]
     lib.kvr_check.restype = ctypes.c_int
     lib.kvr_check.argtypes = [vp, ctypes.POINTER(u32)]
     lib.kvr_queries_done.restype = u64
@@ -184,13 +198,30 @@ def _stats_dicts(arr, n: int) -> List[Dict]:
     return out
 
 
-def kvr_stats(ctx: int, R: int, W: int, check: bool = True) -> List[List[Dict]]:
+def _replica_dicts(arr, n: int) -> List[Dict]:
+    out = []
+    for k in range(n):
+        s = arr[k]
+        d = {name: int(getattr(s, name)) for name in REPLICA_U64}
+        d["last_arrival_us"] = int(s.last_arrival_us)
+        d["phase_ticks"] = [int(x) for x in s.phase_ticks]
+        out.append(d)
+    return out
+
+
+def kvr_stats(ctx: int, R: int, W: int, check: bool = True, with_replicas: bool = False):
+    """Per-worker records as [R][W] dicts; with ``with_replicas`` also the
+    per-replica records: (replicas [R], workers [R][W])."""
     arr = (KvrWorkerStats * (R * W))()
-    st = load_library().kvr_stats(ctypes.c_void_p(ctx), arr, R * W)
+    rep = (KvrReplicaStats * R)() if with_replicas else None
+    st = load_library().kvr_stats(ctypes.c_void_p(ctx), rep, R if with_replicas else 0, arr, R * W)
     if check:
         _check(st, "kvr_stats")
     flat = _stats_dicts(arr, R * W)
-    return [flat[r * W:(r + 1) * W] for r in range(R)]
+    workers = [flat[r * W:(r + 1) * W] for r in range(R)]
+    if with_replicas:
+        return _replica_dicts(rep, R), workers
+    return workers
 
 
 def kvr_check(ctx: int) -> (int, int):

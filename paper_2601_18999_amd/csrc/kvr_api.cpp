@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <string>
 
@@ -82,6 +83,9 @@ kvr_status validate(const kvr_config* c) {
     return fail(KVR_EINVAL, "router tree too large for 32-bit arena offsets");
   if (c->update != KVR_UPD_NLMS && c->update != KVR_UPD_RLS && c->update != KVR_UPD_NONE)
     return fail(KVR_EINVAL, "unknown update rule");
+  if (c->phase_timers != 0 && c->phase_timers != 1) return fail(KVR_EINVAL, "phase_timers must be 0 or 1");
+  if (c->phase_timers && (c->evict != KVR_EVICT_RLT || c->router_tree || c->batch_size != 1))
+    return fail(KVR_EINVAL, "phase_timers needs RLT eviction, no router tree and batch_size 1");
   if (c->pending_capacity < 1 || c->pending_capacity > (1u << 28))
     return fail(KVR_EINVAL, "pending_capacity must be in 1..2^28");
   if (c->node_capacity != 0 && (c->node_capacity < 2 || c->node_capacity > (1u << 30)))
@@ -150,6 +154,8 @@ void kvr_config_default(kvr_config* c, uint32_t R, uint32_t W, uint32_t B, uint3
   c->batch_size = 1;
   c->router_tree = 0;
   c->router_tree_tokens = 0;
+  c->phase_timers = 0;
+  c->pad1 = 0;
   c->update = KVR_UPD_NLMS;
   c->pending_capacity = 65536;
   c->node_capacity = 0;
@@ -240,7 +246,7 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
   c->C.ca_balance_rel = cfg->ca_balance_rel;
   c->C.ca_cache_threshold = cfg->ca_cache_threshold;
   c->C.cache_responses = cfg->cache_responses;
-  c->C.pad = 0;
+  c->C.phase_timers = cfg->phase_timers;
   c->ws = static_cast<char*>(d_workspace);
   c->stream = static_cast<hipStream_t>(hip_stream);
   c->device = dev;
@@ -310,21 +316,58 @@ kvr_status kvr_check(kvr_ctx* ctx, uint32_t* h_bits) {
   return KVR_OK;
 }
 
-kvr_status kvr_stats(kvr_ctx* ctx, kvr_worker_stats* h_out, size_t h_count) {
+kvr_status kvr_stats(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica_count,
+                     kvr_worker_stats* h_workers, size_t worker_count) {
   if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
-  if (!h_out) return fail(KVR_EINVAL, "h_out is NULL");
-  if (h_count < (size_t)ctx->L.R * ctx->L.W)
-    return fail(KVR_EINVAL, "h_out holds " + std::to_string(h_count) + " entries, the context has " +
-                                std::to_string((size_t)ctx->L.R * ctx->L.W));
+  const size_t R = ctx->L.R, RW = (size_t)ctx->L.R * ctx->L.W;
+  if (h_replicas && replica_count < R)
+    return fail(KVR_EINVAL, "h_replicas holds " + std::to_string(replica_count) + " entries, the context has " +
+                                std::to_string(R) + " replicas");
+  if (h_workers && worker_count < RW)
+    return fail(KVR_EINVAL, "h_workers holds " + std::to_string(worker_count) + " entries, the context has " +
+                                std::to_string(RW));
   uint32_t bits = 0;
   kvr_status st = kvr_check(ctx, &bits);
+  // the per-worker records are needed for the replica sums too
   hipError_t e = kvr::launch_stats(ctx->ws, ctx->L, ctx->stream);
   if (e != hipSuccess) return fail_hip(e, "stats kernel launch");
   e = hipStreamSynchronize(ctx->stream);
   if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
-  const size_t n = (size_t)ctx->L.R * ctx->L.W;
-  e = hipMemcpy(h_out, ctx->ws + ctx->L.off_stats, n * sizeof(kvr_worker_stats), hipMemcpyDeviceToHost);
+  kvr_worker_stats* ws = h_workers;
+  std::unique_ptr<kvr_worker_stats[]> own;
+  if (!ws) {
+    own.reset(new (std::nothrow) kvr_worker_stats[RW]);
+    if (!own) return fail(KVR_ENOMEM, "host allocation failed");
+    ws = own.get();
+  }
+  e = hipMemcpy(ws, ctx->ws + ctx->L.off_stats, RW * sizeof(kvr_worker_stats), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return fail_hip(e, "hipMemcpy(stats)");
+  if (h_replicas) {
+    std::unique_ptr<kvr::ReplicaHdr[]> rh(new (std::nothrow) kvr::ReplicaHdr[R]);
+    if (!rh) return fail(KVR_ENOMEM, "host allocation failed");
+    e = hipMemcpy(rh.get(), ctx->ws + ctx->L.off_rhdr, R * sizeof(kvr::ReplicaHdr), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy(replica headers)");
+    for (size_t r = 0; r < R; ++r) {
+      kvr_replica_stats o;
+      std::memset(&o, 0, sizeof(o));
+      o.queries = rh[r].queries;
+      o.route_digest = rh[r].route_digest;
+      o.last_arrival_us = rh[r].tprev;
+      for (int k = 0; k < KVR_PHASES; ++k) o.phase_ticks[k] = rh[r].phase_ticks[k];
+      for (size_t i = 0; i < ctx->L.W; ++i) {
+        const kvr_worker_stats& w = ws[r * ctx->L.W + i];
+        o.prompt_tokens += w.prompt_tokens;
+        o.hit_tokens += w.hit_tokens;
+        o.matched_tokens += w.matched_tokens;
+        o.loads += w.loads;
+        o.evictions += w.evictions;
+        o.completions += w.completions;
+        o.latency_sum_us += w.latency_sum_us;
+        if (w.latency_max_us > o.latency_max_us) o.latency_max_us = w.latency_max_us;
+      }
+      h_replicas[r] = o;
+    }
+  }
   if (st != KVR_OK) return fail(st, describe_bits(bits));
   return KVR_OK;
 }

@@ -110,6 +110,14 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
+// One link of a replica's route digest: D' = mix64(mix64(D + G*(j+1)) +
+// ((route << 32) | hit)), so the chain over the queries in order changes
+// with any routing decision or routed hit.
+__device__ __forceinline__ uint64_t route_chain(uint64_t d, uint64_t jg, uint32_t route, int32_t hit) {
+  d = mix64(d + 0x9E3779B97F4A7C15ull * (jg + 1ull));
+  return mix64(d + (((uint64_t)route << 32) | (uint64_t)(uint32_t)hit));
+}
+
 // rho^k, square-and-multiply from the least significant bit
 __device__ double pow_int(double rho, uint64_t k) {
   double res = 1.0, b = rho;
@@ -2372,69 +2380,161 @@ __device__ void init_worker(const Ptrs& P, double rls_p0) {
   P.nodes[0] = root;
 }
 
-// Final state of one worker with the path-hash digest of the cached tokens
-// H(v) = mix64(H(parent) + G*(tok+1)), H(root) = 0, over a depth-first walk
-// (one thread; P.scratch holds the stack of (node, start hash) pairs).
-__device__ void worker_stats(const Ptrs& P, kvr_worker_stats* out) {
+// Wave sums and exclusive-or of 64-bit values (butterfly over the lanes).
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  for (int o = 1; o < KVR_WAVE; o <<= 1) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, KVR_WAVE);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, KVR_WAVE);
+    v += ((uint64_t)hi << 32) | lo;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_xor_u64(uint64_t v) {
+  for (int o = 1; o < KVR_WAVE; o <<= 1) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, KVR_WAVE);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, KVR_WAVE);
+    v ^= ((uint64_t)hi << 32) | lo;
+  }
+  return v;
+}
+
+// Final state of one worker (whole wave), with the path-hash digest of the
+// cached tokens H(v) = mix64(H(parent) + G*(tok+1)), H(root) = 0.  A
+// token's hash needs its parent's, so the tree is walked top-down: P.scratch
+// holds a FIFO of (node, hash before its edge), starting with the root.  An
+// idle lane takes the next queued node, hashes its edge 16 tokens per round
+// (the loads of a round in flight together) and, at the edge's end, appends
+// the node's children with the edge's last hash.  Long and short edges so
+// share the wave.  Returns false on an inconsistent tree (the counts are
+// then partial).
+__device__ bool worker_stats(const Ptrs& P, kvr_worker_stats* out) {
+  constexpr int kTok = 16;
   const WorkerHdr* h = P.hdr;
-  St s = load_st(h);
+  const St s = load_st(h);
   const int32_t* ar = arena_of(P, s.arena_sel);
+  uint64_t* q = P.scratch;  // entry e: q[2e] = node, q[2e + 1] = hash before its edge
+  const uint64_t cap = P.NC;
   uint64_t count = 0, dsum = 0, dxor = 0, mcount = 0, msum = 0;
-  uint64_t* stack = P.scratch;
-  uint64_t sp = 1;
-  stack[0] = 0;
-  stack[1] = 0;
-  for (uint64_t pops = 0; sp > 0 && pops <= s.hwm; ++pops) {
-    sp -= 1;
-    const int32_t x = (int32_t)stack[2 * sp];
-    if (x < 0 || (uint32_t)x >= s.hwm) break;
-    uint64_t hx = stack[2 * sp + 1];
-    const NodeRec nd = P.nodes[x];
-    for (int32_t k = 0; k < nd.len; ++k) {
-      const int32_t tok = ar[nd.off + (uint32_t)k];
-      hx = mix64(hx + 0x9E3779B97F4A7C15ull * (uint64_t)(int64_t)(tok + 1));
-      count += 1;
-      dsum += hx;
-      dxor ^= hx;
-      if (is_marked(s, nd, x, k)) {
-        mcount += 1;
-        msum += hx;
+  if (lane_id() == 0) {
+    q[0] = 0;
+    q[1] = 0;
+  }
+  wave_mem_sync();
+  uint64_t head = 0, tail = 1;  // wave-uniform
+  int32_t x = -1, k = 0;
+  uint64_t hx = 0;
+  NodeRec nd;
+  nd.parent = nd.len = nd.nchild = nd.ccap = nd.ma = 0;
+  nd.off = nd.coff = nd.mphase = 0;
+  bool bad = false, done = false;
+  const uint64_t bound = (uint64_t)s.hwm + (uint64_t)s.size + 2u;
+  for (uint64_t it = 0; it < bound; ++it) {
+    // idle lanes take queued nodes, in lane order
+    const uint64_t idle = __ballot(x < 0);
+    const uint64_t avail = tail - head;
+    if (x < 0) {
+      const uint64_t rank = (uint64_t)__popcll(idle & lanemask_lt());
+      if (rank < avail) {
+        const uint64_t e = head + rank;
+        const uint64_t id = q[2 * e];
+        hx = q[2 * e + 1];
+        k = 0;
+        if (id < (uint64_t)s.hwm && id < (uint64_t)P.NC) {
+          nd = P.nodes[id];
+          x = (int32_t)id;
+          if (nd.parent == -2 || nd.len < 0 || (uint64_t)nd.off + (uint64_t)nd.len > P.A || nd.nchild < 0 ||
+              (nd.nchild > 0 && (uint64_t)nd.coff + 2ull * (uint64_t)nd.nchild > P.A)) {
+            bad = true;
+            x = -1;
+          }
+        } else {
+          bad = true;
+        }
       }
     }
-    for (int32_t c = 0; c < nd.nchild && sp < P.NC; ++c) {
-      stack[2 * sp] = (uint64_t)(uint32_t)ar[nd.coff + 2 * c + 1];
-      stack[2 * sp + 1] = hx;
-      sp += 1;
+    const uint64_t nidle = (uint64_t)__popcll(idle);
+    head += nidle < avail ? nidle : avail;
+    if (__ballot(bad)) break;
+    if (!__ballot(x >= 0)) {
+      done = true;
+      break;
     }
+    if (x >= 0) {
+      int32_t t[kTok];
+#pragma unroll
+      for (int c = 0; c < kTok; ++c) t[c] = k + c < nd.len ? ar[nd.off + (uint32_t)(k + c)] : 0;
+#pragma unroll
+      for (int c = 0; c < kTok; ++c) {
+        if (k + c < nd.len) {
+          hx = mix64(hx + 0x9E3779B97F4A7C15ull * (uint64_t)(int64_t)(t[c] + 1));
+          count += 1;
+          dsum += hx;
+          dxor ^= hx;
+          if (is_marked(s, nd, x, k + c)) {
+            mcount += 1;
+            msum += hx;
+          }
+        }
+      }
+      k += kTok;
+    }
+    // lanes at the end of their edge queue its children
+    const bool fin = x >= 0 && k >= nd.len;
+    const uint32_t nc = fin ? (uint32_t)nd.nchild : 0u;
+    const uint32_t incl = wave_inclusive_sum(nc);
+    const uint64_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, KVR_WAVE - 1);
+    if (tail + total > cap) {
+      bad = true;
+      break;
+    }
+    if (fin) {
+      const uint64_t e0 = tail + incl - nc;
+      for (uint32_t c = 0; c < nc; ++c) {
+        q[2 * (e0 + c)] = (uint64_t)(uint32_t)ar[nd.coff + 2u * c + 1u];
+        q[2 * (e0 + c) + 1] = hx;
+      }
+      x = -1;
+    }
+    tail += total;
+    wave_mem_sync();  // the queued entries before other lanes read them
   }
-  kvr_worker_stats o;
-  o.routed = h->routed;
-  o.prompt_tokens = h->prompt_tokens;
-  o.hit_tokens = h->hit_tokens;
-  o.matched_tokens = h->matched_tokens;
-  o.loads = h->loads;
-  o.evictions = h->evictions;
-  o.phase = h->phase;
-  o.cnt = h->cnt;
-  o.forced_resets = h->forced_resets;
-  o.resident = count;
-  o.digest_sum = dsum;
-  o.digest_xor = dxor;
-  o.marked_count = mcount;
-  o.marked_sum = msum;
-  o.completions = h->completions;
-  o.pending_depth = h->pend_count;
-  o.pending_max = h->pending_max;
-  o.latency_sum_us = h->lat_sum_us;
-  o.latency_max_us = h->lat_max_us;
-  o.backlog_us = h->Wb;
-  o.last_decay_us = h->tl;
-  o.load_est = h->P;
-  for (int a = 0; a < 4; ++a) o.theta[a] = h->theta[a];
-  o.nodes = h->nnodes;
-  o.gc_runs = h->gc_runs;
-  o.router_resident = o.router_digest_sum = o.router_digest_xor = o.router_evictions = 0;
-  *out = o;
+  count = wave_sum_u64(count);
+  dsum = wave_sum_u64(dsum);
+  dxor = wave_xor_u64(dxor);
+  mcount = wave_sum_u64(mcount);
+  msum = wave_sum_u64(msum);
+  if (lane_id() == 0) {
+    kvr_worker_stats o;
+    o.routed = h->routed;
+    o.prompt_tokens = h->prompt_tokens;
+    o.hit_tokens = h->hit_tokens;
+    o.matched_tokens = h->matched_tokens;
+    o.loads = h->loads;
+    o.evictions = h->evictions;
+    o.phase = h->phase;
+    o.cnt = h->cnt;
+    o.forced_resets = h->forced_resets;
+    o.resident = count;
+    o.digest_sum = dsum;
+    o.digest_xor = dxor;
+    o.marked_count = mcount;
+    o.marked_sum = msum;
+    o.completions = h->completions;
+    o.pending_depth = h->pend_count;
+    o.pending_max = h->pending_max;
+    o.latency_sum_us = h->lat_sum_us;
+    o.latency_max_us = h->lat_max_us;
+    o.backlog_us = h->Wb;
+    o.last_decay_us = h->tl;
+    o.load_est = h->P;
+    for (int a = 0; a < 4; ++a) o.theta[a] = h->theta[a];
+    o.nodes = h->nnodes;
+    o.gc_runs = h->gc_runs;
+    o.router_resident = o.router_digest_sum = o.router_digest_xor = o.router_evictions = 0;
+    *out = o;
+  }
+  return done && !bad;
 }
 
 }  // namespace kvr

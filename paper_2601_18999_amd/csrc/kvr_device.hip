@@ -319,6 +319,12 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   }
   __syncthreads();
   if (abort_sh) return;
+  // the replica's route digest and query count, kept by the routing wave
+  uint64_t chain = 0, routed = 0;
+  if (wave == 0) {
+    chain = rh->route_digest;
+    routed = rh->queries;
+  }
 
   // query 0: stage its path; completions and decay at its arrival; full
   // matches of its prompt
@@ -394,6 +400,10 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         const uint64_t orow = (uint64_t)r * a.n + k;
         if (a.route) a.route[orow] = (int32_t)best;
         if (a.hits) a.hits[orow] = hb;
+        if (!err) {
+          chain = route_chain(chain, a.j0 + k, best, hb);
+          routed += 1;
+        }
         // draws this insertion will take: one per token loaded into a full cache
         const uint32_t nload = (uint32_t)(Lp - hins);
         const uint32_t nfree = a.L.B - size;
@@ -524,9 +534,13 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     __syncthreads();
     if (abort_sh) break;
   }
-  if (threadIdx.x == 0 && !abort_sh && a.n > 0) {
-    rh->tprev = a.arrival[a.n - 1];
-    if (r == 0) g->last_arrival = a.arrival[a.n - 1];
+  if (threadIdx.x == 0) {
+    rh->route_digest = chain;
+    rh->queries = routed;
+    if (!abort_sh && a.n > 0) {
+      rh->tprev = a.arrival[a.n - 1];
+      if (r == 0) g->last_arrival = a.arrival[a.n - 1];
+    }
   }
 }
 
@@ -549,7 +563,15 @@ __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
     g->err_query = 0;
     g->err_val[0] = g->err_val[1] = g->err_val[2] = 0;
   }
-  if (tid < L.R) reinterpret_cast<ReplicaHdr*>(ws + L.off_rhdr)[tid].tprev = 0;
+  if (tid < L.R) {
+    ReplicaHdr h;
+    h.tprev = 0;
+    h.queries = 0;
+    h.route_digest = 0;
+    for (int k = 0; k < KVR_PHASES; ++k) h.phase_ticks[k] = 0;
+    for (int k = 0; k < 5; ++k) h.pad[k] = 0;
+    reinterpret_cast<ReplicaHdr*>(ws + L.off_rhdr)[tid] = h;
+  }
   if (tid < RW) {
     init_worker(worker_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
     if (L.has_router) init_worker(router_ptrs(ws, L, (uint32_t)(tid / L.W), (uint32_t)(tid % L.W)), rls_p0);
@@ -586,25 +608,28 @@ __global__ void validate_tokens_kernel(char* ws, Layout L, const int32_t* tokens
   if (__ballot(bad != 0) && lane_id() == 0) atomicOr(&g->status, (uint32_t)KVR_DEV_BAD_TOKEN);
 }
 
-// Final state of every (replica, worker).
-__global__ void stats_kernel(char* ws, Layout L) {
+// Final state of every (replica, worker): one wave each.  An inconsistent
+// tree (the digest walk could not finish) raises KVR_DEV_INTERNAL.
+__global__ void __launch_bounds__(64) stats_kernel(char* ws, Layout L) {
   const uint64_t widx = blockIdx.x;
-  if (threadIdx.x != 0) return;
   const uint32_t r = (uint32_t)(widx / L.W), i = (uint32_t)(widx % L.W);
-  kvr_worker_stats o;
-  worker_stats(worker_ptrs(ws, L, r, i), &o);
-  o.router_resident = o.router_digest_sum = o.router_digest_xor = o.router_evictions = 0;
+  kvr_worker_stats* out = reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats) + widx;
+  bool ok = worker_stats(worker_ptrs(ws, L, r, i), out);
   if (L.has_router) {
-    // the router's tree of the worker: contents digest and evictions
+    // the router's tree of the worker (its walk reuses the worker's scratch
+    // once the cache's is done): contents digest and evictions
+    wave_mem_sync();
     Ptrs Pr = router_ptrs(ws, L, r, i);
     kvr_worker_stats t;
-    worker_stats(Pr, &t);
-    o.router_resident = t.resident;
-    o.router_digest_sum = t.digest_sum;
-    o.router_digest_xor = t.digest_xor;
-    o.router_evictions = Pr.hdr->evictions;
+    ok = worker_stats(Pr, &t) && ok;
+    if (lane_id() == 0) {
+      out->router_resident = t.resident;
+      out->router_digest_sum = t.digest_sum;
+      out->router_digest_xor = t.digest_xor;
+      out->router_evictions = Pr.hdr->evictions;
+    }
   }
-  reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats)[widx] = o;
+  if (!ok && lane_id() == 0) atomicOr(&reinterpret_cast<GlobalHdr*>(ws + L.off_global)->status, (uint32_t)KVR_DEV_INTERNAL);
 }
 
 // ---------------------------------------------------------------- launchers (host)

@@ -97,9 +97,13 @@ struct WorkerHdr {
 static_assert(sizeof(WorkerHdr) == 512, "worker header is 512 bytes");
 
 struct ReplicaHdr {
-  int64_t tprev;
-  int64_t pad[7];
+  int64_t tprev;          // arrival time of the replica's last query
+  uint64_t queries;       // queries routed
+  uint64_t route_digest;  // hash chain over (query index, route, hit), kvr_replica_stats
+  uint64_t phase_ticks[KVR_PHASES];
+  uint64_t pad[5];
 };
+static_assert(sizeof(ReplicaHdr) == 128, "replica header is 128 bytes");
 
 struct GlobalHdr {
   uint32_t status;       // KVR_DEV_* bits, sticky
@@ -140,7 +144,7 @@ struct Consts {
   int32_t ca_balance_abs;
   double ca_balance_rel, ca_cache_threshold;
   int32_t cache_responses;  // 1: a path is prompt || response (the last out_len tokens)
-  int32_t pad;
+  int32_t phase_timers;     // 1: accumulate the routing wave's ticks per part of a step
 };
 
 // Arguments of one batch for the step kernel (device pointers).

@@ -90,6 +90,10 @@ class Simulator:
     def stats(self, check: bool = True):
         return kvr_stats(self.ctx, self.R, self.W, check=check)
 
+    def replica_stats(self, check: bool = True):
+        """(per-replica records [R], per-worker records [R][W])."""
+        return kvr_stats(self.ctx, self.R, self.W, check=check, with_replicas=True)
+
     def check(self):
         return kvr_check(self.ctx)
 

@@ -239,11 +239,11 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   for (uint32_t r = 0; r < L.R; ++r)
     for (uint32_t i = 0; i < W; ++i) {
       kvr_worker_stats* o = out + (uint64_t)r * W + i;
-      worker_stats(worker_ptrs(ws, L, r, i), o);
+      if (!worker_stats(worker_ptrs(ws, L, r, i), o)) return -7;  // the digest walk could not finish
       if (rtree) {
         Ptrs Pr = router_ptrs(ws, L, r, i);
         kvr_worker_stats t;
-        worker_stats(Pr, &t);
+        if (!worker_stats(Pr, &t)) return -7;
         o->router_resident = t.resident;
         o->router_digest_sum = t.digest_sum;
         o->router_digest_xor = t.digest_xor;

@@ -75,7 +75,7 @@ def test_workspace_size_grows_with_every_dimension():
 def test_null_context_and_arguments():
     lib = K.load_library()
     assert lib.kvr_route_batch(None, 1, None, None, None, None, None, None, None) == K.KVR_EINVAL
-    assert lib.kvr_stats(None, None, 0) == K.KVR_EINVAL
+    assert lib.kvr_stats(None, None, 0, None, 0) == K.KVR_EINVAL
     assert lib.kvr_check(None, None) == K.KVR_EINVAL
     assert lib.kvr_queries_done(None) == 0
     lib.kvr_destroy(None)
@@ -101,7 +101,8 @@ def test_binding_structs_match_the_header(tmp_path):
     if cc is None:
         pytest.skip("no C compiler")
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "kvr.h"', "int main(void) {"]
-    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats)):
+    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats),
+                       ("kvr_replica_stats", K.KvrReplicaStats)):
         lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
         for f, _ in cls._fields_:
             lines.append(f'  printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
@@ -112,7 +113,8 @@ def test_binding_structs_match_the_header(tmp_path):
     subprocess.run([cc, "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
     out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
     got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
-    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats)):
+    for cname, cls in (("kvr_config", K.KvrConfig), ("kvr_worker_stats", K.KvrWorkerStats),
+                       ("kvr_replica_stats", K.KvrReplicaStats)):
         assert got[(cname, "size")] == ctypes.sizeof(cls), cname
         for f, _ in cls._fields_:
             assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)

@@ -177,7 +177,13 @@ def test_invalid_batches_are_rejected_before_any_state_change():
         assert st == K.KVR_EINVAL, (kind, st, bits)
         # a stats buffer one entry short is refused before anything is written
         short = (K.KvrWorkerStats * (sim.R * sim.W))()
-        assert K.load_library().kvr_stats(ctypes.c_void_p(sim.ctx), short, sim.R * sim.W - 1) == K.KVR_EINVAL
+        assert K.load_library().kvr_stats(ctypes.c_void_p(sim.ctx), None, 0, short,
+                                          sim.R * sim.W - 1) == K.KVR_EINVAL
+        assert all(short[i].routed == 0 for i in range(sim.R * sim.W))
+        rshort = (K.KvrReplicaStats * sim.R)()
+        assert K.load_library().kvr_stats(ctypes.c_void_p(sim.ctx), rshort, sim.R - 1, short,
+                                          sim.R * sim.W) == K.KVR_EINVAL
+        assert all(rshort[i].queries == 0 for i in range(sim.R))
         assert all(short[i].routed == 0 for i in range(sim.R * sim.W))
         after = sim.stats(check=False)
         assert before == after, kind
