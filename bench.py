@@ -207,6 +207,9 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="CPU seconds per oracle thread on the timed window")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--phase-timers", action="store_true",
+                    help="build the step kernel with per-part timers of the routing wave and report the "
+                         "microseconds per query and replica of each part over the timed window")
     ap.add_argument("--no-whole", action="store_true",
                     help="stop after the timed window instead of routing the rest of the stream")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -245,7 +248,8 @@ def main() -> int:
               "cache_aware": K.KVR_ROUTE_CACHE_AWARE}[args.router]
     sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router,
                       cache_responses=int(args.responses), batch_size=args.beta,
-                      router_tree=int(args.router_tree), router_tree_tokens=args.router_tree_tokens)
+                      router_tree=int(args.router_tree), router_tree_tokens=args.router_tree_tokens,
+                      phase_timers=int(args.phase_timers))
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -267,7 +271,8 @@ def main() -> int:
         run_batch(k)
         torch.cuda.synchronize()
         log(f"warmup batch {k + 1}/{args.warmup} done")
-    before = totals(sim.stats())
+    reps0, ws0 = sim.replica_stats()
+    before = totals(ws0)
     q0 = args.warmup * args.batch
     q = q0
     torch.cuda.synchronize()
@@ -283,7 +288,8 @@ def main() -> int:
     if st != K.KVR_OK:
         print(f"device status {st} bits {bits}: {K.kvr_last_error()}", file=sys.stderr)
         return 1
-    after = totals(sim.stats())
+    reps1, ws1 = sim.replica_stats()
+    after = totals(ws1)
     d = {k: after[k] - before[k] for k in after}
     kernel_ms = sum(ev[k][0].elapsed_time(ev[k][1]) for k in range(args.warmup, args.warmup + args.steps))
     nq = R * (q - q0)
@@ -337,6 +343,12 @@ def main() -> int:
                      "measured_frac": traffic["bytes_per_launch"] / launch_s / 1e9 / HBM_PEAK_GBS
                      if traffic else None},
     }
+    if args.phase_timers:
+        # 100 MHz ticks summed over the replicas' routing waves
+        ticks = [sum(b["phase_ticks"][p] - a["phase_ticks"][p] for a, b in zip(reps0, reps1))
+                 for p in range(K.KVR_PHASES)]
+        line["phase_us_per_query"] = {name: t * 0.01 / nq for name, t in zip(K.PHASE_NAMES, ticks)}
+        line["phase_us_per_query"]["total"] = sum(ticks) * 0.01 / nq
     if not args.no_whole:
         for k in range(args.warmup + args.steps, nb):
             run_batch(k)

@@ -22,8 +22,9 @@ KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
 KVR_ABI_VERSION = 7
-KVR_PHASES = 8
-PHASE_NAMES = ["route", "stage_wait", "mark", "load", "evict", "finish", "match", "join"]
+KVR_PHASES = 17
+PHASE_NAMES = ["route", "stage_wait", "mark", "load", "evict", "finish", "match", "join", "evictor_wait",
+               "e_evict", "e_finish", "e_idle", "h_stage", "h_wait", "h_draw", "h_other", "h_match"]
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]

@@ -22,6 +22,7 @@ hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st);
 hipError_t set_step_lds_limit(size_t bytes);
 hipError_t step_static_lds(size_t* bytes);
 size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, uint32_t path_sets);
+size_t step_lds_bytes_pipe(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap);
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -34,6 +35,9 @@ struct kvr_ctx {
   uint32_t seen_bits;  // device status bits already reported to the host
   uint32_t ucap;       // candidate entries the step kernel stages in LDS
   uint32_t rcap;       // draw words the step kernel precomputes in LDS
+  uint32_t pipe;       // 1: the pipelined step kernel (a separate evicting wave)
+  uint32_t ucap_p;     // its staged candidates
+  uint32_t rcap_p;     // its draw words per insertion (two insertions' worth)
 };
 
 namespace {
@@ -225,8 +229,34 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
     e = kvr::set_step_lds_limit((size_t)lds_max - static_lds);
     if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
   }
+  // the pipelined kernel (RLT, prompts only, no router tree, single-query
+  // processing): the draw words of two insertions take 2/5 of the room
+  const bool pipe = cfg->evict == KVR_EVICT_RLT && !cfg->router_tree && cfg->batch_size == 1 && !cfg->cache_responses;
+  size_t rcap_p = 0, ucap_p = 0;
+  if (pipe) {
+    const size_t qb = kvr::step_lds_bytes_pipe(L.maxL, L.W, 0, 0);
+    if (qb + static_lds > (size_t)lds_max)
+      return fail(KVR_EINVAL, "max_query_tokens does not fit in LDS (" + std::to_string(lds_max) + " bytes)");
+    // (the candidate list is short on these workloads: 512 staged entries
+    // first, then the draw words of two whole insertions, then the rest)
+    size_t room_p = (size_t)lds_max - static_lds - qb;
+    const size_t ufirst = room_p >= 512u * 16u ? 512u * 16u : 0u;
+    rcap_p = (room_p - ufirst) / 8u;
+    if (rcap_p > L.maxL) rcap_p = L.maxL;
+    room_p -= rcap_p * 8u;
+    ucap_p = room_p / 16u;
+    if (ucap_p > 8192) ucap_p = 8192;
+    if (ucap_p < 64) ucap_p = 0;
+    if (kvr::step_lds_bytes_pipe(L.maxL, L.W, (uint32_t)ucap_p, (uint32_t)rcap_p) > 65536) {
+      e = kvr::set_step_lds_limit((size_t)lds_max - static_lds);
+      if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
+    }
+  }
   kvr_ctx* c = new (std::nothrow) kvr_ctx;
   if (!c) return fail(KVR_ENOMEM, "host allocation failed");
+  c->pipe = pipe ? 1u : 0u;
+  c->ucap_p = (uint32_t)ucap_p;
+  c->rcap_p = (uint32_t)rcap_p;
   c->L = L;
   c->C.seed = cfg->seed;
   c->C.alpha_cached = cfg->alpha_cached;
@@ -285,8 +315,10 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens, co
   a.hits = d_hits;
   a.all_hits = d_all_hits;
   a.n = n;
-  a.ucap = ctx->ucap;
-  a.rcap = ctx->rcap;
+  a.pipe = ctx->pipe;
+  a.pad2 = 0;
+  a.ucap = ctx->pipe ? ctx->ucap_p : ctx->ucap;
+  a.rcap = ctx->pipe ? ctx->rcap_p : ctx->rcap;
   a.j0 = ctx->queries_done;
   hipError_t e = kvr::launch_step(a, ctx->stream);
   if (e != hipSuccess) return fail_hip(e, "step kernel launch");

@@ -80,6 +80,31 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) { return wave_reduc
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) { return wave_reduce_u64<true>(v); }
 
+// ---------------------------------------------------------------- phase timers
+// Per-part timing of a step (phase_timers): ticks of the 100 MHz real-time
+// counter, accumulated in registers by the routing wave.  A no-op unless kOn.
+struct PhaseClock {
+  uint64_t t;
+  uint64_t acc[KVR_PHASES];
+};
+
+template <bool kOn>
+__device__ __forceinline__ void clock_start(PhaseClock* c) {
+  if constexpr (kOn) {
+    c->t = (uint64_t)wall_clock64();
+    for (int k = 0; k < KVR_PHASES; ++k) c->acc[k] = 0;
+  }
+}
+
+template <bool kOn>
+__device__ __forceinline__ void clock_mark(PhaseClock* c, int part) {
+  if constexpr (kOn) {
+    const uint64_t now = (uint64_t)wall_clock64();
+    c->acc[part] += now - c->t;
+    c->t = now;
+  }
+}
+
 // ---------------------------------------------------------------- Philox4x64-10
 // Salmon et al., SC'11: ten rounds, two 64x64->128 products per round, key
 // bumped by the Weyl increments between rounds.  Only word 0 is used.
@@ -367,6 +392,26 @@ __device__ void arr_erase(int32_t* a, uint32_t n, uint32_t pos) {
 // entries per round trip: most child arrays are short, and measured faster
 // than several chunks in flight.)
 __device__ int32_t child_find(const int32_t* ar, const NodeRec& nd, int32_t tok) {
+  if (nd.nchild > KVR_WAVE) {
+    // a wide node (the root of many prefix groups): four chunks per round trip
+    constexpr int kC = 4;
+    for (int32_t b = 0; b < nd.nchild; b += kC * KVR_WAVE) {
+      int2 e[kC];
+#pragma unroll
+      for (int u = 0; u < kC; ++u) {
+        const int32_t k = b + u * KVR_WAVE + lane_id();
+        e[u].x = e[u].y = -1;
+        if (k < nd.nchild) e[u] = *reinterpret_cast<const int2*>(ar + nd.coff + 2 * k);
+      }
+#pragma unroll
+      for (int u = 0; u < kC; ++u) {
+        const int32_t k = b + u * KVR_WAVE + lane_id();
+        const uint64_t m = __ballot(k < nd.nchild && e[u].x == tok);
+        if (m) return __builtin_amdgcn_readlane(e[u].y, first_lane(m));
+      }
+    }
+    return -1;
+  }
   for (int32_t b = 0; b < nd.nchild; b += KVR_WAVE) {
     int32_t k = b + lane_id();
     bool hit = false;
@@ -1308,12 +1353,36 @@ __device__ __forceinline__ NodeRec node_from_lane(const NodeRec& v, int e) {
   return r;
 }
 
-// RLT insertion of q[0, L) into the worker's cache; h = LCP(q, cache) and pr
-// holds the path of that match (or is marked unknown).  On return pr holds
-// the path of q in the updated cache.  Returns the KVR_DEV_* error bits (0
-// on success).
-__device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
-                               int32_t h, const UStage& ustage, const PathRef& pr, int64_t* dbg) {
+// The eviction half of an RLT insertion, as the front half leaves it: the
+// cache state after the marks of the cached part and the load of the new
+// leaf, and what the evictions of the loaded tokens need.  The front half
+// may run on one wave and the back half on another.
+struct EvictJob {
+  St s;
+  InsertArgs ia;
+  int32_t h, L;       // cached length and length of the inserted path
+  int32_t l;          // the new leaf node holding q[h, L) (when h < L)
+  uint32_t nfree;     // free token slots before the load
+  uint32_t nev;       // evictions the load needs
+  uint32_t c0;        // |T| before the loaded tokens were marked
+  int32_t reset_at;   // path position at which |T| reaches B+1 among the loads, or -1
+  uint32_t worker;
+  uint32_t final_size;  // |S| after the insertion
+};
+
+// Front half of the RLT insertion of q[0, L) into the worker's cache (h =
+// LCP(q, cache); pr holds the path of that match, or is marked unknown):
+// the marking walk over the cached part (Algorithm 1: each token joins T,
+// with the reset to {t} when |T| reaches B+1), the split of the edge the
+// match ends in, the new leaf's rank in the leaf list, and the load of
+// q[h, L) as one new leaf node.  pr then holds the path of q in the updated
+// cache, which the evictions never touch.  The evictions and the marks of
+// the loaded tokens are left in *job for rlt_insert_back.  Returns the
+// KVR_DEV_* error bits (0 on success).
+template <bool PT = false>
+__device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
+                                                     int32_t h, const PathRef& pr, int64_t* dbg, EvictJob& job,
+                                                     PhaseClock* clk = nullptr) {
   St s = load_st(P.hdr);
   const uint32_t B = ia.B;
   int32_t* ar = arena_of(P, s.arena_sel);
@@ -1431,6 +1500,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     x = c;
   }
   wave_mem_sync();  // the marks above are read again below
+  clock_mark<PT>(clk, KVR_PHASE_MARK);
 
   if (h < L) {
     const int32_t nload = L - h;
@@ -1509,17 +1579,77 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
       arr_insert(P.leaf, s.nleaves, (uint32_t)pos, l);
       s.nleaves += 1;
     }
+    clock_mark<PT>(clk, KVR_PHASE_LOAD);
 
-    // ---- loads, evictions and the phase reset of the missed part
-    const uint32_t nfree = B - s.size;
-    const uint32_t nev = (uint32_t)nload > nfree ? (uint32_t)nload - nfree : 0u;
-    const uint32_t c0 = s.cnt;
-    int32_t reset_at = (c0 + (uint32_t)nload >= B + 1u) ? h + (int32_t)(B - c0) : -1;
+    // ---- what the evictions of the loaded tokens need
+    job.nfree = B - s.size;
+    job.nev = (uint32_t)nload > job.nfree ? (uint32_t)nload - job.nfree : 0u;
+    job.c0 = s.cnt;
+    job.reset_at = (job.c0 + (uint32_t)nload >= B + 1u) ? h + (int32_t)(B - job.c0) : -1;
+    job.l = l;
+  } else {
+    job.nfree = B - s.size;
+    job.nev = 0;
+    job.c0 = s.cnt;
+    job.reset_at = -1;
+    job.l = 0;
+  }
+  // ---- the path of q in the updated cache: the walked entries (the split
+  // head in place of the split node) and the new leaf
+  {
+    int32_t fc = have_path ? pe : kPathMax + 1;
+    if (fc <= kPathMax) {
+      if (split) {
+        int32_t f1 = fc - 1;
+        path_add(pr, f1, a, laststart, laststart + lastcov);
+      }
+      if (h < L) path_add(pr, fc, l, h, L);
+    }
+    if (lane_id() == 0) *pr.cnt = fc;
+  }
+  job.s = s;
+  job.ia = ia;
+  job.h = h;
+  job.L = L;
+  job.worker = ia.worker;
+  job.final_size = s.size + (uint32_t)(L - h) - job.nev;
+  wave_mem_sync();  // the tree edits before the back half reads them (maybe on another wave)
+  return 0;
+fail:
+  if (lane_id() == 0) *pr.cnt = kPathMax + 1;
+  store_st(P.hdr, s);
+  if (dbg) {
+    dbg[0] = s.dbg_check;
+    dbg[1] = s.dbg_val[0];
+    dbg[2] = s.dbg_val[1];
+    dbg[3] = s.dbg_val[2];
+  }
+  return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
+
+// Back half of the RLT insertion (after rlt_insert_front, on the state in
+// *job): for each loaded token into a full cache, evict the candidate
+// U[floor(r * |U| / 2^64)] (Algorithm 1; U in lexicographic order; r the
+// draw's Philox word), in blocks of draws that commute; the phase reset
+// where |T| reaches B+1 among the loaded tokens; then the marks of the
+// loaded tokens and the cache header.  Returns the KVR_DEV_* error bits.
+template <bool PT = false>
+__device__ __forceinline__ uint32_t rlt_insert_back(const Ptrs& P, const EvictJob& job, const UStage& ustage,
+                                                    int64_t* dbg, PhaseClock* clk = nullptr,
+                                                    int ph_evict = KVR_PHASE_EVICT, int ph_finish = KVR_PHASE_FINISH) {
+  St s = job.s;
+  const int32_t h = job.h, L = job.L, l = job.l;
+  if (h < L) {
+    const int32_t nload = L - h;
+    const uint32_t nfree = job.nfree;
+    const uint32_t nev = job.nev;
+    const uint32_t c0 = job.c0;
+    int32_t reset_at = job.reset_at;
     bool applied = false;
     uint64_t dctr = 0;
     uint32_t k = 0;
     bool staged = false;
-    InsertArgs iq = ia;
+    InsertArgs iq = job.ia;
     // draw words [0, have) are known to be written; before a block reads
     // words past that, wait for the drawing waves' rounds to cover them
     // (bounded: past it the words are computed here instead)
@@ -1603,6 +1733,7 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
     // no fence: the insertion's last fence orders these stores before any
     // later read
     if (staged) stage_out(P, s, ustage, false);
+    clock_mark<PT>(clk, ph_evict);
     if (reset_at >= 0 && !applied) {
       s.phase += 1;
       s.U_valid = 0;
@@ -1635,22 +1766,9 @@ __device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& 
   }
   store_st(P.hdr, s);
   wave_mem_sync();
-  // ---- the path of q in the updated cache: the walked entries (the split
-  // head in place of the split node) and the new leaf
-  {
-    int32_t fc = have_path ? pe : kPathMax + 1;
-    if (fc <= kPathMax) {
-      if (split) {
-        int32_t f1 = fc - 1;
-        path_add(pr, f1, a, laststart, laststart + lastcov);
-      }
-      if (h < L) path_add(pr, fc, l, h, L);
-    }
-    if (lane_id() == 0) *pr.cnt = fc;
-  }
+  clock_mark<PT>(clk, ph_finish);
   return 0;
 fail:
-  if (lane_id() == 0) *pr.cnt = kPathMax + 1;
   store_st(P.hdr, s);
   if (dbg) {
     dbg[0] = s.dbg_check;
@@ -1659,6 +1777,21 @@ fail:
     dbg[3] = s.dbg_val[2];
   }
   return s.err ? s.err : (uint32_t)KVR_DEV_INTERNAL;
+}
+
+// RLT insertion of q[0, L) into the worker's cache on one wave: the front
+// half, then the back half.  On return pr holds the path of q in the
+// updated cache.  Returns the KVR_DEV_* error bits (0 on success).
+template <bool PT = false>
+__device__ __forceinline__ uint32_t rlt_insert(const Ptrs& P, const InsertArgs& ia, const int32_t* qs, int32_t L,
+                                               int32_t h, const UStage& ustage, const PathRef& pr, int64_t* dbg,
+                                               PhaseClock* clk = nullptr) {
+  EvictJob job;
+  uint32_t err = rlt_insert_front<PT>(P, ia, qs, L, h, pr, dbg, job, clk);
+  if (err) return err;
+  err = rlt_insert_back<PT>(P, job, ustage, dbg, clk);
+  if (err && lane_id() == 0) *pr.cnt = kPathMax + 1;
+  return err;
 }
 
 // ---------------------------------------------------------------- continuous batching
@@ -2087,8 +2220,8 @@ fail:
 #ifndef KVR_MATCH_UNROLL
 #define KVR_MATCH_UNROLL 8
 #endif
+template <int kUnroll = KVR_MATCH_UNROLL>
 __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n) {
-  constexpr int kUnroll = KVR_MATCH_UNROLL;
   const uintptr_t ea = reinterpret_cast<uintptr_t>(e);
   const int32_t lead = (int32_t)((ea & 15u) >> 2);
   const int4* base = reinterpret_cast<const int4*>(ea - (uintptr_t)lead * 4u);
@@ -2124,6 +2257,7 @@ __device__ int32_t first_mismatch(const int32_t* e, const int32_t* q, int32_t n)
 // Continue matching q[0, L) from inside node x (x = 0: the root), `off`
 // tokens into its edge, with d tokens matched so far.  Entries of the nodes
 // entered are appended at pc.  Returns h.
+template <int kU = KVR_MATCH_UNROLL>
 __device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L, int32_t x, int32_t off,
                               int32_t d, const PathRef& pr, int32_t& pc) {
   const int32_t* ar = arena_of(P, sel);
@@ -2133,7 +2267,7 @@ __device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const
   if (x != 0 && off < nx.len) {  // the rest of this edge first
     const int32_t rest = nx.len - off;
     const int32_t n = rest < L - d ? rest : L - d;
-    const int32_t k = first_mismatch(ar + nx.off + off, qs + d, n);
+    const int32_t k = first_mismatch<kU>(ar + nx.off + off, qs + d, n);
     d += k;
     if (k < rest) return d;
   }
@@ -2144,7 +2278,7 @@ __device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const
     if (nc.len <= 0) break;  // never true for a consistent tree
     path_add(pr, pc, c, d, d + nc.len);
     const int32_t n = nc.len < L - d ? nc.len : L - d;
-    const int32_t k = 1 + first_mismatch(ar + nc.off + 1, qs + d + 1, n - 1);
+    const int32_t k = 1 + first_mismatch<kU>(ar + nc.off + 1, qs + d + 1, n - 1);
     d += k;
     if (k < nc.len) break;
     nx = nc;
@@ -2154,10 +2288,11 @@ __device__ __forceinline__ int32_t match_from(const Ptrs& P, uint32_t sel, const
 
 // h = length of the longest prefix of q[0, L) cached in the worker's tree,
 // recording the path.
+template <int kU = KVR_MATCH_UNROLL>
 __device__ __forceinline__ int32_t match_lcp(const Ptrs& P, uint32_t sel, const int32_t* qs, int32_t L,
                                              const PathRef& pr) {
   int32_t pc = 0;
-  const int32_t h = match_from(P, sel, qs, L, 0, 0, 0, pr, pc);
+  const int32_t h = match_from<kU>(P, sel, qs, L, 0, 0, 0, pr, pc);
   if (lane_id() == 0) *pr.cnt = pc;
   return h;
 }
@@ -2169,22 +2304,46 @@ __device__ __forceinline__ int32_t match_lcp(const Ptrs& P, uint32_t sel, const 
 // new one leaves q_old's path at depth ell: inside an edge that the old
 // match followed further it stops there; otherwise it continues from that
 // point.  The path record is updated to the new match.
+template <int kU = KVR_MATCH_UNROLL>
 __device__ __forceinline__ int32_t match_incremental(const Ptrs& P, uint32_t sel, const int32_t* qn, int32_t Ln, int32_t h_old,
                                      int32_t ell, const PathRef& pr) {
   int32_t pc = *pr.cnt;
-  if (pc > kPathMax || ell == 0) return match_lcp(P, sel, qn, Ln, pr);
+  if (pc > kPathMax || ell == 0) return match_lcp<kU>(P, sel, qn, Ln, pr);
   if (h_old < ell) return h_old;
   // the entry holding depth ell: the last one starting above it
   int32_t e = pc - 1;
   while (e > 0 && pr.start[e] >= ell) --e;
   const int32_t x = pr.node[e], st = pr.start[e], en = pr.end[e];
-  if (pc == 0 || st >= ell || en < ell) return match_lcp(P, sel, qn, Ln, pr);  // inconsistent record
+  if (pc == 0 || st >= ell || en < ell) return match_lcp<kU>(P, sel, qn, Ln, pr);  // inconsistent record
   pc = e + 1;
   int32_t h;
   if (ell == Ln || (ell < en && h_old > ell)) {
     h = ell;
   } else {
-    h = match_from(P, sel, qn, Ln, x, ell - st, ell, pr, pc);
+    h = match_from<kU>(P, sel, qn, Ln, x, ell - st, ell, pr, pc);
+  }
+  if (lane_id() == 0) *pr.cnt = pc;
+  return h;
+}
+
+// match_incremental that reads the worker's active semispace only when it
+// walks the tree (the common outcomes need no global memory at all).
+template <int kU = KVR_MATCH_UNROLL>
+__device__ __forceinline__ int32_t match_incremental_lazy(const Ptrs& P, const int32_t* qn, int32_t Ln, int32_t h_old,
+                                                          int32_t ell, const PathRef& pr) {
+  int32_t pc = *pr.cnt;
+  if (pc > kPathMax || ell == 0) return match_lcp<kU>(P, P.hdr->arena_sel, qn, Ln, pr);
+  if (h_old < ell) return h_old;
+  int32_t e = pc - 1;
+  while (e > 0 && pr.start[e] >= ell) --e;
+  const int32_t x = pr.node[e], st = pr.start[e], en = pr.end[e];
+  if (pc == 0 || st >= ell || en < ell) return match_lcp<kU>(P, P.hdr->arena_sel, qn, Ln, pr);
+  pc = e + 1;
+  int32_t h;
+  if (ell == Ln || (ell < en && h_old > ell)) {
+    h = ell;
+  } else {
+    h = match_from<kU>(P, P.hdr->arena_sel, qn, Ln, x, ell - st, ell, pr, pc);
   }
   if (lane_id() == 0) *pr.cnt = pc;
   return h;

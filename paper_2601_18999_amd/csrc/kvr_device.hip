@@ -168,6 +168,15 @@ __device__ __forceinline__ uint32_t route_choice(const StepArgs& a, uint32_t r, 
   return wave_argmin(eh, W, eh_sh);
 }
 
+// Record a match length and count it in the workgroup's per-worker sums
+// (LDS; added to the worker headers when the batch ends).
+__device__ __forceinline__ void count_mtok(unsigned long long* mtok, uint32_t w, int32_t h, int32_t* hslot) {
+  if (lane_id() == 0) {
+    *hslot = h;
+    atomicAdd(&mtok[w], (unsigned long long)(uint32_t)h);
+  }
+}
+
 // Record a match length without counting it (the cache's own match when
 // the router scores with its own tree).
 __device__ __forceinline__ void store_h(int32_t h, int32_t* hslot) {
@@ -265,7 +274,7 @@ __device__ __forceinline__ uint32_t router_admit(const StepArgs& a, uint32_t r, 
 // worker is updated by a helper wave.  The approximate router (RT) and
 // continuous batching (BA) are template switches, so the kernel without
 // them carries none of their registers.
-template <bool RT, bool BA>
+template <bool RT, bool BA, bool PT>
 __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
   // dynamic LDS: two query buffers (max_query_tokens entries each), the high
   // halves of the draw words, the match paths (the caches', then the router
@@ -325,6 +334,8 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     chain = rh->route_digest;
     routed = rh->queries;
   }
+  PhaseClock clk;
+  clock_start<PT>(&clk);
 
   // query 0: stage its path; completions and decay at its arrival; full
   // matches of its prompt
@@ -419,7 +430,9 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
     } else if (has_next) {
       stage_next(a.tokens, n0, Ln, qn, qs, Lp, threadIdx.x - KVR_WAVE, blockDim.x - KVR_WAVE, &ell_sh[cur]);
     }
+    if (wave == 0) clock_mark<PT>(&clk, KVR_PHASE_ROUTE);
     __syncthreads();
+    if (wave == 0) clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
     if (abort_sh) break;
     const uint32_t best = (uint32_t)best_sh;
     const uint32_t nev = nev_sh;
@@ -461,7 +474,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
       ia.rank = ranker ? &rank_sh : nullptr;
       ia.rank_ready = &rank_ready_sh;
       int64_t dbg[4] = {0, 0, 0, 0};
-      uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg)
+      uint32_t err = a.C.evict == KVR_EVICT_RLT ? rlt_insert<PT>(P, ia, qs, Lp, hins, ustage, paths.of(best), dbg, &clk)
                                                 : lru_insert(P, ia, qs, Lp, hins, paths.of(best), dbg);
       // continuous batching: the path joins the worker's running batch
       if (BA && !err && P.beta > 1) err = batch_admit(P, paths.of(best), qs, Lp, dbg);
@@ -476,6 +489,7 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
         else
           count_matched(Pb, h, &h_sh[cur ^ 1u][best]);
       }
+      clock_mark<PT>(&clk, KVR_PHASE_MATCH);
       if (nh == 0 && !err) {
         if (has_next) {
           if ((uint32_t)lane < W)
@@ -532,12 +546,565 @@ __global__ void __launch_bounds__(512) step_kernel(StepArgs a) {
                      rpaths, rtree, &next_sh);
     }
     __syncthreads();
+    if (wave == 0) clock_mark<PT>(&clk, KVR_PHASE_JOIN);
     if (abort_sh) break;
   }
   if (threadIdx.x == 0) {
+    if constexpr (PT)
+      for (int p = 0; p < KVR_PHASES; ++p) rh->phase_ticks[p] += clk.acc[p];
     rh->route_digest = chain;
     rh->queries = routed;
     if (!abort_sh && a.n > 0) {
+      rh->tprev = a.arrival[a.n - 1];
+      if (r == 0) g->last_arrival = a.arrival[a.n - 1];
+    }
+  }
+}
+
+// ---------------------------------------------------------------- pipelined step kernel
+//
+// RLT with prompts only, LBGR or a baseline router, no approximate router
+// and single-query processing (the benchmark's path).  The evictions of an
+// insertion only touch the routed worker's cache, and nothing the routing of
+// the next query reads depends on them but that worker's h of the next
+// query.  So a separate wave, the evicting wave, runs the back half of each
+// insertion (evictions, marks of the loaded tokens, header) while the
+// routing wave routes the next query and runs the front half of its
+// insertion (marking walk, split, rank, load of the new leaf).  The routing
+// wave takes the routed worker's h of the next query on the tree after the
+// load and before the evictions: the evictions never remove a token of the
+// inserted path, so when that match ends on the inserted path (h equal to
+// the two queries' longest common prefix) it is exact; otherwise it is taken
+// again once the evictions are done.  One insertion is evicted at a time:
+// the routing wave waits for the evicting wave before it hands it the next
+// insertion or inserts into the worker being evicted.
+//
+// Waves: 0 routes and runs front halves, 1 evicts, 2.. are helpers (stage
+// the next query, compute draw words, rank the new leaf, apply completions
+// and decay, match the next query on the other workers).  They synchronise
+// through the counters below (LDS, workgroup scope, release/acquire); every
+// wait is bounded and checks the stop flag, so an error ends every loop.
+
+struct PipeFlags {
+  uint32_t top;         // the routing wave has begun query top - 1: q_top may be staged
+  uint32_t routed;      // queries routed (route, evictions and slots of query routed - 1 published)
+  uint32_t staged;      // staging waves done, over all queries
+  uint32_t matched;     // helper matches done, over all queries (W - 1 per query)
+  uint32_t decayed;     // arrivals whose completions and decay are applied
+  uint32_t handed;      // insertions handed to the evicting wave
+  uint32_t evicted;     // insertions it has finished
+  uint32_t ework;       // worker of its current insertion, kNoWorker when idle
+  uint32_t ework_size;  // that worker's |S| once the insertion is done
+  uint32_t end;         // no more insertions will be handed
+  uint32_t stop;        // an error stopped the replica
+  uint32_t next[2];     // helper match items taken, by query parity
+  uint32_t last_worker; // worker of the last insertion handed to the evicting wave
+  uint32_t pad;
+  // the next query's matches, claimed per worker (bit i) by the wave that
+  // takes them, by query parity: a helper, or the evicting wave for its
+  // worker once its evictions end
+  unsigned long long claim[2];
+};
+
+constexpr uint32_t kNoWorker = 0xffffffffu;
+// 16-byte compare loads in flight per lane in the pipelined kernel's matches
+// (its next-query matches are on the routing wave's path)
+#ifndef KVR_PIPE_MATCH_UNROLL
+#define KVR_PIPE_MATCH_UNROLL 8
+#endif
+constexpr int kPipeMatchUnroll = KVR_PIPE_MATCH_UNROLL;
+constexpr uint32_t kSpinLimit = 1u << 24;
+
+__device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Publish v (lane 0, after every lane's earlier writes).
+__device__ __forceinline__ void st_rel(uint32_t* p, uint32_t v) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if (lane_id() == 0) __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void add_rel(uint32_t* p, uint32_t v) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if (lane_id() == 0) __hip_atomic_fetch_add(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Stop the replica: the first error of the run is recorded (check id, the
+// query, values), the status bits are set and every wave's waits end.
+__device__ __forceinline__ void pipe_stop(GlobalHdr* g, PipeFlags* f, uint32_t r, uint64_t jg, uint32_t err,
+                                          const int64_t* dbg) {
+  if (lane_id() == 0) {
+    if (atomicCAS(&g->err_taken, 0u, 1u) == 0u) {
+      g->err_check = (uint32_t)dbg[0];
+      g->err_replica = r;
+      g->err_query = jg;
+      g->err_val[0] = dbg[1];
+      g->err_val[1] = dbg[2];
+      g->err_val[2] = dbg[3];
+    }
+    atomicOr(&g->status, err);
+    __hip_atomic_store(&f->stop, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+}
+
+// Wait until *p >= target (or, with ne, until *p != target).  False when
+// the replica was stopped; a wait that runs out stops it (check id 90 +
+// site, an internal error).
+template <bool kNe = false>
+__device__ __forceinline__ bool pipe_wait(const uint32_t* p, uint32_t target, PipeFlags* f, GlobalHdr* g, uint32_t r,
+                                          uint64_t jg, int site) {
+  uint32_t spins = 0;
+  for (;;) {
+    const uint32_t v = ld_acq(p);
+    if (kNe ? v != target : v >= target) return true;
+    if (__hip_atomic_load(&f->stop, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) return false;
+    if (++spins > kSpinLimit) {
+      const int64_t dbg[4] = {90 + site, (int64_t)v, (int64_t)target, 0};
+      pipe_stop(g, f, r, jg, KVR_DEV_INTERNAL, dbg);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+template <bool PT>
+__global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
+  // dynamic LDS: two query buffers, the draw words of two insertions, the
+  // match paths, the staged candidate list
+  extern __shared__ int32_t smem[];
+  const uint32_t W = a.L.W;
+  const uint32_t qstride = (a.L.maxL + 3u) & ~3u;
+  uint32_t* rwb = reinterpret_cast<uint32_t*>(smem + 2 * qstride);  // [2][rcap]
+  PathArea paths;
+  paths.base = reinterpret_cast<int32_t*>(rwb + 2 * a.rcap);
+  paths.W = W;
+  UStage ustage;
+  {
+    int32_t* ub = paths.base + (size_t)W * (3 * kPathMax + 1);
+    ustage.node = ub;
+    ustage.len = ub + a.ucap;
+    ustage.top = ub + 2 * a.ucap;
+    ustage.par = ub + 3 * a.ucap;
+    ustage.cap = a.ucap;
+  }
+  __shared__ int32_t h_sh[2][kMaxWorkers];  // h of q_k in slot k & 1
+  __shared__ double eh_sh[kMaxWorkers];
+  __shared__ int32_t ell_sh[2];             // LCP(q_k, q_k+1) in slot k & 1
+  __shared__ int32_t best_sh[2];
+  __shared__ uint32_t rn_sh[2];             // draw words of insertion k precomputed in slot k & 1
+  __shared__ uint32_t prog_sh[2][16];       // rounds of them each drawing wave has written
+  __shared__ int32_t rank_sh;
+  __shared__ uint32_t rank_ready_sh;
+  __shared__ PipeFlags f;
+  __shared__ EvictJob job_sh[2];            // by insertion count parity
+  __shared__ unsigned long long eticks_sh[KVR_PHASES];  // evicting and helper waves' ticks
+  // matched tokens per worker over the batch (added to the headers at the end)
+  __shared__ unsigned long long mtok_sh[kMaxWorkers];
+
+  const uint32_t r = blockIdx.x;
+  const int lane = lane_id();
+  const uint32_t wave = threadIdx.x / KVR_WAVE;
+  const uint32_t nwaves = blockDim.x / KVR_WAVE;
+  const uint32_t nh = nwaves - 2;  // helper waves (>= 2)
+  // the last helper ranks new leaves; about half of the others compute the
+  // draw words first, the rest start on the next query's matches at once
+  // (both are due about when the front half of the insertion ends)
+#ifndef KVR_PIPE_DRAW_HELPERS
+#define KVR_PIPE_DRAW_HELPERS 3
+#endif
+  const uint32_t ndraw = nh > KVR_PIPE_DRAW_HELPERS ? KVR_PIPE_DRAW_HELPERS : nh - 1;
+  const uint32_t nd = ndraw * KVR_WAVE;  // drawing threads
+  GlobalHdr* g = reinterpret_cast<GlobalHdr*>(a.ws + a.L.off_global);
+  ReplicaHdr* rh = reinterpret_cast<ReplicaHdr*>(a.ws + a.L.off_rhdr) + r;
+
+  if (threadIdx.x == 0) {
+    f.top = 1;  // q_1 may be staged at once (its buffer is free)
+    f.routed = f.staged = f.matched = f.handed = f.evicted = f.end = 0;
+    f.decayed = 0;
+    f.ework = kNoWorker;
+    f.ework_size = 0;
+    f.next[0] = f.next[1] = 0;
+    f.claim[0] = f.claim[1] = 0ull;
+    f.last_worker = kNoWorker;
+    f.pad = 0;
+    f.stop = __atomic_load_n(&g->status, __ATOMIC_RELAXED) ? 1u : 0u;
+    ell_sh[0] = ell_sh[1] = 0x7fffffff;
+    rank_ready_sh = 0;
+    for (uint32_t i = 0; i < kMaxWorkers; ++i) mtok_sh[i] = 0ull;
+    for (int p = 0; p < KVR_PHASES; ++p) eticks_sh[p] = 0;
+  }
+  __syncthreads();
+  if (f.stop) return;
+
+  // query 0: stage it; completions and decay at its arrival; full matches
+  {
+    const uint64_t o0 = a.offsets[0];
+    const int32_t L0 = (int32_t)(a.offsets[1] - o0);
+    for (int32_t x = (int32_t)threadIdx.x; x < L0; x += (int32_t)blockDim.x) smem[x] = a.tokens[o0 + x];
+    if (wave == 0 && (uint32_t)lane < W)
+      complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[0], rh->tprev);
+    __syncthreads();
+    for (uint32_t i = wave; i < W; i += nwaves) {
+      Ptrs P = worker_ptrs(a.ws, a.L, r, i);
+      count_mtok(mtok_sh, i, match_lcp<kPipeMatchUnroll>(P, P.hdr->arena_sel, smem, L0, paths.of(i)), &h_sh[0][i]);
+    }
+    if (threadIdx.x == 0) f.decayed = 1;
+    __syncthreads();
+  }
+
+  if (wave == 0) {
+    // ---------------------------------------------------------- routing wave
+    uint64_t chain = rh->route_digest, routed = rh->queries;
+    PhaseClock clk;
+    clock_start<PT>(&clk);
+    uint32_t issued = 0;    // insertions handed to the evicting wave
+    uint32_t last_job = 0;  // query index (in the batch) of the last one
+    // the routed worker's h of the next query, when it has to be taken again
+    // after the evictions: worker, path length and LCP of the two queries
+    bool redo = false;
+    uint32_t redo_w = 0;
+    int32_t redo_L = 0, redo_ell = 0;
+    for (uint32_t k = 0; k < a.n; ++k) {
+      const uint32_t cur = k & 1u;
+      const uint64_t jg = a.j0 + k;
+      const uint64_t o0 = a.offsets[k];
+      const int32_t Lp = (int32_t)(a.offsets[k + 1] - o0);
+      const int64_t t = a.arrival[k];
+      const int32_t olen = query_out_len(a.out_len, k);
+      const bool has_next = k + 1 < a.n;
+      const int32_t Ln = has_next ? (int32_t)(a.offsets[k + 2] - a.offsets[k + 1]) : 0;
+      int32_t* qs = smem + cur * qstride;
+      const int32_t* qn = smem + (cur ^ 1u) * qstride;
+      // h of q_k on every worker, completions and decay at its arrival
+      if (k > 0 && !pipe_wait(&f.matched, k * (W - 1), &f, g, r, jg, 0)) break;
+      if (!pipe_wait(&f.decayed, k + 1, &f, g, r, jg, 1)) break;
+      if (redo) {
+        // the evictions of the previous insertion are done before this
+        if (!pipe_wait(&f.evicted, issued, &f, g, r, jg, 2)) break;
+        clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
+        Ptrs Pw = worker_ptrs(a.ws, a.L, r, redo_w);
+        count_mtok(mtok_sh, redo_w,
+                   match_incremental<kPipeMatchUnroll>(Pw, Pw.hdr->arena_sel, qs, Lp, redo_L, redo_ell, paths.of(redo_w)),
+                   &h_sh[cur][redo_w]);
+        clock_mark<PT>(&clk, KVR_PHASE_MATCH);
+        redo = false;
+      }
+      clock_mark<PT>(&clk, KVR_PHASE_JOIN);
+
+      // the draw words and rounds of this parity are reused below: the
+      // evicting wave must be done with the insertion that used them
+      if (issued > 0 && (last_job & 1u) == cur && !pipe_wait(&f.evicted, issued, &f, g, r, jg, 11)) break;
+      // ---- route: scores, argmin, commit
+      const uint32_t ew = ld_acq(&f.ework);
+      const uint32_t ew_size = __hip_atomic_load(&f.ework_size, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      double eh = __builtin_huge_val(), ch = 0.0;
+      RouteView v{};
+      if ((uint32_t)lane < W) {
+        v = load_view(worker_ptrs(a.ws, a.L, r, (uint32_t)lane).hdr);
+        // the worker being evicted: its size once the evictions are done
+        if ((uint32_t)lane == ew) v.size = ew_size;
+        eh = lbgr_score(a.C, v, h_sh[cur][lane], Lp, &ch);
+        eh_sh[lane] = eh;
+      }
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t best = route_choice(a, r, k, W, eh, h_sh[cur], Lp, eh_sh, v);
+      Ptrs P = worker_ptrs(a.ws, a.L, r, best);
+      const int32_t hb = h_sh[cur][best];
+      uint32_t cerr = 0;
+      if ((uint32_t)lane == best) cerr = commit_route(a.C, P, v, ch, hb, hb, Lp, t, olen);
+      const uint32_t err0 = (uint32_t)__builtin_amdgcn_readlane((int)cerr, (int)best);
+      const uint32_t size = (uint32_t)__builtin_amdgcn_readlane((int)v.size, (int)best);
+      const uint32_t nload = (uint32_t)(Lp - hb);
+      const uint32_t nfree = a.L.B - size;
+      const uint32_t nev = nload > nfree ? nload - nfree : 0u;
+      const uint32_t rn = nev < a.rcap ? nev : a.rcap;
+      if ((uint32_t)lane < 16u) prog_sh[cur][lane] = 0u;
+      if (lane == 0) {
+        best_sh[cur] = (int32_t)best;
+        rn_sh[cur] = rn;
+        f.next[cur] = 0;
+        f.claim[cur] = 0ull;
+        rank_ready_sh = 0;
+        const uint64_t orow = (uint64_t)r * a.n + k;
+        if (a.route) a.route[orow] = (int32_t)best;
+        if (a.hits) a.hits[orow] = hb;
+        if (!err0) {
+          chain = route_chain(chain, jg, best, hb);
+          routed += 1;
+        }
+      }
+      if (a.all_hits && (uint32_t)lane < W) a.all_hits[((uint64_t)r * a.n + k) * W + (uint32_t)lane] = h_sh[cur][lane];
+      if (err0) {
+        const int64_t dbg[4] = {0, 0, 0, 0};
+        pipe_stop(g, &f, r, jg, err0, dbg);
+        break;
+      }
+      st_rel(&f.routed, k + 1);
+      clock_mark<PT>(&clk, KVR_PHASE_ROUTE);
+
+      // ---- front half of the insertion of q_k (the worker being evicted first
+      // finishes its evictions)
+      if (ew == best && !pipe_wait(&f.evicted, issued, &f, g, r, jg, 3)) break;
+      clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
+      EvictJob& job = job_sh[issued & 1u];
+      {
+        InsertArgs ia;
+        ia.seed = a.C.seed;
+        ia.jg = jg;
+        ia.worker = best;
+        ia.replica = r;
+        ia.B = a.L.B;
+        ia.rn = rn;
+        ia.rw = rwb + (size_t)cur * a.rcap;
+        ia.prog = rn ? prog_sh[cur] : nullptr;
+        ia.nprog = ndraw;
+        ia.round = 2u * nd;
+        ia.rank = hb < Lp ? &rank_sh : nullptr;
+        ia.rank_ready = &rank_ready_sh;
+        int64_t dbg[4] = {0, 0, 0, 0};
+        const uint32_t err = rlt_insert_front<PT>(P, ia, qs, Lp, hb, paths.of(best), dbg, job, &clk);
+        if (err) {
+          pipe_stop(g, &f, r, jg, err, dbg);
+          break;
+        }
+      }
+      // q_k's buffer is free: q_k+2 may be staged (its LCP with q_k+1 goes to
+      // the slot of LCP(q_k-1, q_k), which nothing reads any more)
+      if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
+      st_rel(&f.top, k + 2);
+      // ---- the routed worker's h of the next query, on the tree after the
+      // load: exact when it ends on the inserted path or nothing is evicted
+      if (has_next) {
+        if (!pipe_wait(&f.staged, (k + 1) * nh, &f, g, r, jg, 4)) break;
+        clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
+        const int32_t ellp = ell_sh[cur];
+        const int32_t ell_r = ellp < Ln ? ellp : Ln;
+        const int32_t h = match_incremental<kPipeMatchUnroll>(P, job.s.arena_sel, qn, Ln, Lp, ell_r, paths.of(best));
+        if (job.nev == 0 || h == ell_r) {
+          count_mtok(mtok_sh, best, h, &h_sh[cur ^ 1u][best]);
+        } else {
+          redo = true;
+          redo_w = best;
+          redo_L = Lp;
+          redo_ell = ell_r;
+        }
+        clock_mark<PT>(&clk, KVR_PHASE_MATCH);
+      }
+      // ---- the back half: here when nothing is evicted, else on the
+      // evicting wave once it is free
+      if (job.nev == 0) {
+        int64_t dbg[4] = {0, 0, 0, 0};
+        const uint32_t err = rlt_insert_back<PT>(P, job, ustage, dbg, &clk);
+        if (err) {
+          pipe_stop(g, &f, r, jg, err, dbg);
+          break;
+        }
+      } else {
+        if (!pipe_wait(&f.evicted, issued, &f, g, r, jg, 5)) break;
+        clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
+        if (lane == 0) {
+          __hip_atomic_store(&f.ework, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          __hip_atomic_store(&f.ework_size, job.final_size, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+        issued += 1;
+        last_job = k;
+        st_rel(&f.handed, issued);
+      }
+    }
+    st_rel(&f.end, 1u);
+    if (lane == 0) {
+      rh->route_digest = chain;
+      rh->queries = routed;
+      if constexpr (PT)
+        for (int p = 0; p < KVR_PHASES; ++p) rh->phase_ticks[p] += clk.acc[p];
+    }
+  } else if (wave == 1) {
+    // ---------------------------------------------------------- evicting wave
+    PhaseClock clk;
+    clock_start<PT>(&clk);
+    uint32_t done = 0;
+    for (;;) {
+      // the next insertion, or the end (the bound on the wait restarts
+      // whenever the routing wave routes a query)
+      uint32_t spins = 0, seen = ld_acq(&f.routed);
+      bool quit = false;
+      for (;;) {
+        if (ld_acq(&f.handed) > done) break;
+        const uint32_t now = ld_acq(&f.routed);
+        if (now != seen) {
+          seen = now;
+          spins = 0;
+        }
+        if (ld_acq(&f.end) && ld_acq(&f.handed) == done) {
+          quit = true;
+          break;
+        }
+        if (__hip_atomic_load(&f.stop, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) {
+          quit = true;
+          break;
+        }
+        if (++spins > kSpinLimit) {
+          const int64_t dbg[4] = {96, (int64_t)done, 0, 0};
+          pipe_stop(g, &f, r, a.j0, KVR_DEV_INTERNAL, dbg);
+          quit = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (quit) break;
+      clock_mark<PT>(&clk, KVR_PHASE_E_IDLE);
+      const EvictJob& job = job_sh[done & 1u];
+      const uint32_t w = job.worker;
+      int64_t dbg[4] = {0, 0, 0, 0};
+      const uint32_t err = rlt_insert_back<PT>(worker_ptrs(a.ws, a.L, r, w), job, ustage, dbg, &clk,
+                                               KVR_PHASE_E_EVICT, KVR_PHASE_E_FINISH);
+      if (err) {
+        pipe_stop(g, &f, r, job.ia.jg, err, dbg);
+        break;
+      }
+      if (lane == 0) __hip_atomic_store(&f.ework, kNoWorker, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP);
+      done += 1;
+      st_rel(&f.evicted, done);
+      // the helpers may be matching q_s+1 (s = the last query routed) and
+      // have left this worker to this wave: take that match unless a helper
+      // claimed it (or the worker is the one q_s went to)
+      {
+        const uint32_t rt = __hip_atomic_load(&f.routed, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (rt > 0 && rt < a.n) {
+          const uint32_t sq = rt - 1u, sc = sq & 1u;
+          unsigned long long old = 0ull;
+          if ((uint32_t)best_sh[sc] != w && lane == 0) old = atomicOr(&f.claim[sc], 1ull << w);
+          old = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(old >> 32), 0) << 32) |
+                (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)old, 0);
+          if ((uint32_t)best_sh[sc] != w && !(old & (1ull << w))) {
+            if (!pipe_wait(&f.staged, rt * nh, &f, g, r, a.j0 + rt, 12)) break;
+            const int32_t Ls = (int32_t)(a.offsets[sq + 1] - a.offsets[sq]);
+            const int32_t Lnx = (int32_t)(a.offsets[sq + 2] - a.offsets[sq + 1]);
+            const int32_t ellp = ell_sh[sc];
+            const int32_t ell_r = ellp < Lnx ? ellp : Lnx;
+            const int32_t ell = ell_r < Ls ? ell_r : Ls;
+            Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
+            count_mtok(mtok_sh, w,
+                       match_incremental_lazy<kPipeMatchUnroll>(Pw, smem + (sc ^ 1u) * qstride, Lnx, h_sh[sc][w], ell,
+                                                                paths.of(w)),
+                       &h_sh[sc ^ 1u][w]);
+            add_rel(&f.matched, 1u);
+          }
+        }
+      }
+    }
+    if constexpr (PT)
+      if (lane == 0)
+        for (int p = KVR_PHASE_E_EVICT; p <= KVR_PHASE_E_IDLE; ++p) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
+  } else {
+    // ---------------------------------------------------------- helper waves
+    const uint32_t hw = wave - 2u;  // 0 .. nh-1
+    PhaseClock clk;
+    clock_start<PT>(&clk);
+    for (uint32_t k = 0; k < a.n; ++k) {
+      const uint32_t cur = k & 1u;
+      const uint64_t jg = a.j0 + k;
+      const uint64_t o0 = a.offsets[k];
+      const int32_t Lp = (int32_t)(a.offsets[k + 1] - o0);
+      const int64_t t = a.arrival[k];
+      const bool has_next = k + 1 < a.n;
+      const uint64_t n0 = has_next ? a.offsets[k + 1] : 0;
+      const int32_t Ln = has_next ? (int32_t)(a.offsets[k + 2] - n0) : 0;
+      const int32_t* qs = smem + cur * qstride;
+      int32_t* qn = smem + (cur ^ 1u) * qstride;
+      // stage q_k+1 once the routing wave has begun q_k
+      if (has_next) {
+        if (!pipe_wait(&f.top, k + 1, &f, g, r, jg, 6)) break;
+        clock_mark<PT>(&clk, KVR_PHASE_H_WAIT);
+        stage_next(a.tokens, n0, Ln, qn, qs, Lp, hw * KVR_WAVE + (uint32_t)lane, nh * KVR_WAVE, &ell_sh[cur]);
+        add_rel(&f.staged, 1u);
+        clock_mark<PT>(&clk, KVR_PHASE_H_STAGE);
+      }
+      if (!pipe_wait(&f.routed, k + 1, &f, g, r, jg, 7)) break;
+      clock_mark<PT>(&clk, KVR_PHASE_H_WAIT);
+      const uint32_t best = (uint32_t)best_sh[cur];
+      const uint32_t rn = rn_sh[cur];
+      // completions and decay at the next arrival (the first helper)
+      if (hw == 0 && has_next) {
+        if ((uint32_t)lane < W)
+          complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[k + 1], t);
+        st_rel(&f.decayed, k + 2);
+        clock_mark<PT>(&clk, KVR_PHASE_H_OTHER);
+      }
+      const int32_t hb = h_sh[cur][best];
+      if (hw == nh - 1u) {
+        // the last helper ranks the new leaf (on the tree before the
+        // insertion; the worker's previous evictions come first)
+        if (hb < Lp) {
+          if (!pipe_wait<true>(&f.ework, best, &f, g, r, jg, 8)) break;
+          rank_for_insertion(worker_ptrs(a.ws, a.L, r, best), paths.of(best), qs, hb, &rank_sh, &rank_ready_sh);
+          clock_mark<PT>(&clk, KVR_PHASE_H_OTHER);
+        }
+      } else if (hw < ndraw) {
+        // the drawing helpers compute the draw words, a round of 2*nd words
+        // at a time, and publish each round they complete
+        uint32_t* rw = rwb + (size_t)cur * a.rcap;
+        uint32_t rounds = 0;
+        for (uint32_t base = 0; base < rn; base += 2u * nd) {
+          const uint32_t d0 = base + hw * KVR_WAVE + (uint32_t)lane, d1 = d0 + nd;
+          const uint64_t w0 = philox_word0(jg, best, d0, 0ull, a.C.seed, r);
+          const uint64_t w1 = philox_word0(jg, best, d1, 0ull, a.C.seed, r);
+          if (d0 < rn) rw[d0] = (uint32_t)(w0 >> 32);
+          if (d1 < rn) rw[d1] = (uint32_t)(w1 >> 32);
+          ++rounds;
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          if (lane == 0) __hip_atomic_store(&prog_sh[cur][hw], rounds, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+        clock_mark<PT>(&clk, KVR_PHASE_H_DRAW);
+      }
+      // h of q_k+1 on every worker but the routed one, the worker whose
+      // evictions may still run taken last
+      if (has_next) {
+        if (!pipe_wait(&f.staged, (k + 1) * nh, &f, g, r, jg, 9)) break;
+        clock_mark<PT>(&clk, KVR_PHASE_H_WAIT);
+        const int32_t ellp = ell_sh[cur];
+        const int32_t ell_r = ellp < Ln ? ellp : Ln;
+        const int32_t ell = ell_r < Lp ? ell_r : Lp;
+        const uint32_t prev = k > 0 ? (uint32_t)best_sh[cur ^ 1u] : 0u;
+        bool ok = true;
+        uint32_t mine = 0;
+        for (uint32_t it = 0; it < W; ++it) {
+          uint32_t got = 0;
+          if (lane == 0) got = atomicAdd(&f.next[cur], 1u);
+          const uint32_t item = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
+          if (item >= W) break;
+          const uint32_t w = (prev + 1u + item) % W;
+          if (w == best) continue;
+          // the worker being evicted: its match is the evicting wave's, when
+          // its evictions end; any other is claimed here (unless that wave
+          // took it first)
+          if (__hip_atomic_load(&f.ework, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP) == w) continue;
+          unsigned long long old = 0ull;
+          if (lane == 0) old = atomicOr(&f.claim[cur], 1ull << w);
+          const uint32_t taken = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((old >> w) & 1ull), 0);
+          if (taken) continue;
+          Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
+          count_mtok(mtok_sh, w, match_incremental_lazy<kPipeMatchUnroll>(Pw, qn, Ln, h_sh[cur][w], ell, paths.of(w)),
+                     &h_sh[cur ^ 1u][w]);
+          ++mine;
+        }
+        // this wave's matches, published at once
+        add_rel(&f.matched, mine);
+        clock_mark<PT>(&clk, KVR_PHASE_H_MATCH);
+        if (!ok) break;
+      }
+    }
+    if constexpr (PT)
+      if (lane == 0)
+        for (int p = KVR_PHASE_H_STAGE; p < KVR_PHASES; ++p) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
+  }
+  __syncthreads();
+  if (threadIdx.x < W) worker_ptrs(a.ws, a.L, r, threadIdx.x).hdr->matched_tokens += mtok_sh[threadIdx.x];
+  if (threadIdx.x == 0) {
+    if constexpr (PT)
+      for (int p = KVR_PHASE_E_EVICT; p < KVR_PHASES; ++p) rh->phase_ticks[p] += eticks_sh[p];
+    if (!f.stop && a.n > 0) {
       rh->tprev = a.arrival[a.n - 1];
       if (r == 0) g->last_arrival = a.arrival[a.n - 1];
     }
@@ -569,7 +1136,7 @@ __global__ void init_kernel(char* ws, Layout L, double rls_p0) {
     h.queries = 0;
     h.route_digest = 0;
     for (int k = 0; k < KVR_PHASES; ++k) h.phase_ticks[k] = 0;
-    for (int k = 0; k < 5; ++k) h.pad[k] = 0;
+    for (int k = 0; k < 12; ++k) h.pad[k] = 0;
     reinterpret_cast<ReplicaHdr*>(ws + L.off_rhdr)[tid] = h;
   }
   if (tid < RW) {
@@ -640,6 +1207,14 @@ size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, u
 }
 
 
+// Dynamic LDS of the pipelined step kernel: two query buffers, the draw
+// words of two insertions (rcap each), the match paths, ucap staged
+// candidates.
+size_t step_lds_bytes_pipe(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap) {
+  return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + 2 * (size_t)rcap * sizeof(uint32_t) +
+         (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
+}
+
 hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st) {
   const uint64_t work = (uint64_t)L.R * L.W > L.R ? (uint64_t)L.R * L.W : L.R;
   const uint32_t blocks = (uint32_t)((work + 255) / 256);
@@ -661,14 +1236,22 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   const uint32_t waves = a.L.W < kMaxWavesPerBlock ? a.L.W : kMaxWavesPerBlock;
   const size_t lds = step_lds_bytes(a.L.maxL, a.L.W, a.ucap, a.rcap, a.L.has_router ? 2u : 1u);
   const bool rt = a.L.has_router != 0, ba = a.L.beta > 1;
-  if (rt && ba)
-    hipLaunchKernelGGL((step_kernel<true, true>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  if (a.pipe) {
+    const size_t lds_p = step_lds_bytes_pipe(a.L.maxL, a.L.W, a.ucap, a.rcap);
+    if (a.C.phase_timers)
+      hipLaunchKernelGGL((step_kernel_pipe<true>), dim3(a.L.R), dim3(64 * kMaxWavesPerBlock), lds_p, st, a);
+    else
+      hipLaunchKernelGGL((step_kernel_pipe<false>), dim3(a.L.R), dim3(64 * kMaxWavesPerBlock), lds_p, st, a);
+  } else if (rt && ba)
+    hipLaunchKernelGGL((step_kernel<true, true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   else if (rt)
-    hipLaunchKernelGGL((step_kernel<true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+    hipLaunchKernelGGL((step_kernel<true, false, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   else if (ba)
-    hipLaunchKernelGGL((step_kernel<false, true>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+    hipLaunchKernelGGL((step_kernel<false, true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+  else if (a.C.phase_timers)
+    hipLaunchKernelGGL((step_kernel<false, false, true>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   else
-    hipLaunchKernelGGL((step_kernel<false, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
+    hipLaunchKernelGGL((step_kernel<false, false, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   return hipGetLastError();
 }
 
@@ -677,9 +1260,13 @@ hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st) {
   return hipGetLastError();
 }
 
-static const void* const kStepKernels[4] = {
-    reinterpret_cast<const void*>(step_kernel<false, false>), reinterpret_cast<const void*>(step_kernel<false, true>),
-    reinterpret_cast<const void*>(step_kernel<true, false>), reinterpret_cast<const void*>(step_kernel<true, true>)};
+static const void* const kStepKernels[7] = {
+    reinterpret_cast<const void*>(step_kernel_pipe<false>), reinterpret_cast<const void*>(step_kernel_pipe<true>),
+    reinterpret_cast<const void*>(step_kernel<false, false, false>),
+    reinterpret_cast<const void*>(step_kernel<false, true, false>),
+    reinterpret_cast<const void*>(step_kernel<true, false, false>),
+    reinterpret_cast<const void*>(step_kernel<true, true, false>),
+    reinterpret_cast<const void*>(step_kernel<false, false, true>)};
 
 // Static LDS of the step kernels (their __shared__ variables, the largest),
 // from the compiled kernels' attributes.

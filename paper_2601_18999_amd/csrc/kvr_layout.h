@@ -101,9 +101,9 @@ struct ReplicaHdr {
   uint64_t queries;       // queries routed
   uint64_t route_digest;  // hash chain over (query index, route, hit), kvr_replica_stats
   uint64_t phase_ticks[KVR_PHASES];
-  uint64_t pad[5];
+  uint64_t pad[12];
 };
-static_assert(sizeof(ReplicaHdr) == 128, "replica header is 128 bytes");
+static_assert(sizeof(ReplicaHdr) == 256, "replica header is 256 bytes");
 
 struct GlobalHdr {
   uint32_t status;       // KVR_DEV_* bits, sticky
@@ -163,6 +163,8 @@ struct StepArgs {
   uint32_t ucap;  // candidate entries staged in LDS (0: U stays in global memory)
   uint32_t rcap;  // draw words precomputed in LDS per insertion
   uint64_t j0;
+  uint32_t pipe;  // 1: the pipelined step kernel (a separate evicting wave)
+  uint32_t pad2;
 };
 
 inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }

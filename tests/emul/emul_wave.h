@@ -25,6 +25,7 @@ inline int __builtin_amdgcn_readlane(int v, int) { return v; }
 inline int __builtin_amdgcn_update_dpp(int old, int, int, int, int, bool) { return old; }
 inline int __builtin_amdgcn_readfirstlane(int v) { return v; }
 inline void __builtin_amdgcn_s_sleep(int) {}
+inline long long wall_clock64() { return 0; }
 #define __ATOMIC_ACQUIRE_EMUL 0
 template <typename T> inline T __hip_atomic_load(const T* p, int, int) { return *p; }
 template <typename T> inline void __hip_atomic_store(T* p, T v, int, int) { *p = v; }

@@ -10,6 +10,12 @@
 
 using namespace kvr;
 
+// next-query matches on the routed worker that the pipelined order had to
+// take again after the evictions (last emul_run call)
+static uint64_t g_pipe_unsafe = 0, g_pipe_steps = 0;
+extern "C" uint64_t emul_pipe_unsafe(void) { return g_pipe_unsafe; }
+extern "C" uint64_t emul_pipe_steps(void) { return g_pipe_steps; }
+
 extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens, const uint64_t* offsets,
                         const int64_t* arrival, const uint16_t* out_len, int32_t* route, int32_t* hits,
                         int32_t* all_hits, kvr_worker_stats* out, char* ws_out, uint32_t ucap_in) {
@@ -34,6 +40,10 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
   const bool resp = cfg->cache_responses != 0;
   const bool rtree = L.has_router != 0;
   const uint32_t W = L.W;
+  // the order of the pipelined step kernel (RLT, no router tree, no
+  // continuous batching, prompts only)
+  const bool pipe = C.evict == KVR_EVICT_RLT && !rtree && L.beta == 1 && !resp;
+  g_pipe_unsafe = g_pipe_steps = 0;
   // candidate list staging buffer (LDS on the device)
   const uint32_t ucap = ucap_in;
   std::vector<int32_t> ubuf(4 * (size_t)(ucap ? ucap : 1));
@@ -188,8 +198,30 @@ extern "C" int emul_run(const kvr_config* cfg, uint64_t n, const int32_t* tokens
           ia.rank = &rank;
           ia.rank_ready = &rank_ready;
         }
-        err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, path_of(best), nullptr)
-                                       : lru_insert(P, ia, qs, Lp, hins, path_of(best), nullptr);
+        if (pipe) {
+          // the pipelined kernel's order: the front half of the insertion;
+          // the routed worker's h of the next query on the tree before the
+          // evictions (exact when it stays on the inserted path, which no
+          // eviction touches); the back half; a new match if it was not
+          EvictJob job;
+          err = rlt_insert_front(P, ia, qs, Lp, hins, path_of(best), nullptr, job);
+          int32_t hspec = -1;
+          bool safe = false;
+          if (!err && has_next) {
+            hspec = match_incremental(P, job.s.arena_sel, qn, Lnq, Lp, ell_r, path_of(best));
+            safe = hspec == ell_r || job.nev == 0;
+          }
+          if (!err) err = rlt_insert_back(P, job, ustage, nullptr);
+          if (!err && has_next) {
+            const int32_t hpost = match_incremental(P, P.hdr->arena_sel, qn, Lnq, Lp, ell_r, path_of(best));
+            if (safe && hpost != hspec) return -8;  // the early match was not exact
+            g_pipe_unsafe += safe ? 0 : 1;
+            g_pipe_steps += 1;
+          }
+        } else {
+          err = C.evict == KVR_EVICT_RLT ? rlt_insert(P, ia, qs, Lp, hins, ustage, path_of(best), nullptr)
+                                         : lru_insert(P, ia, qs, Lp, hins, path_of(best), nullptr);
+        }
         if (!err && P.beta > 1) err = batch_admit(P, path_of(best), qs, Lp, nullptr);
       }
       if (err) return (int)err;

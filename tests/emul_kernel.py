@@ -40,6 +40,8 @@ def lib():
         _lib = ctypes.CDLL(build())
         _lib.emul_run.restype = ctypes.c_int
         _lib.emul_run.argtypes = [ctypes.POINTER(K.KvrConfig), ctypes.c_uint64] + [ctypes.c_void_p] * 9 + [ctypes.c_uint32]
+        _lib.emul_pipe_unsafe.restype = ctypes.c_uint64
+        _lib.emul_pipe_steps.restype = ctypes.c_uint64
         _lib.emul_draw_index.restype = ctypes.c_uint32
         _lib.emul_draw_index.argtypes = [ctypes.c_uint64, ctypes.c_uint32]
         _lib.emul_draw_index_decided.restype = ctypes.c_int
@@ -63,4 +65,5 @@ def run(stream, R, W, B, all_hits=True, ws=None, ucap=8192, **cfg):
                         ws.ctypes.data if ws is not None else None, ucap)
     flat = K._stats_dicts(st, R * W)
     return {"rc": rc, "route": route, "hits": hits, "all_hits": ah,
-            "workers": [flat[r * W:(r + 1) * W] for r in range(R)]}
+            "workers": [flat[r * W:(r + 1) * W] for r in range(R)],
+            "pipe_unsafe": int(lib().emul_pipe_unsafe()), "pipe_steps": int(lib().emul_pipe_steps())}

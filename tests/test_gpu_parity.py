@@ -525,3 +525,26 @@ def test_two_live_contexts_with_different_lds_needs():
     assert_parity(s2, res["b"], res["b_stats"], W2, B2, range(2))
     assert sum(w["evictions"] for w in res["a_stats"][0]) > 0
     assert sum(w["evictions"] for w in res["b_stats"][0]) > 0
+
+
+def test_phase_timers_change_nothing_but_the_ticks():
+    """phase_timers = 1 builds the step kernel with the routing wave's
+    per-part timers: the same routes, hits and state as the oracle, and
+    every part of the step timed (ticks > 0 in total)."""
+    s = generate(small_spec(n=300, groups=6, prefix_len=(10, 80), suffix_len=(5, 40), vocab=40, seed=5))
+    R, W, B = 4, 3, 300
+    sim = K.Simulator(R, W, B, s.max_len, phase_timers=1)
+    try:
+        res = sim.run(s, batch=97, all_hits=True)
+        st, bits = sim.check()
+        reps, stats = sim.replica_stats(check=False)
+    finally:
+        sim.close()
+    res["status"], res["bits"] = st, bits
+    assert_parity(s, res, stats, W, B, replicas=range(R))
+    for rep in reps:
+        assert rep["queries"] == s.n
+        assert sum(rep["phase_ticks"]) > 0
+        # the evictions: on the evicting wave (pipelined kernel) or the routing wave
+        assert (rep["phase_ticks"][K.PHASE_NAMES.index("e_evict")] +
+                rep["phase_ticks"][K.PHASE_NAMES.index("evict")]) > 0

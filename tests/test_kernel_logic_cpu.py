@@ -43,6 +43,23 @@ def test_random_instances(block):
         _compare(s, 2, W, B, update=["nlms", "rls", "none"][case % 3], seed=case)
 
 
+def test_pipelined_order_takes_both_branches_of_the_early_match():
+    """The pipelined kernel matches the next query on the routed worker
+    before the evictions; that match is exact when it stays on the inserted
+    path, otherwise it is taken again after them.  On small vocabularies both
+    happen often; the replay checks every early match that it keeps against
+    the post-eviction one, and the whole run against the oracle."""
+    unsafe = steps = 0
+    rng = np.random.default_rng(5)
+    for case in range(30):
+        s = generate(small_spec(n=200, groups=int(rng.integers(2, 8)), prefix_len=(2, 30), suffix_len=(1, 20),
+                                vocab=int(rng.integers(2, 8)), seed=300 + case))
+        e = _compare(s, 2, int(rng.integers(1, 5)), int(max(s.max_len, rng.integers(20, 120))), seed=case)
+        unsafe += e["pipe_unsafe"]
+        steps += e["pipe_steps"]
+    assert steps > 1000 and 0 < unsafe < steps, (unsafe, steps)
+
+
 def test_collector_stress():
     s = generate(small_spec(n=400, groups=6, prefix_len=(10, 60), suffix_len=(5, 40), vocab=30))
     B = 300
