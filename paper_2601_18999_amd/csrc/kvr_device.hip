@@ -76,10 +76,10 @@ __device__ __forceinline__ void count_matched(const Ptrs& P, int32_t h, int32_t*
 // in aligned 16-byte blocks of four tokens, eight blocks per thread in flight;
 // the first and last block may reach up to three tokens outside the query,
 // inside the same aligned 16 bytes, and those are not staged.
+template <int kUnroll = 8>  // blocks in flight per thread
 __device__ __forceinline__ void stage_next(const int32_t* tokens, uint64_t n0, int32_t Ln, int32_t* qn,
                                            const int32_t* qc, int32_t Lc, uint32_t t0, uint32_t stride,
                                            int32_t* ell) {
-  constexpr int kUnroll = 8;  // blocks in flight per thread
   const uintptr_t sa = reinterpret_cast<uintptr_t>(tokens + n0);
   const int32_t lead = (int32_t)((sa & 15u) >> 2);
   const int4* base = reinterpret_cast<const int4*>(sa - (uintptr_t)lead * 4u);
@@ -668,6 +668,72 @@ __device__ __forceinline__ bool pipe_wait(const uint32_t* p, uint32_t target, Pi
   }
 }
 
+// Root filters of the pipelined kernel: per worker a 256-bit Bloom filter
+// (in LDS) of the first tokens of its root's children, two bits per token,
+// built when the kernel starts and extended when an insertion adds a child
+// to the root.  A clear bit proves that no cached path starts with the
+// token, so a match that starts at the root is 0 without a memory access; a
+// set bit (also one left by a child evicted since) only means the tree is
+// walked.
+constexpr uint32_t kRootFilterWords = 8;
+
+__device__ __forceinline__ uint32_t rf_bit1(int32_t t) { return ((uint32_t)t * 0x9E3779B1u) >> 24; }
+__device__ __forceinline__ uint32_t rf_bit2(int32_t t) { return ((uint32_t)t * 0x85EBCA6Bu + 0x632BE5ABu) >> 24; }
+
+__device__ __forceinline__ void rf_add(uint32_t* rf, int32_t t) {
+  atomicOr(&rf[rf_bit1(t) >> 5], 1u << (rf_bit1(t) & 31u));
+  atomicOr(&rf[rf_bit2(t) >> 5], 1u << (rf_bit2(t) & 31u));
+}
+
+__device__ __forceinline__ bool rf_may(const uint32_t* rf, int32_t t) {
+  return ((rf[rf_bit1(t) >> 5] >> (rf_bit1(t) & 31u)) & 1u) && ((rf[rf_bit2(t) >> 5] >> (rf_bit2(t) & 31u)) & 1u);
+}
+
+// h of qn[0, Ln) on a worker from its recorded path (match_incremental);
+// sel = the active semispace, or -1 to read it from the header when the tree
+// is walked.  A match that would start at the root is settled by the root
+// filter when it rules out qn[0].
+__device__ __forceinline__ int32_t match_pipe(const Ptrs& P, int32_t sel, const uint32_t* rf, const int32_t* qn,
+                                              int32_t Ln, int32_t h_old, int32_t ell, const PathRef& pr) {
+  if ((ell == 0 || *pr.cnt > kPathMax) && !rf_may(rf, qn[0])) {
+    if (lane_id() == 0) *pr.cnt = 0;
+    return 0;
+  }
+  if (sel < 0) return match_incremental_lazy<kPipeMatchUnroll>(P, qn, Ln, h_old, ell, pr);
+  return match_incremental<kPipeMatchUnroll>(P, (uint32_t)sel, qn, Ln, h_old, ell, pr);
+}
+
+// The next query's h on the workers other than the routed one (best) of
+// query parity cur, taken one item at a time from the LDS counter; the
+// worker being evicted is left to the evicting wave, and every other is
+// claimed first (the evicting wave may have taken it).  Returns the number
+// of matches done (the caller publishes them).
+__device__ __forceinline__ uint32_t take_matches_pipe(const StepArgs& a, uint32_t r, uint32_t W, uint32_t cur,
+                                                      uint32_t best, uint32_t prev, const int32_t* qn, int32_t Ln,
+                                                      int32_t ell, const int32_t* h_cur, int32_t* h_next, PipeFlags* f,
+                                                      unsigned long long* mtok, const uint32_t* rootf,
+                                                      const PathArea& paths) {
+  uint32_t mine = 0;
+  for (uint32_t it = 0; it < W; ++it) {
+    uint32_t got = 0;
+    if (lane_id() == 0) got = atomicAdd(&f->next[cur], 1u);
+    const uint32_t item = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
+    if (item >= W) break;
+    const uint32_t w = (prev + 1u + item) % W;
+    if (w == best) continue;
+    if (__hip_atomic_load(&f->ework, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP) == w) continue;
+    unsigned long long old = 0ull;
+    if (lane_id() == 0) old = atomicOr(&f->claim[cur], 1ull << w);
+    const uint32_t taken = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((old >> w) & 1ull), 0);
+    if (taken) continue;
+    Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
+    count_mtok(mtok, w, match_pipe(Pw, -1, rootf + w * kRootFilterWords, qn, Ln, h_cur[w], ell, paths.of(w)),
+               &h_next[w]);
+    ++mine;
+  }
+  return mine;
+}
+
 template <bool PT>
 __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
   // dynamic LDS: two query buffers, the draw words of two insertions, the
@@ -679,9 +745,11 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
   PathArea paths;
   paths.base = reinterpret_cast<int32_t*>(rwb + 2 * a.rcap);
   paths.W = W;
+  // root filters (kRootFilterWords words per worker), then the candidates
+  uint32_t* rootf = reinterpret_cast<uint32_t*>(paths.base + (size_t)W * (3 * kPathMax + 1));
   UStage ustage;
   {
-    int32_t* ub = paths.base + (size_t)W * (3 * kPathMax + 1);
+    int32_t* ub = reinterpret_cast<int32_t*>(rootf + (size_t)W * kRootFilterWords);
     ustage.node = ub;
     ustage.len = ub + a.ucap;
     ustage.top = ub + 2 * a.ucap;
@@ -734,6 +802,7 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
     for (uint32_t i = 0; i < kMaxWorkers; ++i) mtok_sh[i] = 0ull;
     for (int p = 0; p < KVR_PHASES; ++p) eticks_sh[p] = 0;
   }
+  for (uint32_t x = threadIdx.x; x < W * kRootFilterWords; x += blockDim.x) rootf[x] = 0u;
   __syncthreads();
   if (f.stop) return;
 
@@ -744,6 +813,13 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
     for (int32_t x = (int32_t)threadIdx.x; x < L0; x += (int32_t)blockDim.x) smem[x] = a.tokens[o0 + x];
     if (wave == 0 && (uint32_t)lane < W)
       complete_and_decay(a.C, worker_ptrs(a.ws, a.L, r, (uint32_t)lane), a.arrival[0], rh->tprev);
+    // the root filters: the first token of every child of every root
+    for (uint32_t i = wave; i < W; i += nwaves) {
+      Ptrs P = worker_ptrs(a.ws, a.L, r, i);
+      const int32_t* ar = arena_of(P, P.hdr->arena_sel);
+      const NodeRec root = P.nodes[0];
+      for (int32_t c = lane; c < root.nchild; c += KVR_WAVE) rf_add(rootf + i * kRootFilterWords, ar[root.coff + 2 * c]);
+    }
     __syncthreads();
     for (uint32_t i = wave; i < W; i += nwaves) {
       Ptrs P = worker_ptrs(a.ws, a.L, r, i);
@@ -776,7 +852,20 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
       const int32_t Ln = has_next ? (int32_t)(a.offsets[k + 2] - a.offsets[k + 1]) : 0;
       int32_t* qs = smem + cur * qstride;
       const int32_t* qn = smem + (cur ^ 1u) * qstride;
-      // h of q_k on every worker, completions and decay at its arrival
+      // h of q_k on every worker (taking any match no other wave has taken
+      // yet), completions and decay at its arrival
+      if (k > 0) {
+        const uint32_t pc = cur ^ 1u;
+        const int32_t Lprev = (int32_t)(a.offsets[k] - a.offsets[k - 1]);
+        const int32_t ellp = ell_sh[pc];
+        const int32_t ell_r = ellp < Lp ? ellp : Lp;
+        const int32_t ell = ell_r < Lprev ? ell_r : Lprev;
+        const uint32_t prev = k > 1 ? (uint32_t)best_sh[cur] : 0u;
+        const uint32_t mine = take_matches_pipe(a, r, W, pc, (uint32_t)best_sh[pc], prev, qs, Lp, ell, h_sh[pc],
+                                                h_sh[cur], &f, mtok_sh, rootf, paths);
+        if (mine) add_rel(&f.matched, mine);
+        clock_mark<PT>(&clk, KVR_PHASE_MATCH);
+      }
       if (k > 0 && !pipe_wait(&f.matched, k * (W - 1), &f, g, r, jg, 0)) break;
       if (!pipe_wait(&f.decayed, k + 1, &f, g, r, jg, 1)) break;
       if (redo) {
@@ -785,7 +874,7 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
         clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
         Ptrs Pw = worker_ptrs(a.ws, a.L, r, redo_w);
         count_mtok(mtok_sh, redo_w,
-                   match_incremental<kPipeMatchUnroll>(Pw, Pw.hdr->arena_sel, qs, Lp, redo_L, redo_ell, paths.of(redo_w)),
+                   match_pipe(Pw, -1, rootf + redo_w * kRootFilterWords, qs, Lp, redo_L, redo_ell, paths.of(redo_w)),
                    &h_sh[cur][redo_w]);
         clock_mark<PT>(&clk, KVR_PHASE_MATCH);
         redo = false;
@@ -869,6 +958,8 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
           break;
         }
       }
+      // a new child of the root: its first token joins the root filter
+      if (hb == 0 && lane == 0) rf_add(rootf + best * kRootFilterWords, qs[0]);
       // q_k's buffer is free: q_k+2 may be staged (its LCP with q_k+1 goes to
       // the slot of LCP(q_k-1, q_k), which nothing reads any more)
       if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
@@ -880,7 +971,8 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
         clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
         const int32_t ellp = ell_sh[cur];
         const int32_t ell_r = ellp < Ln ? ellp : Ln;
-        const int32_t h = match_incremental<kPipeMatchUnroll>(P, job.s.arena_sel, qn, Ln, Lp, ell_r, paths.of(best));
+        const int32_t h = match_pipe(P, (int32_t)job.s.arena_sel, rootf + best * kRootFilterWords, qn, Ln, Lp, ell_r,
+                                     paths.of(best));
         if (job.nev == 0 || h == ell_r) {
           count_mtok(mtok_sh, best, h, &h_sh[cur ^ 1u][best]);
         } else {
@@ -986,8 +1078,8 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
             const int32_t ell = ell_r < Ls ? ell_r : Ls;
             Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
             count_mtok(mtok_sh, w,
-                       match_incremental_lazy<kPipeMatchUnroll>(Pw, smem + (sc ^ 1u) * qstride, Lnx, h_sh[sc][w], ell,
-                                                                paths.of(w)),
+                       match_pipe(Pw, -1, rootf + w * kRootFilterWords, smem + (sc ^ 1u) * qstride, Lnx, h_sh[sc][w],
+                                  ell, paths.of(w)),
                        &h_sh[sc ^ 1u][w]);
             add_rel(&f.matched, 1u);
           }
@@ -1068,27 +1160,8 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
         const int32_t ell = ell_r < Lp ? ell_r : Lp;
         const uint32_t prev = k > 0 ? (uint32_t)best_sh[cur ^ 1u] : 0u;
         bool ok = true;
-        uint32_t mine = 0;
-        for (uint32_t it = 0; it < W; ++it) {
-          uint32_t got = 0;
-          if (lane == 0) got = atomicAdd(&f.next[cur], 1u);
-          const uint32_t item = (uint32_t)__builtin_amdgcn_readlane((int)got, 0);
-          if (item >= W) break;
-          const uint32_t w = (prev + 1u + item) % W;
-          if (w == best) continue;
-          // the worker being evicted: its match is the evicting wave's, when
-          // its evictions end; any other is claimed here (unless that wave
-          // took it first)
-          if (__hip_atomic_load(&f.ework, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP) == w) continue;
-          unsigned long long old = 0ull;
-          if (lane == 0) old = atomicOr(&f.claim[cur], 1ull << w);
-          const uint32_t taken = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((old >> w) & 1ull), 0);
-          if (taken) continue;
-          Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
-          count_mtok(mtok_sh, w, match_incremental_lazy<kPipeMatchUnroll>(Pw, qn, Ln, h_sh[cur][w], ell, paths.of(w)),
-                     &h_sh[cur ^ 1u][w]);
-          ++mine;
-        }
+        const uint32_t mine = take_matches_pipe(a, r, W, cur, best, prev, qn, Ln, ell, h_sh[cur], h_sh[cur ^ 1u], &f,
+                                                mtok_sh, rootf, paths);
         // this wave's matches, published at once
         add_rel(&f.matched, mine);
         clock_mark<PT>(&clk, KVR_PHASE_H_MATCH);
@@ -1208,11 +1281,12 @@ size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, u
 
 
 // Dynamic LDS of the pipelined step kernel: two query buffers, the draw
-// words of two insertions (rcap each), the match paths, ucap staged
-// candidates.
+// words of two insertions (rcap each), the match paths, the root filters,
+// ucap staged candidates.
 size_t step_lds_bytes_pipe(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap) {
   return 2 * (size_t)((maxL + 3u) & ~3u) * sizeof(int32_t) + 2 * (size_t)rcap * sizeof(uint32_t) +
-         (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)ucap * 4u * sizeof(int32_t);
+         (size_t)W * (3 * kPathMax + 1) * sizeof(int32_t) + (size_t)W * kRootFilterWords * sizeof(uint32_t) +
+         (size_t)ucap * 4u * sizeof(int32_t);
 }
 
 hipError_t launch_init(char* ws, const Layout& L, double rls_p0, hipStream_t st) {
