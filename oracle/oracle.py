@@ -79,37 +79,53 @@ class OrcRunOpts(ctypes.Structure):
     ]
 
 
-def build(force: bool = False) -> str:
-    """Compile the oracle with g++ (plain C++17, no FMA contraction)."""
-    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
-        tmp = LIB + ".tmp"
-        subprocess.check_call(["g++", "-std=c++17", "-O2", "-ffp-contract=off", "-fPIC",
-                               "-shared", "-o", tmp, SRC])
-        os.replace(tmp, LIB)
-    return LIB
+def build(force: bool = False, sanitize: bool = False) -> str:
+    """Compile the oracle with g++ (plain C++17, no FMA contraction); with
+    sanitize, an AddressSanitizer + UndefinedBehaviorSanitizer build (load it
+    in a process that preloads the ASan runtime)."""
+    out = LIB if not sanitize else LIB.replace(".so", "_asan.so")
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(SRC):
+        tmp = out + ".tmp"
+        flags = ["-std=c++17", "-O2", "-ffp-contract=off", "-fPIC", "-shared"]
+        if sanitize:
+            flags += ["-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"]
+        subprocess.check_call(["g++", *flags, "-o", tmp, SRC])
+        os.replace(tmp, out)
+    return out
 
 
 _lib: Optional[ctypes.CDLL] = None
 
 
+def _bind(l: ctypes.CDLL) -> ctypes.CDLL:
+    l.orc_run.restype = ctypes.c_int
+    l.orc_run.argtypes = [ctypes.POINTER(OrcConfig), ctypes.c_uint32, ctypes.c_uint64,
+                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                          ctypes.POINTER(OrcWorkerStats)]
+    l.orc_run_ex.restype = ctypes.c_int
+    l.orc_run_ex.argtypes = list(l.orc_run.argtypes) + [ctypes.POINTER(OrcRunOpts)]
+    l.orc_check_selftest.restype = ctypes.c_int
+    l.orc_check_selftest.argtypes = [ctypes.c_int]
+    l.orc_philox4x64_10.restype = None
+    l.orc_philox4x64_10.argtypes = [ctypes.c_void_p] * 3
+    l.orc_pow_int.restype = ctypes.c_double
+    l.orc_pow_int.argtypes = [ctypes.c_double, ctypes.c_uint64]
+    return l
+
+
 def lib() -> ctypes.CDLL:
     global _lib
     if _lib is None:
-        _lib = ctypes.CDLL(build())
-        _lib.orc_run.restype = ctypes.c_int
-        _lib.orc_run.argtypes = [ctypes.POINTER(OrcConfig), ctypes.c_uint32, ctypes.c_uint64,
-                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                 ctypes.POINTER(OrcWorkerStats)]
-        _lib.orc_run_ex.restype = ctypes.c_int
-        _lib.orc_run_ex.argtypes = list(_lib.orc_run.argtypes) + [ctypes.POINTER(OrcRunOpts)]
-        _lib.orc_check_selftest.restype = ctypes.c_int
-        _lib.orc_check_selftest.argtypes = [ctypes.c_int]
-        _lib.orc_philox4x64_10.restype = None
-        _lib.orc_philox4x64_10.argtypes = [ctypes.c_void_p] * 3
-        _lib.orc_pow_int.restype = ctypes.c_double
-        _lib.orc_pow_int.argtypes = [ctypes.c_double, ctypes.c_uint64]
+        _lib = _bind(ctypes.CDLL(build()))
     return _lib
+
+
+def use_library(path: str) -> None:
+    """Route every call of this module to another build of the oracle (the
+    sanitized one)."""
+    global _lib
+    _lib = _bind(ctypes.CDLL(path))
 
 
 DEFAULTS: Dict[str, Any] = dict(
