@@ -265,6 +265,21 @@ kvr_status kvr_route_batch(kvr_ctx* ctx, uint32_t n, const int32_t* d_tokens,
 kvr_status kvr_stats(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica_count,
                      kvr_worker_stats* h_workers, size_t worker_count);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * records as kvr_stats, computed without allocating anything and without the
+ * workspace's statistics scratch.  The digest walks use a static device array
+ * of the library (32 MiB per device, held until the process ends): workers
+ * are processed in groups that fit it, and a configuration whose single
+ * worker needs more (16 bytes per node of its tree, plus its record) is
+ * refused with KVR_EINVAL.  h_workers is required (the replica sums come
+ * from it); h_replicas may be NULL.  Every call on a device shares that
+ * array: calls that overlap on one device (other threads, other contexts on
+ * the same device) race and must be serialised by the caller.  Synchronous;
+ * returns the device status as kvr_check does. */
+kvr_status kvr_stats_noalloc(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica_count,
+                             kvr_worker_stats* h_workers, size_t worker_count);
+
 /* Synchronise the stream and return the sticky device status as a
  * kvr_status; *h_bits (optional) receives the raw KVR_DEV_* bits. */
 kvr_status kvr_check(kvr_ctx* ctx, uint32_t* h_bits);

@@ -27,7 +27,7 @@ PHASE_NAMES = ["route", "stage_wait", "mark", "load", "evict", "finish", "match"
                "e_evict", "e_finish", "e_idle", "h_stage", "h_wait", "h_draw", "h_other", "h_match"]
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
-            "kvr_stats", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
+            "kvr_stats", "kvr_stats_noalloc", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]
 
 
 class KvrConfig(ctypes.Structure):
@@ -128,6 +128,9 @@ def load_library() -> ctypes.CDLL:
     lib.kvr_stats.restype = ctypes.c_int
     lib.kvr_stats.argtypes = [vp, ctypes.POINTER(KvrReplicaStats), ctypes.c_size_t,
                               ctypes.POINTER(KvrWorkerStats), ctypes.c_size_t]
+    lib.kvr_stats_noalloc.restype = ctypes.c_int
+    lib.kvr_stats_noalloc.argtypes = [vp, ctypes.POINTER(KvrReplicaStats), ctypes.c_size_t,
+                                      ctypes.POINTER(KvrWorkerStats), ctypes.c_size_t]
     lib.kvr_check.restype = ctypes.c_int
     lib.kvr_check.argtypes = [vp, ctypes.POINTER(u32)]
     lib.kvr_queries_done.restype = u64
@@ -223,6 +226,18 @@ def kvr_stats(ctx: int, R: int, W: int, check: bool = True, with_replicas: bool 
     if with_replicas:
         return _replica_dicts(rep, R), workers
     return workers
+
+
+def kvr_stats_noalloc(ctx: int, R: int, W: int, check: bool = True):
+    """kvr_stats without any allocation by the library: (replicas [R],
+    workers [R][W])."""
+    arr = (KvrWorkerStats * (R * W))()
+    rep = (KvrReplicaStats * R)()
+    st = load_library().kvr_stats_noalloc(ctypes.c_void_p(ctx), rep, R, arr, R * W)
+    if check:
+        _check(st, "kvr_stats_noalloc")
+    flat = _stats_dicts(arr, R * W)
+    return _replica_dicts(rep, R), [flat[r * W:(r + 1) * W] for r in range(R)]
 
 
 def kvr_check(ctx: int) -> (int, int):

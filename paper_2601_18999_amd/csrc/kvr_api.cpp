@@ -23,6 +23,9 @@ hipError_t set_step_lds_limit(size_t bytes);
 hipError_t step_static_lds(size_t* bytes);
 size_t step_lds_bytes(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap, uint32_t path_sets);
 size_t step_lds_bytes_pipe(uint32_t maxL, uint32_t W, uint32_t ucap, uint32_t rcap);
+hipError_t noalloc_scratch(int device, void** ptr, size_t* bytes);
+hipError_t launch_stats_into(char* ws, const Layout& L, uint64_t w0, uint32_t n, uint64_t* fifo, uint64_t fifo_words,
+                             kvr_worker_stats* out, hipStream_t st);
 }  // namespace kvr
 
 struct kvr_ctx {
@@ -38,6 +41,8 @@ struct kvr_ctx {
   uint32_t pipe;       // 1: the pipelined step kernel (a separate evicting wave)
   uint32_t ucap_p;     // its staged candidates
   uint32_t rcap_p;     // its draw words per insertion (two insertions' worth)
+  void* scratch;       // the device's static scratch of kvr_stats_noalloc
+  size_t scratch_bytes;
 };
 
 namespace {
@@ -252,8 +257,16 @@ kvr_status kvr_init_replicas(const kvr_config* cfg, void* d_workspace, size_t by
       if (e != hipSuccess) return fail_hip(e, "hipFuncSetAttribute(max dynamic LDS)");
     }
   }
+  // the static scratch of kvr_stats_noalloc on this device (its address,
+  // looked up once per device, with the device current)
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  e = kvr::noalloc_scratch(dev, &scratch, &scratch_bytes);
+  if (e != hipSuccess) return fail_hip(e, "hipGetSymbolAddress(scratch)");
   kvr_ctx* c = new (std::nothrow) kvr_ctx;
   if (!c) return fail(KVR_ENOMEM, "host allocation failed");
+  c->scratch = scratch;
+  c->scratch_bytes = scratch_bytes;
   c->pipe = pipe ? 1u : 0u;
   c->ucap_p = (uint32_t)ucap_p;
   c->rcap_p = (uint32_t)rcap_p;
@@ -402,6 +415,75 @@ kvr_status kvr_stats(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica
   }
   if (st != KVR_OK) return fail(st, describe_bits(bits));
   return KVR_OK;
+}
+
+kvr_status kvr_stats_noalloc(kvr_ctx* ctx, kvr_replica_stats* h_replicas, size_t replica_count,
+                             kvr_worker_stats* h_workers, size_t worker_count) {
+  if (!ctx) return fail(KVR_EINVAL, "ctx is NULL");
+  const size_t R = ctx->L.R, RW = (size_t)ctx->L.R * ctx->L.W;
+  if (!h_workers) return fail(KVR_EINVAL, "h_workers is NULL (kvr_stats_noalloc needs it)");
+  if (worker_count < RW)
+    return fail(KVR_EINVAL, "h_workers holds " + std::to_string(worker_count) + " entries, the context has " +
+                                std::to_string(RW));
+  if (h_replicas && replica_count < R)
+    return fail(KVR_EINVAL, "h_replicas holds " + std::to_string(replica_count) + " entries, the context has " +
+                                std::to_string(R) + " replicas");
+  if (!ctx->scratch) return fail(KVR_EDEVICE, "no static scratch on this device");
+  // per worker: the digest walk's FIFO (two words per node the tree can
+  // hold, the router's tree included) and its record
+  const uint64_t nodes = ctx->L.has_router && ctx->L.NCr > ctx->L.NC ? ctx->L.NCr : ctx->L.NC;
+  const uint64_t fifo_words = 2ull * nodes;
+  const uint64_t per = fifo_words * 8ull + sizeof(kvr_worker_stats);
+  const uint64_t m = ctx->scratch_bytes / per;
+  if (m == 0)
+    return fail(KVR_EINVAL, "the digest walk of one worker needs " + std::to_string(per) +
+                                " bytes of scratch; kvr_stats_noalloc has " + std::to_string(ctx->scratch_bytes) +
+                                " (use kvr_stats)");
+  uint32_t bits = 0;
+  kvr_status st = kvr_check(ctx, &bits);
+  uint64_t* fifo = static_cast<uint64_t*>(ctx->scratch);
+  kvr_worker_stats* recs =
+      reinterpret_cast<kvr_worker_stats*>(static_cast<char*>(ctx->scratch) + m * fifo_words * 8ull);
+  for (uint64_t w0 = 0; w0 < RW; w0 += m) {
+    const uint32_t n = (uint32_t)(RW - w0 < m ? RW - w0 : m);
+    hipError_t e = kvr::launch_stats_into(ctx->ws, ctx->L, w0, n, fifo, fifo_words, recs, ctx->stream);
+    if (e != hipSuccess) return fail_hip(e, "stats kernel launch");
+    e = hipMemcpyAsync(h_workers + w0, recs, n * sizeof(kvr_worker_stats), hipMemcpyDeviceToHost, ctx->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync(stats)");
+    e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  }
+  if (h_replicas) {
+    for (size_t r = 0; r < R; ++r) {
+      kvr::ReplicaHdr rh;
+      hipError_t e = hipMemcpy(&rh, ctx->ws + ctx->L.off_rhdr + r * sizeof(kvr::ReplicaHdr), sizeof(rh),
+                               hipMemcpyDeviceToHost);
+      if (e != hipSuccess) return fail_hip(e, "hipMemcpy(replica header)");
+      kvr_replica_stats o;
+      std::memset(&o, 0, sizeof(o));
+      o.queries = rh.queries;
+      o.route_digest = rh.route_digest;
+      o.last_arrival_us = rh.tprev;
+      for (int k = 0; k < KVR_PHASES; ++k) o.phase_ticks[k] = rh.phase_ticks[k];
+      for (size_t i = 0; i < ctx->L.W; ++i) {
+        const kvr_worker_stats& w = h_workers[r * ctx->L.W + i];
+        o.prompt_tokens += w.prompt_tokens;
+        o.hit_tokens += w.hit_tokens;
+        o.matched_tokens += w.matched_tokens;
+        o.loads += w.loads;
+        o.evictions += w.evictions;
+        o.completions += w.completions;
+        o.latency_sum_us += w.latency_sum_us;
+        if (w.latency_max_us > o.latency_max_us) o.latency_max_us = w.latency_max_us;
+      }
+      h_replicas[r] = o;
+    }
+  }
+  // the walks' own consistency checks
+  uint32_t bits2 = 0;
+  const kvr_status st2 = kvr_check(ctx, &bits2);
+  if (st != KVR_OK) return fail(st, describe_bits(bits));
+  return st2;
 }
 
 uint64_t kvr_queries_done(const kvr_ctx* ctx) { return ctx ? ctx->queries_done : 0; }

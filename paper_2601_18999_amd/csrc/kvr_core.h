@@ -2567,13 +2567,15 @@ __device__ __forceinline__ uint64_t wave_xor_u64(uint64_t v) {
 // the node's children with the edge's last hash.  Long and short edges so
 // share the wave.  Returns false on an inconsistent tree (the counts are
 // then partial).
-__device__ bool worker_stats(const Ptrs& P, kvr_worker_stats* out) {
+__device__ bool worker_stats(const Ptrs& P, kvr_worker_stats* out, uint64_t* fifo = nullptr, uint64_t fifo_cap = 0) {
   constexpr int kTok = 16;
   const WorkerHdr* h = P.hdr;
   const St s = load_st(h);
   const int32_t* ar = arena_of(P, s.arena_sel);
-  uint64_t* q = P.scratch;  // entry e: q[2e] = node, q[2e + 1] = hash before its edge
-  const uint64_t cap = P.NC;
+  // the FIFO (entry e: q[2e] = node, q[2e + 1] = hash before its edge): the
+  // worker's scratch region, or the caller's
+  uint64_t* q = fifo ? fifo : P.scratch;
+  const uint64_t cap = fifo ? fifo_cap : P.NC;
   uint64_t count = 0, dsum = 0, dxor = 0, mcount = 0, msum = 0;
   if (lane_id() == 0) {
     q[0] = 0;

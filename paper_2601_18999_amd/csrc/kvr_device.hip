@@ -42,6 +42,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "kvr_core.h"
 
 namespace kvr {
@@ -1248,25 +1250,30 @@ __global__ void validate_tokens_kernel(char* ws, Layout L, const int32_t* tokens
   if (__ballot(bad != 0) && lane_id() == 0) atomicOr(&g->status, (uint32_t)KVR_DEV_BAD_TOKEN);
 }
 
-// Final state of every (replica, worker): one wave each.  An inconsistent
-// tree (the digest walk could not finish) raises KVR_DEV_INTERNAL.
-__global__ void __launch_bounds__(64) stats_kernel(char* ws, Layout L) {
-  const uint64_t widx = blockIdx.x;
+// Final state of every (replica, worker): one wave each, for the workers
+// w0 .. w0 + gridDim.x - 1 (index r * W + i).  The digest walk's FIFO is
+// fifo + (widx - w0) * fifo_words (fifo_words / 2 entries), or the worker's
+// scratch region when fifo is null; the records go to out[widx - w0].  An
+// inconsistent tree or a FIFO too short raises KVR_DEV_INTERNAL.
+__global__ void __launch_bounds__(64) stats_kernel(char* ws, Layout L, uint64_t w0, uint64_t* fifo,
+                                                   uint64_t fifo_words, kvr_worker_stats* out) {
+  const uint64_t widx = w0 + blockIdx.x;
   const uint32_t r = (uint32_t)(widx / L.W), i = (uint32_t)(widx % L.W);
-  kvr_worker_stats* out = reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats) + widx;
-  bool ok = worker_stats(worker_ptrs(ws, L, r, i), out);
+  kvr_worker_stats* o = out + blockIdx.x;
+  uint64_t* q = fifo ? fifo + (uint64_t)blockIdx.x * fifo_words : nullptr;
+  bool ok = worker_stats(worker_ptrs(ws, L, r, i), o, q, fifo_words / 2);
   if (L.has_router) {
-    // the router's tree of the worker (its walk reuses the worker's scratch
-    // once the cache's is done): contents digest and evictions
+    // the router's tree of the worker (its walk reuses the same FIFO once
+    // the cache's is done): contents digest and evictions
     wave_mem_sync();
     Ptrs Pr = router_ptrs(ws, L, r, i);
     kvr_worker_stats t;
-    ok = worker_stats(Pr, &t) && ok;
+    ok = worker_stats(Pr, &t, q, fifo_words / 2) && ok;
     if (lane_id() == 0) {
-      out->router_resident = t.resident;
-      out->router_digest_sum = t.digest_sum;
-      out->router_digest_xor = t.digest_xor;
-      out->router_evictions = Pr.hdr->evictions;
+      o->router_resident = t.resident;
+      o->router_digest_sum = t.digest_sum;
+      o->router_digest_xor = t.digest_xor;
+      o->router_evictions = Pr.hdr->evictions;
     }
   }
   if (!ok && lane_id() == 0) atomicOr(&reinterpret_cast<GlobalHdr*>(ws + L.off_global)->status, (uint32_t)KVR_DEV_INTERNAL);
@@ -1330,7 +1337,47 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_stats(char* ws, const Layout& L, hipStream_t st) {
-  hipLaunchKernelGGL(stats_kernel, dim3(L.R * L.W), dim3(64), 0, st, ws, L);
+  hipLaunchKernelGGL(stats_kernel, dim3(L.R * L.W), dim3(64), 0, st, ws, L, 0ull, nullptr, 0ull,
+                     reinterpret_cast<kvr_worker_stats*>(ws + L.off_stats));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- allocation-free statistics
+//
+// kvr_stats_noalloc keeps the digest walk's FIFO and the staged records in
+// this array instead of the workspace; one copy per device, for the life of
+// the process.  Host code uses its address from hipGetSymbolAddress, never
+// its name.
+constexpr size_t kScratchBytes = 32ull << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// The device address of `scratch` on the current device (looked up once per
+// device).
+hipError_t noalloc_scratch(int device, void** ptr, size_t* bytes) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = p;
+  }
+  *ptr = g_scratch_ptr[device];
+  *bytes = kScratchBytes;
+  return hipSuccess;
+}
+
+// Workers w0 .. w0 + n - 1 with their FIFOs (fifo_words each) and records
+// in caller-given device memory.
+hipError_t launch_stats_into(char* ws, const Layout& L, uint64_t w0, uint32_t n, uint64_t* fifo, uint64_t fifo_words,
+                             kvr_worker_stats* out, hipStream_t st) {
+  hipLaunchKernelGGL(stats_kernel, dim3(n), dim3(64), 0, st, ws, L, w0, fifo, fifo_words, out);
   return hipGetLastError();
 }
 
