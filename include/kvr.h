@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 7u
+#define KVR_ABI_VERSION 8u
 
 typedef enum kvr_status {
   KVR_OK = 0,
@@ -175,8 +175,8 @@ typedef struct kvr_worker_stats {
 /* Parts of a step timed with phase_timers = 1 (kvr_replica_stats.phase_ticks):
  * ticks of the routing wave (0-8) and, when a separate evicting wave runs
  * the evictions of each insertion while the routing wave goes on to the
- * next query, of the evicting wave (9-11) and of the helper waves, summed
- * over them (12-16). */
+ * next query, of the evicting wave (9-11, 17) and of the helper waves,
+ * summed over them (12-16). */
 enum {
   KVR_PHASE_ROUTE = 0,        /* scores, argmin and commit (Algorithm 2 routing thread) */
   KVR_PHASE_STAGE_WAIT = 1,   /* waiting for the next query's staging                  */
@@ -184,7 +184,7 @@ enum {
   KVR_PHASE_LOAD = 3,         /* split, new leaf's rank, edge copy, tree and list edits */
   KVR_PHASE_EVICT = 4,        /* evictions of the loaded tokens (Algorithm 1)          */
   KVR_PHASE_FINISH = 5,       /* marks of the loaded tokens, cache header              */
-  KVR_PHASE_MATCH = 6,        /* the routed worker's h of the next query               */
+  KVR_PHASE_MATCH = 6,        /* h of the next query (routed worker), any left by helpers */
   KVR_PHASE_JOIN = 7,         /* waiting for the other workers' h of the next query    */
   KVR_PHASE_EVICTOR_WAIT = 8, /* waiting for the evicting wave                         */
   KVR_PHASE_E_EVICT = 9,      /* evicting wave: evictions                              */
@@ -195,7 +195,8 @@ enum {
   KVR_PHASE_H_DRAW = 14,      /* helper waves: draw words (Philox4x64-10)              */
   KVR_PHASE_H_OTHER = 15,     /* helper waves: completions, decay, new leaf's rank     */
   KVR_PHASE_H_MATCH = 16,     /* helper waves: h of the next query on the other workers */
-  KVR_PHASES = 17
+  KVR_PHASE_E_MATCH = 17,     /* evicting wave: the routed worker's h of the next query */
+  KVR_PHASES = 18
 };
 
 /* Per-replica state and counters (kvr_stats): the Sec. 5 metrics summed over

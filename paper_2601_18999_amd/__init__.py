@@ -21,10 +21,11 @@ STATUS_NAMES = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_ENOMEM", -3: "KVR_EDEVIC
 KVR_EVICT_RLT, KVR_EVICT_LRU = 0, 1
 KVR_ROUTE_LBGR, KVR_ROUTE_RANDOM, KVR_ROUTE_ROUND_ROBIN, KVR_ROUTE_CACHE_AWARE = 0, 1, 2, 3
 KVR_UPD_NLMS, KVR_UPD_RLS, KVR_UPD_NONE = 0, 1, 2
-KVR_ABI_VERSION = 7
-KVR_PHASES = 17
+KVR_ABI_VERSION = 8
+KVR_PHASES = 18
 PHASE_NAMES = ["route", "stage_wait", "mark", "load", "evict", "finish", "match", "join", "evictor_wait",
-               "e_evict", "e_finish", "e_idle", "h_stage", "h_wait", "h_draw", "h_other", "h_match"]
+               "e_evict", "e_finish", "e_idle", "h_stage", "h_wait", "h_draw", "h_other", "h_match",
+               "e_match"]
 
 EXPORTED = ["kvr_config_default", "kvr_workspace_size", "kvr_init_replicas", "kvr_route_batch",
             "kvr_stats", "kvr_stats_noalloc", "kvr_check", "kvr_queries_done", "kvr_destroy", "kvr_last_error"]

@@ -770,10 +770,14 @@ __device__ __forceinline__ int32_t split_node(const Ptrs& P, St& s, int32_t x, i
   nh.ccap = 2;
   nh.mphase = nx.mphase;
   nh.ma = nx.ma < k ? nx.ma : k;
-  NodeRec nt = nx;
+  NodeRec nt;
   nt.parent = hd;
   nt.off = nx.off + (uint32_t)k;
   nt.len = nx.len - k;
+  nt.nchild = nx.nchild;
+  nt.coff = nx.coff;
+  nt.ccap = nx.ccap;
+  nt.mphase = nx.mphase;
   nt.ma = nx.ma - k > 0 ? nx.ma - k : 0;
   if (s.rnode == x) {
     if (s.rphase != s.phase) {

@@ -616,6 +616,10 @@ constexpr uint32_t kNoWorker = 0xffffffffu;
 #endif
 constexpr int kPipeMatchUnroll = KVR_PIPE_MATCH_UNROLL;
 constexpr uint32_t kSpinLimit = 1u << 24;
+#ifndef KVR_PIPE_WAVES
+#define KVR_PIPE_WAVES 8
+#endif
+constexpr uint32_t kPipeWaves = KVR_PIPE_WAVES;
 
 __device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -737,7 +741,7 @@ __device__ __forceinline__ uint32_t take_matches_pipe(const StepArgs& a, uint32_
 }
 
 template <bool PT>
-__global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
+__global__ void __launch_bounds__(64 * kPipeWaves) step_kernel_pipe(StepArgs a) {
   // dynamic LDS: two query buffers, the draw words of two insertions, the
   // match paths, the staged candidate list
   extern __shared__ int32_t smem[];
@@ -768,6 +772,10 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
   __shared__ uint32_t rank_ready_sh;
   __shared__ PipeFlags f;
   __shared__ EvictJob job_sh[2];            // by insertion count parity
+  // per handed insertion (same parity): the routed worker's h of the next
+  // query not taken yet (0), taken and exact (1), taken but to be taken
+  // again after the evictions (2)
+  __shared__ uint32_t early_sh[2];
   __shared__ unsigned long long eticks_sh[KVR_PHASES];  // evicting and helper waves' ticks
   // matched tokens per worker over the batch (added to the headers at the end)
   __shared__ unsigned long long mtok_sh[kMaxWorkers];
@@ -838,11 +846,6 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
     clock_start<PT>(&clk);
     uint32_t issued = 0;    // insertions handed to the evicting wave
     uint32_t last_job = 0;  // query index (in the batch) of the last one
-    // the routed worker's h of the next query, when it has to be taken again
-    // after the evictions: worker, path length and LCP of the two queries
-    bool redo = false;
-    uint32_t redo_w = 0;
-    int32_t redo_L = 0, redo_ell = 0;
     for (uint32_t k = 0; k < a.n; ++k) {
       const uint32_t cur = k & 1u;
       const uint64_t jg = a.j0 + k;
@@ -868,19 +871,11 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
         if (mine) add_rel(&f.matched, mine);
         clock_mark<PT>(&clk, KVR_PHASE_MATCH);
       }
-      if (k > 0 && !pipe_wait(&f.matched, k * (W - 1), &f, g, r, jg, 0)) break;
+      // every worker's h of q_k: W per query from q_1 on (the routed
+      // worker's from this wave or the evicting wave, the others' from the
+      // helpers, this wave or the evicting wave)
+      if (k > 0 && !pipe_wait(&f.matched, k * W, &f, g, r, jg, 0)) break;
       if (!pipe_wait(&f.decayed, k + 1, &f, g, r, jg, 1)) break;
-      if (redo) {
-        // the evictions of the previous insertion are done before this
-        if (!pipe_wait(&f.evicted, issued, &f, g, r, jg, 2)) break;
-        clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
-        Ptrs Pw = worker_ptrs(a.ws, a.L, r, redo_w);
-        count_mtok(mtok_sh, redo_w,
-                   match_pipe(Pw, -1, rootf + redo_w * kRootFilterWords, qs, Lp, redo_L, redo_ell, paths.of(redo_w)),
-                   &h_sh[cur][redo_w]);
-        clock_mark<PT>(&clk, KVR_PHASE_MATCH);
-        redo = false;
-      }
       clock_mark<PT>(&clk, KVR_PHASE_JOIN);
 
       // the draw words and rounds of this parity are reused below: the
@@ -966,28 +961,22 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
       // the slot of LCP(q_k-1, q_k), which nothing reads any more)
       if (lane == 0) ell_sh[cur ^ 1u] = 0x7fffffff;
       st_rel(&f.top, k + 2);
-      // ---- the routed worker's h of the next query, on the tree after the
-      // load: exact when it ends on the inserted path or nothing is evicted
-      if (has_next) {
-        if (!pipe_wait(&f.staged, (k + 1) * nh, &f, g, r, jg, 4)) break;
-        clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
-        const int32_t ellp = ell_sh[cur];
-        const int32_t ell_r = ellp < Ln ? ellp : Ln;
-        const int32_t h = match_pipe(P, (int32_t)job.s.arena_sel, rootf + best * kRootFilterWords, qn, Ln, Lp, ell_r,
-                                     paths.of(best));
-        if (job.nev == 0 || h == ell_r) {
-          count_mtok(mtok_sh, best, h, &h_sh[cur ^ 1u][best]);
-        } else {
-          redo = true;
-          redo_w = best;
-          redo_L = Lp;
-          redo_ell = ell_r;
-        }
-        clock_mark<PT>(&clk, KVR_PHASE_MATCH);
-      }
-      // ---- the back half: here when nothing is evicted, else on the
-      // evicting wave once it is free
+      // ---- nothing to evict: the routed worker's h of the next query (on
+      // the tree after the load, which is final) and the back half here;
+      // else both on the evicting wave once it is free
       if (job.nev == 0) {
+        if (has_next) {
+          if (!pipe_wait(&f.staged, (k + 1) * nh, &f, g, r, jg, 4)) break;
+          clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
+          const int32_t ellp = ell_sh[cur];
+          const int32_t ell_r = ellp < Ln ? ellp : Ln;
+          count_mtok(mtok_sh, best,
+                     match_pipe(P, (int32_t)job.s.arena_sel, rootf + best * kRootFilterWords, qn, Ln, Lp, ell_r,
+                                paths.of(best)),
+                     &h_sh[cur ^ 1u][best]);
+          add_rel(&f.matched, 1u);
+          clock_mark<PT>(&clk, KVR_PHASE_MATCH);
+        }
         int64_t dbg[4] = {0, 0, 0, 0};
         const uint32_t err = rlt_insert_back<PT>(P, job, ustage, dbg, &clk);
         if (err) {
@@ -995,9 +984,30 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
           break;
         }
       } else {
+        // the evicting wave takes the routed worker's h of the next query
+        // before its evictions; while it still evicts for an earlier
+        // insertion, this wave takes that match here first
+        uint32_t early = 0;
+        if (has_next && ld_acq(&f.evicted) < issued) {
+          if (!pipe_wait(&f.staged, (k + 1) * nh, &f, g, r, jg, 4)) break;
+          clock_mark<PT>(&clk, KVR_PHASE_STAGE_WAIT);
+          const int32_t ellp = ell_sh[cur];
+          const int32_t ell_r = ellp < Ln ? ellp : Ln;
+          const int32_t h = match_pipe(P, (int32_t)job.s.arena_sel, rootf + best * kRootFilterWords, qn, Ln, Lp,
+                                       ell_r, paths.of(best));
+          if (h == ell_r) {
+            count_mtok(mtok_sh, best, h, &h_sh[cur ^ 1u][best]);
+            add_rel(&f.matched, 1u);
+            early = 1;
+          } else {
+            early = 2;
+          }
+          clock_mark<PT>(&clk, KVR_PHASE_MATCH);
+        }
         if (!pipe_wait(&f.evicted, issued, &f, g, r, jg, 5)) break;
         clock_mark<PT>(&clk, KVR_PHASE_EVICTOR_WAIT);
         if (lane == 0) {
+          early_sh[issued & 1u] = early;
           __hip_atomic_store(&f.ework, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
           __hip_atomic_store(&f.ework_size, job.final_size, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
@@ -1050,12 +1060,46 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
       clock_mark<PT>(&clk, KVR_PHASE_E_IDLE);
       const EvictJob& job = job_sh[done & 1u];
       const uint32_t w = job.worker;
+      const Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
+      // the routed worker's h of the next query q_kq+1, first on the tree
+      // after the load: exact when it ends where q_kq+1 leaves the inserted
+      // path (depth LCP(q_kq, q_kq+1), marked, so no eviction shortens it;
+      // no child can match there later, as evictions only remove tokens),
+      // else taken again after the evictions
+      const uint32_t kq = (uint32_t)(job.ia.jg - a.j0);
+      const bool has_next = kq + 1u < a.n;
+      const uint32_t early = early_sh[done & 1u];
+      bool exact = early != 2u;
+      int32_t Lnx = 0, ell_r = 0;
+      const int32_t* qnx = smem + ((kq + 1u) & 1u) * qstride;
+      if (has_next) {
+        if (!pipe_wait(&f.staged, (kq + 1u) * nh, &f, g, r, job.ia.jg, 13)) break;
+        Lnx = (int32_t)(a.offsets[kq + 2] - a.offsets[kq + 1]);
+        const int32_t ellp = ell_sh[kq & 1u];
+        ell_r = ellp < Lnx ? ellp : Lnx;
+      }
+      if (has_next && early == 0u) {
+        const int32_t h = match_pipe(Pw, (int32_t)job.s.arena_sel, rootf + w * kRootFilterWords, qnx, Lnx, job.L,
+                                     ell_r, paths.of(w));
+        exact = h == ell_r;
+        if (exact) {
+          count_mtok(mtok_sh, w, h, &h_sh[(kq + 1u) & 1u][w]);
+          add_rel(&f.matched, 1u);
+        }
+        clock_mark<PT>(&clk, KVR_PHASE_E_MATCH);
+      }
       int64_t dbg[4] = {0, 0, 0, 0};
-      const uint32_t err = rlt_insert_back<PT>(worker_ptrs(a.ws, a.L, r, w), job, ustage, dbg, &clk,
-                                               KVR_PHASE_E_EVICT, KVR_PHASE_E_FINISH);
+      const uint32_t err = rlt_insert_back<PT>(Pw, job, ustage, dbg, &clk, KVR_PHASE_E_EVICT, KVR_PHASE_E_FINISH);
       if (err) {
         pipe_stop(g, &f, r, job.ia.jg, err, dbg);
         break;
+      }
+      if (has_next && !exact) {
+        count_mtok(mtok_sh, w,
+                   match_pipe(Pw, -1, rootf + w * kRootFilterWords, qnx, Lnx, job.L, ell_r, paths.of(w)),
+                   &h_sh[(kq + 1u) & 1u][w]);
+        add_rel(&f.matched, 1u);
+        clock_mark<PT>(&clk, KVR_PHASE_E_MATCH);
       }
       if (lane == 0) __hip_atomic_store(&f.ework, kNoWorker, __ATOMIC_SEQ_CST, __HIP_MEMORY_SCOPE_WORKGROUP);
       done += 1;
@@ -1090,7 +1134,8 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
     }
     if constexpr (PT)
       if (lane == 0)
-        for (int p = KVR_PHASE_E_EVICT; p <= KVR_PHASE_E_IDLE; ++p) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
+        for (int p = KVR_PHASE_E_EVICT; p < KVR_PHASES; ++p)
+          if (p <= KVR_PHASE_E_IDLE || p == KVR_PHASE_E_MATCH) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
   } else {
     // ---------------------------------------------------------- helper waves
     const uint32_t hw = wave - 2u;  // 0 .. nh-1
@@ -1172,7 +1217,7 @@ __global__ void __launch_bounds__(512) step_kernel_pipe(StepArgs a) {
     }
     if constexpr (PT)
       if (lane == 0)
-        for (int p = KVR_PHASE_H_STAGE; p < KVR_PHASES; ++p) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
+        for (int p = KVR_PHASE_H_STAGE; p <= KVR_PHASE_H_MATCH; ++p) atomicAdd(&eticks_sh[p], (unsigned long long)clk.acc[p]);
   }
   __syncthreads();
   if (threadIdx.x < W) worker_ptrs(a.ws, a.L, r, threadIdx.x).hdr->matched_tokens += mtok_sh[threadIdx.x];
@@ -1320,9 +1365,9 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   if (a.pipe) {
     const size_t lds_p = step_lds_bytes_pipe(a.L.maxL, a.L.W, a.ucap, a.rcap);
     if (a.C.phase_timers)
-      hipLaunchKernelGGL((step_kernel_pipe<true>), dim3(a.L.R), dim3(64 * kMaxWavesPerBlock), lds_p, st, a);
+      hipLaunchKernelGGL((step_kernel_pipe<true>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
     else
-      hipLaunchKernelGGL((step_kernel_pipe<false>), dim3(a.L.R), dim3(64 * kMaxWavesPerBlock), lds_p, st, a);
+      hipLaunchKernelGGL((step_kernel_pipe<false>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
   } else if (rt && ba)
     hipLaunchKernelGGL((step_kernel<true, true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   else if (rt)

@@ -101,7 +101,7 @@ struct ReplicaHdr {
   uint64_t queries;       // queries routed
   uint64_t route_digest;  // hash chain over (query index, route, hit), kvr_replica_stats
   uint64_t phase_ticks[KVR_PHASES];
-  uint64_t pad[12];
+  uint64_t pad[11];
 };
 static_assert(sizeof(ReplicaHdr) == 256, "replica header is 256 bytes");
 
