@@ -102,7 +102,8 @@ typedef struct kvr_config {
   uint32_t pending_capacity; /* completion ring per (replica, worker), >= 1; 65536 by default */
   uint32_t node_capacity;    /* nodes per (replica, worker); 0 = cache_tokens + 3  */
   uint32_t arena_words;      /* words per semispace per (replica, worker), 0 = default
-                                8*B + 2*max_query_tokens + 4096; else >= B + 2*max_q + 64 */
+                                min(32*B + 2*max_query_tokens + 4096, 2^32 - 16);
+                                else >= B + 2*max_q + 64                           */
   double alpha_cached;       /* s per 1k cached tokens (App. A: 0)                 */
   double alpha_miss;         /* s per 1k missed tokens (App. A: 1)                 */
   double rho;                /* load decay factor (App. A: 31/32), in (0, 1]       */

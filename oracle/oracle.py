@@ -85,7 +85,7 @@ def build(force: bool = False, sanitize: bool = False) -> str:
     in a process that preloads the ASan runtime)."""
     out = LIB if not sanitize else LIB.replace(".so", "_asan.so")
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(SRC):
-        tmp = out + ".tmp"
+        tmp = f"{out}.{os.getpid()}.tmp"
         flags = ["-std=c++17", "-O2", "-ffp-contract=off", "-fPIC", "-shared"]
         if sanitize:
             flags += ["-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"]

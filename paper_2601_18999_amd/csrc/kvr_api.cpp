@@ -102,9 +102,8 @@ kvr_status validate(const kvr_config* c) {
   const uint64_t min_arena = (uint64_t)c->cache_tokens + 2ull * c->max_query_tokens + 64ull;
   if (c->arena_words != 0 && c->arena_words < min_arena)
     return fail(KVR_EINVAL, "arena_words must be 0 or >= cache_tokens + 2*max_query_tokens + 64");
-  const uint64_t dflt_arena = 8ull * c->cache_tokens + 2ull * c->max_query_tokens + 4096ull;
-  if (c->arena_words == 0 && dflt_arena >= (1ull << 32))
-    return fail(KVR_EINVAL, "cache too large for 32-bit arena offsets");
+  // (the default, 32*B + 2*max_q + 4096 capped at 2^32 - 16, is at least
+  // min_arena for every cache_tokens <= 2^30)
   if (!finite(c->alpha_cached) || !finite(c->alpha_miss))
     return fail(KVR_EINVAL, "alpha_cached/alpha_miss must be finite");
   if (!finite(c->rho) || !(c->rho > 0.0) || c->rho > 1.0) return fail(KVR_EINVAL, "rho must be in (0, 1]");

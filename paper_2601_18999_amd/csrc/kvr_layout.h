@@ -179,9 +179,12 @@ inline Layout make_layout(const kvr_config& c) {
   // every non-root node holds >= 1 token, and an insertion adds at most a split
   // head and the new leaf before its evictions free space: B + 3 always fits
   L.NC = c.node_capacity ? c.node_capacity : c.cache_tokens + 3u;
-  // 8 words per cache token: the live data takes about 1.2 B words, so the
-  // collector runs once per (8 - 1.2) B words appended
-  uint64_t dflt_arena = 8ull * c.cache_tokens + 2ull * c.max_query_tokens + 4096ull;
+  // 32 words per cache token: the live data takes about 1.2 B words, so the
+  // collector (one wave copying the live data) runs once per about 31 B
+  // words appended; HBM holds this easily (two semispaces of 128 B bytes
+  // per worker), and each collection delays its step by tens of us
+  uint64_t dflt_arena = 32ull * c.cache_tokens + 2ull * c.max_query_tokens + 4096ull;
+  if (dflt_arena > 0xfffffff0ull) dflt_arena = 0xfffffff0ull;
   L.A = c.arena_words ? c.arena_words : (uint32_t)dflt_arena;
   L.A &= ~1u;  // even, so child arrays stay 8-byte aligned in both semispaces
   L.PC = c.pending_capacity;

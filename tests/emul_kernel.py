@@ -26,8 +26,10 @@ def build(sanitize: bool = False) -> str:
     flags = ["-std=c++17", "-O1", "-g", "-ffp-contract=off", "-fPIC", "-shared", "-Wno-unknown-pragmas"]
     if sanitize:
         flags += ["-fsanitize=address,undefined", "-fno-omit-frame-pointer"]
-    subprocess.check_call(["g++", *flags, "-o", out + ".tmp", SRC])
-    os.replace(out + ".tmp", out)
+    # a private temporary name: parallel test workers may build at once
+    tmp = f"{out}.{os.getpid()}.tmp"
+    subprocess.check_call(["g++", *flags, "-o", tmp, SRC])
+    os.replace(tmp, out)
     return out
 
 
