@@ -615,6 +615,12 @@ constexpr uint32_t kNoWorker = 0xffffffffu;
 #define KVR_PIPE_MATCH_UNROLL 8
 #endif
 constexpr int kPipeMatchUnroll = KVR_PIPE_MATCH_UNROLL;
+// ... in the matches taken from the shared item counter (most of them, on
+// the helper waves, whose registers are not the kernel's peak)
+#ifndef KVR_PIPE_ITEM_UNROLL
+#define KVR_PIPE_ITEM_UNROLL 8
+#endif
+constexpr int kPipeItemUnroll = KVR_PIPE_ITEM_UNROLL;
 constexpr uint32_t kSpinLimit = 1u << 24;
 #ifndef KVR_PIPE_WAVES
 #define KVR_PIPE_WAVES 8
@@ -699,14 +705,15 @@ __device__ __forceinline__ bool rf_may(const uint32_t* rf, int32_t t) {
 // sel = the active semispace, or -1 to read it from the header when the tree
 // is walked.  A match that would start at the root is settled by the root
 // filter when it rules out qn[0].
+template <int kU = kPipeMatchUnroll>
 __device__ __forceinline__ int32_t match_pipe(const Ptrs& P, int32_t sel, const uint32_t* rf, const int32_t* qn,
                                               int32_t Ln, int32_t h_old, int32_t ell, const PathRef& pr) {
   if ((ell == 0 || *pr.cnt > kPathMax) && !rf_may(rf, qn[0])) {
     if (lane_id() == 0) *pr.cnt = 0;
     return 0;
   }
-  if (sel < 0) return match_incremental_lazy<kPipeMatchUnroll>(P, qn, Ln, h_old, ell, pr);
-  return match_incremental<kPipeMatchUnroll>(P, (uint32_t)sel, qn, Ln, h_old, ell, pr);
+  if (sel < 0) return match_incremental_lazy<kU>(P, qn, Ln, h_old, ell, pr);
+  return match_incremental<kU>(P, (uint32_t)sel, qn, Ln, h_old, ell, pr);
 }
 
 // The next query's h on the workers other than the routed one (best) of
@@ -714,6 +721,7 @@ __device__ __forceinline__ int32_t match_pipe(const Ptrs& P, int32_t sel, const 
 // worker being evicted is left to the evicting wave, and every other is
 // claimed first (the evicting wave may have taken it).  Returns the number
 // of matches done (the caller publishes them).
+template <int kU>
 __device__ __forceinline__ uint32_t take_matches_pipe(const StepArgs& a, uint32_t r, uint32_t W, uint32_t cur,
                                                       uint32_t best, uint32_t prev, const int32_t* qn, int32_t Ln,
                                                       int32_t ell, const int32_t* h_cur, int32_t* h_next, PipeFlags* f,
@@ -733,7 +741,8 @@ __device__ __forceinline__ uint32_t take_matches_pipe(const StepArgs& a, uint32_
     const uint32_t taken = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((old >> w) & 1ull), 0);
     if (taken) continue;
     Ptrs Pw = worker_ptrs(a.ws, a.L, r, w);
-    count_mtok(mtok, w, match_pipe(Pw, -1, rootf + w * kRootFilterWords, qn, Ln, h_cur[w], ell, paths.of(w)),
+    count_mtok(mtok, w,
+               match_pipe<kU>(Pw, -1, rootf + w * kRootFilterWords, qn, Ln, h_cur[w], ell, paths.of(w)),
                &h_next[w]);
     ++mine;
   }
@@ -866,7 +875,7 @@ __global__ void __launch_bounds__(64 * kPipeWaves) step_kernel_pipe(StepArgs a) 
         const int32_t ell_r = ellp < Lp ? ellp : Lp;
         const int32_t ell = ell_r < Lprev ? ell_r : Lprev;
         const uint32_t prev = k > 1 ? (uint32_t)best_sh[cur] : 0u;
-        const uint32_t mine = take_matches_pipe(a, r, W, pc, (uint32_t)best_sh[pc], prev, qs, Lp, ell, h_sh[pc],
+        const uint32_t mine = take_matches_pipe<kPipeMatchUnroll>(a, r, W, pc, (uint32_t)best_sh[pc], prev, qs, Lp, ell, h_sh[pc],
                                                 h_sh[cur], &f, mtok_sh, rootf, paths);
         if (mine) add_rel(&f.matched, mine);
         clock_mark<PT>(&clk, KVR_PHASE_MATCH);
@@ -1207,7 +1216,7 @@ __global__ void __launch_bounds__(64 * kPipeWaves) step_kernel_pipe(StepArgs a) 
         const int32_t ell = ell_r < Lp ? ell_r : Lp;
         const uint32_t prev = k > 0 ? (uint32_t)best_sh[cur ^ 1u] : 0u;
         bool ok = true;
-        const uint32_t mine = take_matches_pipe(a, r, W, cur, best, prev, qn, Ln, ell, h_sh[cur], h_sh[cur ^ 1u], &f,
+        const uint32_t mine = take_matches_pipe<kPipeItemUnroll>(a, r, W, cur, best, prev, qn, Ln, ell, h_sh[cur], h_sh[cur ^ 1u], &f,
                                                 mtok_sh, rootf, paths);
         // this wave's matches, published at once
         add_rel(&f.matched, mine);
