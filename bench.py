@@ -204,6 +204,13 @@ def main() -> int:
                     help="approximate router: the router scores with matches on L-LRU trees of its own "
                          "(one per worker, the routed prompts) instead of the workers' caches")
     ap.add_argument("--router-tree-tokens", type=int, default=0, help="budget of each router tree (0 = B)")
+    ap.add_argument("--replicas", type=int, default=0,
+                    help="replicas of the workload's shape on the GPU (0 = the configuration's R); a "
+                         "scaling measurement, not a configuration's line")
+    ap.add_argument("--arena-words", type=int, default=0,
+                    help="arena words per semispace per (replica, worker) (0 = the library's default)")
+    ap.add_argument("--pending-capacity", type=int, default=0,
+                    help="completion records per (replica, worker) (0 = the library's default)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="CPU seconds per oracle thread on the timed window")
     ap.add_argument("--no-cpu", action="store_true")
@@ -235,6 +242,8 @@ def main() -> int:
 
     p = PRESETS[args.config]
     R, W, B = p["R"], p["W"], p["B"]
+    if args.replicas:
+        R = args.replicas
     t0 = time.perf_counter()
     stream = generate(dict(p["stream"], responses=True) if args.responses else p["stream"])
     log(f"{p['name']}: {stream.n} queries, {stream.tokens.size} tokens ({time.perf_counter() - t0:.1f} s)")
@@ -249,7 +258,8 @@ def main() -> int:
     sim = K.Simulator(R, W, B, stream.max_len, device="cuda:0", evict=evict, router=router,
                       cache_responses=int(args.responses), batch_size=args.beta,
                       router_tree=int(args.router_tree), router_tree_tokens=args.router_tree_tokens,
-                      phase_timers=int(args.phase_timers))
+                      phase_timers=int(args.phase_timers), arena_words=args.arena_words,
+                      **({"pending_capacity": args.pending_capacity} if args.pending_capacity else {}))
     ds = sim.upload(stream)
     out = sim.alloc_outputs(args.batch)
     torch.cuda.synchronize()
@@ -305,8 +315,8 @@ def main() -> int:
                  + 96 * nq)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     workload = p["name"]
-    default_run = (args.evict, args.router, args.responses, args.beta, args.router_tree) == \
-        ("rlt", "lbgr", False, 1, False)
+    default_run = (args.evict, args.router, args.responses, args.beta, args.router_tree, args.replicas,
+                   args.arena_words, args.pending_capacity) == ("rlt", "lbgr", False, 1, False, 0, 0, 0)
     traffic = load_traffic(workload, args.batch, args.warmup, args.steps) if default_run else None
     launch_s = kernel_ms * 1e-3 / args.steps
     line = {
@@ -325,7 +335,7 @@ def main() -> int:
         "config": {"workload": workload + ("_responses" if args.responses else ""), "eviction": args.evict,
                    "router": args.router, "cached_responses": bool(args.responses), "batch_size": args.beta,
                    "router_tree": bool(args.router_tree), "router_tree_tokens": args.router_tree_tokens or None,
-                   "replicas": R,
+                   "replicas": R, "arena_words": args.arena_words or None,
                    "workers": W, "cache_tokens": B,
                    "batch_queries": args.batch, "timed_queries": q - q0,
                    "first_timed_query": q0, "stream_queries": stream.n},
