@@ -1403,6 +1403,9 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
   pre.off = pre.coff = pre.mphase = 0;
   if (KVR_WAVE >= kPathMax && have_path && lane_id() < pc) pre = P.nodes[pr.node[lane_id()]];
   int32_t x = 0, d = 0, last = 0, lastcov = 0;
+  // the record of `last` (its length and child array: the marks below do
+  // not change them)
+  NodeRec lastrec = pre;
   while (d < h) {
     int32_t c;
     NodeRec nc;
@@ -1501,6 +1504,7 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
     d += cov;
     last = c;
     lastcov = cov;
+    lastrec = nc;
     x = c;
   }
   wave_mem_sync();  // the marks above are read again below
@@ -1510,14 +1514,11 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
     const int32_t nload = L - h;
     // ---- attachment point: end of `last`, splitting it if needed
     a = last;
-    if (h > 0) {
-      NodeRec nl = P.nodes[last];
-      if (lastcov < nl.len) {
-        a = split_node(P, s, last, lastcov);
-        if (a < 0) goto fail;
-        split = true;
-        ar = arena_of(P, s.arena_sel);
-      }
+    if (h > 0 && lastcov < lastrec.len) {
+      a = split_node(P, s, last, lastcov);
+      if (a < 0) goto fail;
+      split = true;
+      ar = arena_of(P, s.arena_sel);
     }
     // ---- rank of the new leaf in the leaf list: from another wave, which
     // computes it on the tree before this insertion while this one marks
@@ -1526,7 +1527,11 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
     const bool rank_helper = ia.rank != nullptr && have_path && !split;
     // a's child count, capacity and array offset, for the child added below
     int32_t a_known[3];
-    {
+    if (h > 0 && !split) {
+      a_known[0] = lastrec.nchild;
+      a_known[1] = lastrec.ccap;
+      a_known[2] = (int32_t)lastrec.coff;
+    } else {
       const NodeRec na = P.nodes[a];
       a_known[0] = na.nchild;
       a_known[1] = na.ccap;
