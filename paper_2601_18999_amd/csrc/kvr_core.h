@@ -341,8 +341,11 @@ __device__ int32_t arr_find(const int32_t* a, uint32_t n, int32_t v) {
 }
 
 // a[pos+1 .. n+1) = a[pos .. n); a[pos] = v.  Top-down rounds of eight
-// chunks: every load of a round completes before its stores are issued.
-__device__ void arr_insert(int32_t* a, uint32_t n, uint32_t pos, int32_t v) {
+// chunks: every load of a round completes before its stores are issued (a
+// round's stores and the next round's loads touch disjoint words).  With
+// fence = false the stores are left outstanding: the caller fences before
+// anything reads the array.
+__device__ void arr_insert(int32_t* a, uint32_t n, uint32_t pos, int32_t v, bool fence = true) {
   constexpr int kUnroll = 8;
   constexpr int64_t kSpan = (int64_t)kUnroll * KVR_WAVE;
   for (int64_t hi = (int64_t)n; hi > (int64_t)pos; hi -= kSpan) {
@@ -359,10 +362,10 @@ __device__ void arr_insert(int32_t* a, uint32_t n, uint32_t pos, int32_t v) {
       const int64_t k = lo + u * KVR_WAVE + lane_id();
       if (k < hi) a[k + 1] = x[u];
     }
-    wave_mem_sync();
+    if (fence) wave_mem_sync();
   }
   if (lane_id() == 0) a[pos] = v;
-  wave_mem_sync();
+  if (fence) wave_mem_sync();
 }
 
 // a[pos .. n-1) = a[pos+1 .. n), bottom-up rounds of eight chunks
@@ -644,9 +647,12 @@ __device__ __forceinline__ void node_free(const Ptrs& P, St& s, int32_t id) {
 
 // Add child c (first token tok) to node a.  When the caller has read a's
 // child count, capacity and array offset (in semispace sel_read), they are
-// used unless a collection has switched semispaces since.
+// used unless a collection has switched semispaces since.  With fence =
+// false the final stores are left outstanding (the caller fences before
+// anything reads them).
 __device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32_t tok, int32_t c,
-                                          const int32_t* known = nullptr, uint32_t sel_read = 0) {
+                                          const int32_t* known = nullptr, uint32_t sel_read = 0,
+                                          bool fence = true) {
   NodeRec na;
   if (known != nullptr && s.arena_sel == sel_read) {
     na.nchild = known[0];
@@ -659,6 +665,7 @@ __device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32
     int32_t ncap = na.ccap ? 2 * na.ccap : 2;
     uint32_t off;
     if (!arena_alloc(P, s, 2u * (uint32_t)ncap, true, off)) return false;
+    wave_mem_sync();
     na = P.nodes[a];  // the collector may have moved the old array
     int32_t* ar = arena_of(P, s.arena_sel);
     for (int32_t k = lane_id(); k < 2 * na.nchild; k += KVR_WAVE) ar[off + k] = ar[na.coff + k];
@@ -674,7 +681,7 @@ __device__ __forceinline__ bool child_add(const Ptrs& P, St& s, int32_t a, int32
     P.nodes[a].ccap = na.ccap;
     P.nodes[a].nchild = na.nchild + 1;
   }
-  wave_mem_sync();
+  if (fence) wave_mem_sync();
   return true;
 }
 
@@ -1539,6 +1546,11 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
     }
     const uint32_t a_sel = s.arena_sel;
     const bool replace = a != 0 && a_known[0] == 0;
+    // the free list's next entry, loaded before the stores below (an
+    // allocation after them would wait for them)
+    const int32_t fh = s.free_head;
+    uint32_t fh_next = 0;
+    if (fh >= 0) fh_next = P.nodes[fh].off;
     if (!rank_helper) pos = new_leaf_rank(P, s, ar, split ? last : a, 0, split ? 1 : 0, qs[h]);
     // ---- the new leaf node holding q[h, L)
     bool ranked = false;
@@ -1561,9 +1573,18 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
       pos = await_rank(ia);
       if (pos < 0) pos = new_leaf_rank(P, s, ar, a, 0, 0, qs[h]);
     }
-    l = node_alloc(P, s);
+    if (fh >= 0 && s.free_head == fh) {
+      l = fh;
+      s.free_head = (int32_t)fh_next;
+      s.nnodes += 1;
+    } else {
+      l = node_alloc(P, s);
+    }
     if (l < 0) goto fail;
-    {
+    // the new node, child entry and leaf-list entry: none of these stores is
+    // read again before the fence that ends this half (a collection fences
+    // first), so they are not fenced one by one
+    if (lane_id() == 0) {
       NodeRec nl;
       nl.parent = a;
       nl.off = eoff;
@@ -1573,9 +1594,9 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
       nl.ccap = 0;
       nl.mphase = 0;
       nl.ma = 0;
-      node_put(P, l, nl);
+      P.nodes[l] = nl;
     }
-    if (!child_add(P, s, a, qs[h], l, a_known, a_sel)) goto fail;
+    if (!child_add(P, s, a, qs[h], l, a_known, a_sel, false)) goto fail;
     ar = arena_of(P, s.arena_sel);
     if (pos < 0 || (uint32_t)pos > s.nleaves) {
       KVR_FAIL_CHECK(s, 4, pos, s.nleaves, a);
@@ -1583,9 +1604,8 @@ __device__ __forceinline__ uint32_t rlt_insert_front(const Ptrs& P, const Insert
     }
     if (replace) {
       if (lane_id() == 0) P.leaf[pos] = l;
-      wave_mem_sync();
     } else {
-      arr_insert(P.leaf, s.nleaves, (uint32_t)pos, l);
+      arr_insert(P.leaf, s.nleaves, (uint32_t)pos, l, false);
       s.nleaves += 1;
     }
     clock_mark<PT>(clk, KVR_PHASE_LOAD);
