@@ -626,6 +626,18 @@ constexpr uint32_t kSpinLimit = 1u << 24;
 #define KVR_PIPE_WAVES 8
 #endif
 constexpr uint32_t kPipeWaves = KVR_PIPE_WAVES;
+// Waves per workgroup for replicas of many workers: four more helpers for
+// the next query's matches, at a register cap of 168 VGPRs instead of 256
+// (the routing wave's loop state then partly lives in scratch).  Measured
+// faster at 32 workers and slower at 16, so used from 17 on.
+#ifndef KVR_PIPE_WAVES_WIDE
+#define KVR_PIPE_WAVES_WIDE 12
+#endif
+#ifndef KVR_PIPE_WIDE_WORKERS
+#define KVR_PIPE_WIDE_WORKERS 17
+#endif
+constexpr uint32_t kPipeWavesWide = KVR_PIPE_WAVES_WIDE;
+constexpr uint32_t kPipeWideWorkers = KVR_PIPE_WIDE_WORKERS;
 
 __device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -757,8 +769,9 @@ __device__ __forceinline__ uint32_t take_matches_pipe(const StepArgs& a, uint32_
   return mine;
 }
 
-template <bool PT>
-__global__ void __launch_bounds__(64 * kPipeWaves) step_kernel_pipe(StepArgs a) {
+// NW = waves per workgroup (the kernel itself takes it from blockDim).
+template <bool PT, uint32_t NW>
+__global__ void __launch_bounds__(64 * NW) step_kernel_pipe(StepArgs a) {
   // dynamic LDS: two query buffers, the draw words of two insertions, the
   // match paths, the staged candidate list
   extern __shared__ int32_t smem[];
@@ -802,13 +815,10 @@ __global__ void __launch_bounds__(64 * kPipeWaves) step_kernel_pipe(StepArgs a) 
   const uint32_t wave = threadIdx.x / KVR_WAVE;
   const uint32_t nwaves = blockDim.x / KVR_WAVE;
   const uint32_t nh = nwaves - 2;  // helper waves (>= 2)
-  // the last helper ranks new leaves; about half of the others compute the
-  // draw words first, the rest start on the next query's matches at once
-  // (both are due about when the front half of the insertion ends)
-#ifndef KVR_PIPE_DRAW_HELPERS
-#define KVR_PIPE_DRAW_HELPERS 3
-#endif
-  const uint32_t ndraw = nh > KVR_PIPE_DRAW_HELPERS ? KVR_PIPE_DRAW_HELPERS : nh - 1;
+  // the last helper ranks new leaves; half of the helpers compute the draw
+  // words first, the rest start on the next query's matches at once (both
+  // are due about when the front half of the insertion ends)
+  const uint32_t ndraw = nh / 2u < 16u ? nh / 2u : 16u;
   const uint32_t nd = ndraw * KVR_WAVE;  // drawing threads
   GlobalHdr* g = reinterpret_cast<GlobalHdr*>(a.ws + a.L.off_global);
   ReplicaHdr* rh = reinterpret_cast<ReplicaHdr*>(a.ws + a.L.off_rhdr) + r;
@@ -1381,10 +1391,20 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   const bool rt = a.L.has_router != 0, ba = a.L.beta > 1;
   if (a.pipe) {
     const size_t lds_p = step_lds_bytes_pipe(a.L.maxL, a.L.W, a.ucap, a.rcap);
-    if (a.C.phase_timers)
-      hipLaunchKernelGGL((step_kernel_pipe<true>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
-    else
-      hipLaunchKernelGGL((step_kernel_pipe<false>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
+    const bool wide = a.L.W >= kPipeWideWorkers;
+    if (a.C.phase_timers) {
+      if (wide)
+        hipLaunchKernelGGL((step_kernel_pipe<true, kPipeWavesWide>), dim3(a.L.R), dim3(64 * kPipeWavesWide), lds_p, st,
+                           a);
+      else
+        hipLaunchKernelGGL((step_kernel_pipe<true, kPipeWaves>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
+    } else {
+      if (wide)
+        hipLaunchKernelGGL((step_kernel_pipe<false, kPipeWavesWide>), dim3(a.L.R), dim3(64 * kPipeWavesWide), lds_p,
+                           st, a);
+      else
+        hipLaunchKernelGGL((step_kernel_pipe<false, kPipeWaves>), dim3(a.L.R), dim3(64 * kPipeWaves), lds_p, st, a);
+    }
   } else if (rt && ba)
     hipLaunchKernelGGL((step_kernel<true, true, false>), dim3(a.L.R), dim3(64 * waves), lds, st, a);
   else if (rt)
@@ -1443,8 +1463,11 @@ hipError_t launch_stats_into(char* ws, const Layout& L, uint64_t w0, uint32_t n,
   return hipGetLastError();
 }
 
-static const void* const kStepKernels[7] = {
-    reinterpret_cast<const void*>(step_kernel_pipe<false>), reinterpret_cast<const void*>(step_kernel_pipe<true>),
+static const void* const kStepKernels[9] = {
+    reinterpret_cast<const void*>(step_kernel_pipe<false, kPipeWaves>),
+    reinterpret_cast<const void*>(step_kernel_pipe<true, kPipeWaves>),
+    reinterpret_cast<const void*>(step_kernel_pipe<false, kPipeWavesWide>),
+    reinterpret_cast<const void*>(step_kernel_pipe<true, kPipeWavesWide>),
     reinterpret_cast<const void*>(step_kernel<false, false, false>),
     reinterpret_cast<const void*>(step_kernel<false, true, false>),
     reinterpret_cast<const void*>(step_kernel<true, false, false>),
