@@ -55,11 +55,25 @@ def test_collector_under_small_arena():
 
 
 def test_many_waves_per_replica():
-    """W = 24 workers: 16 waves per workgroup, several workers per wave."""
+    """W = 24 workers: the 12-wave form of the pipelined kernel (ten helpers,
+    several match items each per query)."""
     s = generate(small_spec(n=300, groups=12, prefix_len=(20, 120), suffix_len=(5, 40), vocab=200))
     W, B, R = 24, 500, 3
     res, stats = gpu_run(s, R, W, B)
     assert_parity(s, res, stats, W, B, range(R))
+
+
+@pytest.mark.parametrize("W", [16, 17, 31])
+def test_wave_form_threshold_small_vocab(W):
+    """Both sides of the worker count at which the pipelined kernel takes
+    its 12-wave form, on a small vocabulary (frequent splits, inexact early
+    matches and evictions into shared prefixes)."""
+    s = generate(small_spec(n=400, groups=8, prefix_len=(4, 60), suffix_len=(2, 40), vocab=6, seed=W))
+    B, R = int(max(s.max_len, 90)), 3
+    note(f"wave form threshold: W={W} B={B} n={s.n}")
+    res, stats = gpu_run(s, R, W, B, seed=W)
+    assert_parity(s, res, stats, W, B, range(R), seed=W)
+    assert sum(w["evictions"] for rr in stats for w in rr) > 0
 
 
 def test_config1_full_all_replicas_ragged_batches():
