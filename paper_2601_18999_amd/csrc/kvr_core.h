@@ -226,7 +226,6 @@ struct St {
   int32_t rnode, rlo, rhi;
   uint32_t rphase;
   uint32_t arena_sel, arena_top, nnodes;
-  uint64_t loads, evictions, forced, gc_runs;
   uint32_t err;
   // first failing internal check (diagnostics only)
   int32_t dbg_check;
@@ -261,10 +260,6 @@ __device__ __forceinline__ St load_st(const WorkerHdr* h) {
   s.arena_sel = h->arena_sel;
   s.arena_top = h->arena_top;
   s.nnodes = h->nnodes;
-  s.loads = h->loads;
-  s.evictions = h->evictions;
-  s.forced = h->forced_resets;
-  s.gc_runs = h->gc_runs;
   s.err = 0;
   s.dbg_check = 0;
   s.dbg_val[0] = s.dbg_val[1] = s.dbg_val[2] = 0;
@@ -288,10 +283,14 @@ __device__ __forceinline__ void store_st(WorkerHdr* h, const St& s) {
   h->arena_sel = s.arena_sel;
   h->arena_top = s.arena_top;
   h->nnodes = s.nnodes;
-  h->loads = s.loads;
-  h->evictions = s.evictions;
-  h->forced_resets = s.forced;
-  h->gc_runs = s.gc_runs;
+}
+
+// Add v to one of a worker's 64-bit event counters (loads, evictions,
+// forced resets, collections), which are kept out of St so that they do not
+// occupy registers through an insertion.  Lane 0; the result is not used,
+// so nothing waits for it.
+__device__ __forceinline__ void hdr_count(uint64_t* c, uint64_t v) {
+  if (lane_id() == 0) __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 __device__ __forceinline__ int32_t* arena_of(const Ptrs& P, uint32_t sel) {
@@ -594,7 +593,7 @@ __device__ __forceinline__ bool collect(const Ptrs& P, St& s) {
   if (top == ~0ull) return false;
   s.arena_sel ^= 1u;
   s.arena_top = (uint32_t)top;
-  s.gc_runs += 1;
+  hdr_count(&P.hdr->gc_runs, 1u);
   return true;
 }
 
@@ -1702,7 +1701,7 @@ __device__ __forceinline__ uint32_t rlt_insert_back(const Ptrs& P, const EvictJo
           staged = false;
         }
         s.phase += 1;
-        s.forced += 1;
+        hdr_count(&P.hdr->forced_resets, 1u);
         rebuild_U(P, s, l);
         reset_at = p;
         applied = true;
@@ -1790,8 +1789,8 @@ __device__ __forceinline__ uint32_t rlt_insert_back(const Ptrs& P, const EvictJo
       }
     }
     s.size = s.size + (uint32_t)nload - nev;
-    s.loads += (uint64_t)nload;
-    s.evictions += nev;
+    hdr_count(&P.hdr->loads, (uint64_t)nload);
+    hdr_count(&P.hdr->evictions, nev);
   }
   store_st(P.hdr, s);
   wave_mem_sync();
@@ -2211,8 +2210,8 @@ __device__ __forceinline__ uint32_t lru_insert(const Ptrs& P, const InsertArgs& 
       wave_mem_sync();
     }
     s.size = s.size + (uint32_t)nload - nev;
-    s.loads += (uint64_t)nload;
-    s.evictions += nev;
+    hdr_count(&P.hdr->loads, (uint64_t)nload);
+    hdr_count(&P.hdr->evictions, nev);
   }
   store_st(P.hdr, s);
   wave_mem_sync();
