@@ -53,3 +53,21 @@ def test_random_cases_match_the_oracle(seed):
         res, stats = gpu_run(s, c["R"], c["W"], c["B"], batch=c["batch"], max_len=c["maxL"],
                              evict=EVICT[c["evict"]], router=ROUTER[c["router"]], **extra)
         assert_parity(s, res, stats, c["W"], c["B"], range(c["R"]), evict=c["evict"], router=c["router"], **extra)
+
+
+@pytest.mark.parametrize("seed", [4041])
+def test_random_wide_cases_match_the_oracle(seed):
+    """As above, with every other case given 17 to 48 workers: the pipelined
+    kernel's 12-wave form under the same variety of shapes."""
+    rng = np.random.default_rng(seed)
+    for case in range(100):
+        s, c = make_case(rng, case)
+        if case % 2 == 0:
+            c["W"] = int(rng.choice([17, 20, 24, 32, 40, 48]))
+        note(f"wide seed {seed} case {case}: {c} max_len={s.max_len} n={s.n}")
+        extra = dict(batch_size=c["beta"]) if c["beta"] > 1 else {}
+        if c["rt"]:
+            extra.update(router_tree=1, router_tree_tokens=c["RB"])
+        res, stats = gpu_run(s, c["R"], c["W"], c["B"], batch=c["batch"], max_len=c["maxL"],
+                             evict=EVICT[c["evict"]], router=ROUTER[c["router"]], **extra)
+        assert_parity(s, res, stats, c["W"], c["B"], range(c["R"]), evict=c["evict"], router=c["router"], **extra)
